@@ -1,0 +1,285 @@
+"""Fork-aware decode attention benchmark (one GPU).
+
+A step is one fork-decode step of one attention layer: every sequence of the fork
+(main thread + 4 branches) appends its new K/V token and attends with one new query
+over the shared prefix and its own suffix.  The default workload is the long agent
+context: 32768-token shared prefix, 5 sequences, 40 query / 8 KV heads, head_dim 128,
+suffixes of 512..2048 tokens, 256 appended tokens per layer.  Layers are replicated
+so that the working set (>= 1 GiB) exceeds the 256 MB Infinity Cache and every step
+reads HBM; step i runs on replica i % R.  Inputs are resident in HBM before the timed
+region.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+MALL_BYTES = 256 << 20
+
+DESCRIPTIONS = {
+    "long": "long agent context: 32768-token shared prefix, 5 sequences (main + 4 branches), 40 q / 8 kv heads, "
+            "head_dim 128, suffixes 512..2048 tokens, one appended token per sequence per step",
+    "very-long": "very long context: 131072-token shared prefix, 5 sequences, 64 q / 8 kv heads, head_dim 128, "
+                 "suffixes 1024..4096 tokens",
+    "mid": "mid context: 8192-token shared prefix, 5 sequences, 32 q / 8 kv heads, head_dim 128, "
+           "suffixes 256..1024 tokens",
+    "tiny": "tiny: 512-token shared prefix, 5 sequences, 8 q / 2 kv heads, head_dim 64, suffixes 0..64 tokens",
+    "paged": "concurrent agents, paged: 16 tasks x 5 sequences, 32 q / 8 kv heads, head_dim 128, prefixes "
+             "4096..65536, suffixes 0..2048, 16-token pages from a permuted pool",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: 256 appends per replica)")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="long", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--replicas", type=int, default=0, help="layer replicas (0: enough for >= 1 GiB)")
+    ap.add_argument("--split", type=int, default=0, help="prefix tokens per work item (0: automatic)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-naive", action="store_true", help="skip the naive per-branch GPU baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: fork-aware decode attention is not sharded across GPUs here "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import oracle
+    from paper_2608_13667_amd import forkattn as fa
+    from paper_2608_13667_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    t0 = time.time()
+    w = W.make(args.workload)
+    spec = w.spec
+    log(f"[bench] generated {args.workload} in {time.time() - t0:.1f}s")
+    paged = spec.paged
+    appends = spec.steps > 0
+    if paged:
+        kvb = W.kv_bytes_paged(w)
+    else:
+        kvb = W.kv_bytes_contig(w)
+    R = args.replicas or max(1, math.ceil((1 << 30) / kvb["total"]))
+    K = args.steps if args.steps is not None else (256 * R if appends else max(200, 20 * R))
+    if appends and math.ceil(K / R) > spec.steps:
+        sys.exit(f"--steps {K} over {R} replicas exceeds the {spec.steps} appends each suffix buffer holds")
+
+    # device replicas of the layer (same values, distinct memory)
+    per_tok = 2 * spec.n_kv_heads * spec.head_dim * 2
+    if paged:
+        base = dict(q=dev(w.q), k_pool=dev(w.k_pool), v_pool=dev(w.v_pool),
+                    page_table=torch.from_numpy(w.page_table).cuda(), suffix_len=torch.from_numpy(w.suffix_len).cuda())
+        reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(R - 1)]
+
+        def mk_plan(share):
+            return fa.Plan.paged_plan(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.group_start, w.prefix_len,
+                                      w.page_table.shape[1], w.k_pool.shape[0], int(w.suffix_len.max()),
+                                      share_prefix=share, split_tokens=args.split)
+    else:
+        base = dict(q=dev(w.q), prefix_k=dev(w.prefix_k), prefix_v=dev(w.prefix_v), suffix_k=dev(w.suffix_k),
+                    suffix_v=dev(w.suffix_v), suffix_len=torch.from_numpy(w.suffix_len).cuda())
+        reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(R - 1)]
+
+        def mk_plan(share):
+            return fa.Plan.contig(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.n_branches, w.prefix_len,
+                                  w.suffix_cap, w.suffix_cap, share_prefix=share, split_tokens=args.split)
+    n_seq = w.q.shape[0]
+    out = torch.empty((n_seq, spec.n_q_heads, spec.head_dim), device="cuda")
+    lse = torch.empty((n_seq, spec.n_q_heads), device="cuda")
+    if appends:
+        step_q, step_k, step_v = dev(w.step_q), dev(w.step_k), dev(w.step_v)
+    len0 = torch.from_numpy(w.suffix_len).cuda()
+    log(f"[bench] {R} replicas x {kvb['total'] / 2**20:.1f} MiB, {K} timed steps")
+
+    def run(plan, i):
+        r = reps[i % R]
+        if paged:
+            plan.decode_paged(r["q"], r["k_pool"], r["v_pool"], r["page_table"], r["suffix_len"], out, lse)
+        elif appends:
+            j = i // R
+            plan.step(step_q[j], step_k[j], step_v[j], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"],
+                      r["suffix_len"], out, lse)
+        else:
+            plan.decode(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"], out, lse)
+
+    def reset():
+        for r in reps:
+            r["suffix_len"].copy_(len0)
+
+    def timed_loop(plan, n_steps, warmup):
+        reset()
+        for i in range(warmup):
+            run(plan, i)
+        torch.cuda.synchronize()
+        reset()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(n_steps):
+            run(plan, i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    def step_bytes(n_steps):
+        """Algorithmic K/V bytes of the timed loop: prefix once per step plus every suffix at its length."""
+        total = 0
+        sl0 = int(np.sum(w.suffix_len))
+        for i in range(n_steps):
+            extra = (i // R + 1) * n_seq if appends else 0
+            total += kvb["prefix"] + (sl0 + extra) * per_tok
+        return total
+
+    plan = mk_plan(True)
+    info = plan.info()
+    secs = timed_loop(plan, K, args.warmup)
+    assert plan.device_error() == 0
+    alg = step_bytes(K)
+    gbps = alg / secs / 1e9
+    log(f"[bench] fork-aware: {K / secs:.1f} steps/s, {secs / K * 1e6:.2f} us/step, {gbps:.0f} GB/s")
+
+    # dominant kernel alone: the partial-attention kernel, timed on the stream it runs on
+    n_slots = info.max_prefix_parts + info.n_suffix_parts
+    po = torch.empty((max(1, n_slots), n_seq, spec.n_q_heads, spec.head_dim), device="cuda")
+    pl = torch.empty((max(1, n_slots), n_seq, spec.n_q_heads), device="cuda")
+    reset()
+    kp = max(50, min(K, 400))
+    if not paged:
+        def part(i):
+            r = reps[i % R]
+            plan.partials(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"], po, pl)
+        for i in range(5):
+            part(i)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(kp):
+            part(i)
+        e1.record()
+        torch.cuda.synchronize()
+        k_secs = e0.elapsed_time(e1) * 1e-3 / kp
+        k_bytes = kvb["total"]
+        roof_name = "partials_kernel (prefix + suffix partial attention)"
+    else:
+        k_secs = secs / K
+        k_bytes = kvb["total"]
+        roof_name = "whole paged step (partials + merge)"
+    k_gbps = k_bytes / k_secs / 1e9
+
+    result_extra = {}
+    if not args.no_naive:
+        nplan = mk_plan(False)
+        kn = max(R, K // 4)
+        nsecs = timed_loop(nplan, kn, min(args.warmup, kn))
+        nalg = step_bytes(kn)
+        result_extra["naive_per_branch"] = {
+            "steps_per_s": kn / nsecs, "us_per_step": nsecs / kn * 1e6,
+            "effective_kv_gbps": nalg / nsecs / 1e9,
+            "requested_kv_gbps": (nalg + (kvb["naive"] - kvb["total"]) * kn) / nsecs / 1e9,
+            "prefix_reuse_speedup": (nsecs / kn) / (secs / K)}
+        log(f"[bench] naive: {kn / nsecs:.1f} steps/s, speed-up of sharing {(nsecs / kn) / (secs / K):.2f}x")
+        nplan.close()
+
+    # MALL-warm single-replica figure (labelled: the working set fits in the 256 MB Infinity Cache)
+    if not paged and kvb["total"] < MALL_BYTES:
+        r0 = reps[0]
+        reset()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        nw = min(K, 200)
+        e0.record()
+        for i in range(nw):
+            plan.decode(r0["q"], r0["prefix_k"], r0["prefix_v"], r0["suffix_k"], r0["suffix_v"], r0["suffix_len"], out,
+                        lse)
+        e1.record()
+        torch.cuda.synchronize()
+        ws = e0.elapsed_time(e1) * 1e-3
+        result_extra["mall_warm_single_replica"] = {"steps_per_s": nw / ws, "kv_gbps": kvb["total"] * nw / ws / 1e9}
+
+    # read-bandwidth probe for context: a 2 GiB fp32 sum
+    x = torch.empty(1 << 29, dtype=torch.float32, device="cuda").fill_(1.0)
+    torch.cuda.synchronize()
+    x.sum()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        x.sum()
+    e1.record()
+    torch.cuda.synchronize()
+    probe = 5 * x.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del x
+    result_extra["read_probe_gbps"] = probe
+
+    cpu = None
+    if not args.no_cpu:
+        oracle.build(force=False)
+        t_start = time.time()
+        n = 0
+        while True:
+            oracle.decode_workload(w)
+            n += 1
+            if time.time() - t_start >= args.cpu_seconds:
+                break
+        cs = time.time() - t_start
+        cpu = {"value": n / cs, "unit": "steps/s", "cores": oracle.threads(), "kind": "oracle",
+               "sample": f"{n} full decode steps (all {n_seq} x {spec.n_q_heads} rows) at the initial lengths, "
+                         f"fp64 on the host"}
+        log(f"[bench] cpu oracle: {n / cs:.3f} steps/s on {cpu['cores']} threads")
+
+    cfg = {"workload": DESCRIPTIONS[args.workload], "name": args.workload, "replicas": R,
+           "working_set_gib": R * kvb["total"] / 2**30, "split_tokens": info.split_tokens,
+           "suffix_split_tokens": info.suffix_split_tokens, "work_items": info.n_items}
+    res = {
+        "metric": "fork-decode attention steps/s and effective KV GB/s (% of HBM peak), 1 GPU",
+        "value": K / secs,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": secs / K * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": cfg,
+        "effective_kv_gbps": gbps,
+        "hbm_peak_frac": gbps / HBM_PEAK_GBPS,
+        "roofline": {"bound": "hbm", "kernel": roof_name, "achieved": k_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": k_gbps / HBM_PEAK_GBPS, "traffic": None, "avg_launch_us": k_secs * 1e6,
+                     "bytes_per_launch": k_bytes},
+        "cpu_baseline": cpu,
+    }
+    res.update(result_extra)
+    plan.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,248 @@
+/*
+ * forkattn.h -- C ABI of libforkattn.so: fork-aware decode attention on gfx950.
+ *
+ * The operation (paper, Sec. 3.2 Overview and Sec. 3.3 Forking via Trajectory
+ * Continuation).  When the main thread of a ReAct agent finishes its Thought,
+ * auxiliary branches are forked; every branch receives the same snapshot (the
+ * history H_t followed by the thought R_t) plus its own short continuation, and
+ * the key/value cache of the shared snapshot is reused by all decoding streams.
+ * The main thread and the branches then decode concurrently.  One decode step is
+ * therefore N sequences (main thread + branches), each with one new query token,
+ * all reading one shared prefix K/V and each reading its own suffix K/V.  The
+ * result for sequence b and query head h is ordinary scaled dot-product softmax
+ * attention of q[b][h] over [shared prefix ; suffix of b], using the K/V head
+ * h / G (G = n_q_heads / n_kv_heads).  Sharing the prefix is purely an
+ * optimisation: the library reads each prefix K/V tile from memory once and
+ * scores it against all N * G query rows of its K/V head, so the results equal
+ * the per-branch attention.  Branches never see each other's suffixes.
+ *
+ * Conventions for every call
+ *   - Tensors are caller-owned device memory passed as raw pointers.  bf16 means
+ *     IEEE bfloat16 bit patterns (uint16 in memory).  All layouts are dense,
+ *     row-major (C order), innermost dimension last.
+ *   - Pointers to K/V/q data must be 16-byte aligned (the kernels use 128-bit loads).
+ *   - Calls enqueue work on `stream` (a hipStream_t; NULL = the default stream)
+ *     and return without synchronising.  Results are valid once the stream has
+ *     reached that point.
+ *   - Calls never allocate, free or synchronise, except fka_plan_create_*
+ *     (allocates the plan's device workspace and work list, copies the work
+ *     list to the device), fka_plan_destroy (frees them) and
+ *     fka_plan_device_error (reads the device error word).
+ *   - A plan owns a workspace for partial results, so it may be used by one
+ *     stream at a time.  Plans are independent of each other.
+ *   - Arguments are validated on the host before anything is launched; on an
+ *     error nothing is enqueued, the call returns a negative fka_status and
+ *     fka_last_error() describes it.  Values that live on the device (suffix
+ *     lengths, page ids) are not visible to the host: the kernels clamp them to
+ *     the plan's bounds and record a violation in a device flag that
+ *     fka_plan_device_error() reports.
+ *   - Nothing crosses the ABI as an exception; the library never prints or exits.
+ */
+#ifndef FORKATTN_H
+#define FORKATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FKA_OK = 0,
+    FKA_ERR_INVALID_ARG = -1, /* null/misaligned pointer, inconsistent sizes */
+    FKA_ERR_UNSUPPORTED = -2, /* valid request outside what the kernels implement (head_dim, rows per KV head) */
+    FKA_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed; the HIP message is in fka_last_error() */
+    FKA_ERR_NOMEM = -4        /* device allocation failed in fka_plan_create_* */
+} fka_status;
+
+/* Version of this ABI (major * 10000 + minor * 100 + patch). */
+int fka_version(void);
+
+/* Message describing the last failed call on this thread ("" if none).  The
+ * string is owned by the library and valid until the next fka_* call on the
+ * same thread. */
+const char *fka_last_error(void);
+
+/* Attention head geometry shared by all sequences of a plan. */
+typedef struct {
+    int32_t n_q_heads;   /* Hq: query heads per sequence */
+    int32_t n_kv_heads;  /* Hkv: key/value heads; Hq % Hkv == 0, G = Hq / Hkv */
+    int32_t head_dim;    /* d: 64 or 128 */
+    float softmax_scale; /* scores are scale * q.k; 0 selects 1 / sqrt(head_dim) */
+} fka_heads;
+
+/* Opaque plan: the split of the work into tiles, a device work list and the
+ * workspace for partial (o, lse) results.  Built once per fork (the prefix
+ * length is fixed at the fork instant), reused for every decode step. */
+typedef struct fka_plan fka_plan;
+
+/* ---------------------------------------------------------------- contiguous KV */
+
+/* One fork: n_branches sequences (main thread + auxiliary branches) sharing a
+ * contiguous prefix of prefix_len tokens (Sec. 3.3). */
+typedef struct {
+    int32_t n_branches;     /* N >= 1 sequences sharing the prefix */
+    int32_t prefix_len;     /* Lp >= 0, fixed at the fork */
+    int32_t suffix_cap;     /* rows allocated per (branch, kv head) in the suffix buffers, >= 1 */
+    int32_t max_suffix_len; /* upper bound on suffix_len[b] over the plan's lifetime, <= suffix_cap */
+    int32_t share_prefix;   /* 1: fork-aware (prefix tiles read once for all N branches);
+                               0: naive baseline, every branch re-reads the prefix on its own */
+    int32_t split_tokens;   /* prefix tokens per work item (multiple of 128); 0 = automatic */
+} fka_contig_desc;
+
+/* Build a plan for the contiguous layout.  Allocates device memory (work list,
+ * workspace, error flag) on the current device.  *out receives the plan, owned by
+ * the caller until fka_plan_destroy.  Errors: FKA_ERR_INVALID_ARG (null pointer,
+ * non-positive sizes, Hq % Hkv != 0, max_suffix_len > suffix_cap),
+ * FKA_ERR_UNSUPPORTED (head_dim not 64/128, more than 64 rows N*G per KV head),
+ * FKA_ERR_NOMEM, FKA_ERR_HIP. */
+fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc *desc, fka_plan **out);
+
+/*
+ * One decode step: every branch's query attends to the shared prefix and to its
+ * own suffix (Sec. 3.2, Sec. 3.3).
+ *   q          bf16 [N][Hq][d]                  one new query token per branch
+ *   prefix_k   bf16 [Hkv][Lp][d]                shared prefix keys (prefix_v likewise)
+ *   suffix_k   bf16 [N][Hkv][suffix_cap][d]     per-branch suffix keys (suffix_v likewise)
+ *   suffix_len int32 [N] (device)               valid suffix rows per branch, 0..max_suffix_len
+ *   out        fp32 [N][Hq][d]                  attention output
+ *   out_lse    fp32 [N][Hq] or NULL             natural-log log-sum-exp of the scaled scores
+ * A sequence with no keys at all (Lp = 0 and suffix_len = 0) gets out = 0 and
+ * out_lse = -inf.  Suffix rows at or past suffix_len[b] are never read.
+ */
+fka_status fka_fork_decode(const fka_plan *plan, const void *q, const void *prefix_k, const void *prefix_v,
+                           const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *out,
+                           float *out_lse, void *stream);
+
+/*
+ * Append one token per branch (each branch decodes its own continuation,
+ * Sec. 3.2): for every branch b, K/V row suffix_len[b] of every KV head is set to
+ * k_new[b] / v_new[b] and suffix_len[b] is incremented.  A branch already at
+ * max_suffix_len is left unchanged and flagged (fka_plan_device_error).
+ *   k_new, v_new bf16 [N][Hkv][d];  suffix_k/suffix_v/suffix_len as in fka_fork_decode.
+ */
+fka_status fka_append_kv(const fka_plan *plan, const void *k_new, const void *v_new, void *suffix_k,
+                         void *suffix_v, int32_t *suffix_len, void *stream);
+
+/* Append (as fka_append_kv) and then decode (as fka_fork_decode) in one call:
+ * the decode sees the appended token. */
+fka_status fka_fork_step(const fka_plan *plan, const void *q, const void *k_new, const void *v_new,
+                         const void *prefix_k, const void *prefix_v, void *suffix_k, void *suffix_v,
+                         int32_t *suffix_len, float *out, float *out_lse, void *stream);
+
+/* ---------------------------------------------------------------------- paged KV */
+
+/* Several independent forks ("groups", e.g. one per agent task) whose K/V live in
+ * one pool of fixed-size pages.  Sequence i of group t shares the t-th prefix
+ * pages with the other sequences of its group. */
+typedef struct {
+    int32_t n_seqs;            /* S sequences over all groups */
+    int32_t n_groups;          /* T groups */
+    int32_t page_size;         /* tokens per page: 16 */
+    int32_t max_pages_per_seq; /* columns of page_table */
+    int32_t n_pool_pages;      /* pages in k_pool / v_pool; page ids outside [0, n_pool_pages) are never read */
+    int32_t max_suffix_len;    /* upper bound on suffix_len[i] over the plan's lifetime */
+    int32_t share_prefix;      /* 1 fork-aware, 0 naive baseline (as in fka_contig_desc) */
+    int32_t split_tokens;      /* prefix tokens per work item (multiple of 128); 0 = automatic */
+} fka_paged_desc;
+
+/*
+ * Build a plan for the paged layout.
+ *   host_group_start      host int32 [n_groups + 1]: sequences of group t are
+ *                         group_start[t] .. group_start[t+1]-1 (0 = start[0] <= ... = n_seqs)
+ *   host_group_prefix_len host int32 [n_groups]: shared prefix length of each group
+ * Page-table convention: logical position p < Lp of a sequence lives in page
+ * page_table[i][p / page_size] at slot p % page_size; suffix position u starts on a
+ * fresh page, at page index ceil(Lp / page_size) + u / page_size, slot u % page_size.
+ * The sequences of one group hold the same prefix page ids.
+ * Errors as fka_plan_create_contig; also FKA_ERR_INVALID_ARG when a group is empty,
+ * page_size is not 16, or a group's prefix plus max_suffix_len needs more than
+ * max_pages_per_seq pages.
+ */
+fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *desc, const int32_t *host_group_start,
+                                 const int32_t *host_group_prefix_len, fka_plan **out);
+
+/*
+ * One decode step over the paged pool.
+ *   q          bf16 [S][Hq][d]
+ *   k_pool     bf16 [n_pages][Hkv][page_size][d]   (v_pool likewise); a (page, head) block is contiguous
+ *   page_table int32 [S][max_pages_per_seq] (device)
+ *   suffix_len int32 [S] (device)
+ *   out fp32 [S][Hq][d]; out_lse fp32 [S][Hq] or NULL
+ * A page id outside [0, n_pool_pages) is not read: its rows count as zeros and
+ * flag 4 is raised in the plan's device error word.
+ */
+fka_status fka_fork_decode_paged(const fka_plan *plan, const void *q, const void *k_pool, const void *v_pool,
+                                 const int32_t *page_table, const int32_t *suffix_len, float *out, float *out_lse,
+                                 void *stream);
+
+/* Append one token per sequence into its pre-assigned suffix page (the caller
+ * assigns suffix pages in page_table ahead of time), then increment suffix_len.
+ *   k_new, v_new bf16 [S][Hkv][d]. */
+fka_status fka_append_kv_paged(const fka_plan *plan, const void *k_new, const void *v_new, void *k_pool,
+                               void *v_pool, const int32_t *page_table, int32_t *suffix_len, void *stream);
+
+/* Copy logical positions [0, out_len) of sequence `seq` out of the pool into
+ * contiguous k_out / v_out bf16 [Hkv][out_len][d] (bit copies).  out_len counts
+ * prefix plus suffix positions and must fit in max_pages_per_seq pages. */
+fka_status fka_gather_paged(const fka_plan *plan, int32_t seq, const void *k_pool, const void *v_pool,
+                            const int32_t *page_table, int32_t out_len, void *k_out, void *v_out, void *stream);
+
+/* -------------------------------------------------------------- stage entry points */
+
+/* Split geometry of a plan: the prefix of group t is cut into work items of
+ * split_tokens tokens (the last one shorter); suffixes into items of
+ * suffix_split_tokens.  max_prefix_parts is the largest number of prefix items of
+ * any group, n_suffix_parts the number of suffix items per sequence. */
+typedef struct {
+    int32_t split_tokens;
+    int32_t suffix_split_tokens;
+    int32_t max_prefix_parts;
+    int32_t n_suffix_parts;
+    int32_t n_items;           /* work items launched per decode */
+    size_t workspace_bytes;    /* device bytes held by the plan */
+} fka_plan_info;
+
+fka_status fka_plan_get_info(const fka_plan *plan, fka_plan_info *info);
+
+/*
+ * Partial results of the first stage (test hook; the decode calls write the same
+ * values to the plan's workspace).  Part p of sequence b (contiguous plans) is the
+ * attention of q[b] over prefix tokens [p*split, min((p+1)*split, Lp)) for
+ * p < max_prefix_parts, and over suffix tokens [s*ssplit, min((s+1)*ssplit, len_b))
+ * for p = max_prefix_parts + s.  o is normalised; lse is the natural-log
+ * log-sum-exp of the scaled scores; a part with no tokens is (0, -inf) or left
+ * unwritten when its range is empty on the device (suffix parts past len_b).
+ *   part_o   fp32 [max_prefix_parts + n_suffix_parts][N][Hq][d]
+ *   part_lse fp32 [max_prefix_parts + n_suffix_parts][N][Hq]
+ */
+fka_status fka_partials(const fka_plan *plan, const void *q, const void *prefix_k, const void *prefix_v,
+                        const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *part_o,
+                        float *part_lse, void *stream);
+
+/*
+ * Log-sum-exp merge of partial softmax results (combine attention over disjoint
+ * key sets into attention over their union):
+ *   M = max_p lse_p;  w_p = exp(lse_p - M);  o = sum_p w_p o_p / sum_p w_p;  lse = M + ln sum_p w_p
+ * Parts with lse = -inf have weight 0; all parts empty gives o = 0, lse = -inf.
+ *   part_o fp32 [n_parts][rows][d], part_lse fp32 [n_parts][rows]; out fp32 [rows][d];
+ *   out_lse fp32 [rows] or NULL.  d must be 64 or 128.
+ */
+fka_status fka_lse_merge(int32_t rows, int32_t n_parts, int32_t head_dim, const float *part_o,
+                         const float *part_lse, float *out, float *out_lse, void *stream);
+
+/* Read and clear the plan's device error flag (synchronises with the device):
+ * *flags receives a bit mask: 1 = a suffix length above max_suffix_len was
+ * clamped, 2 = an append found no room (length at max_suffix_len or no page),
+ * 4 = a page id outside the page table bounds was met. */
+fka_status fka_plan_device_error(const fka_plan *plan, int32_t *flags);
+
+/* Release a plan and its device memory.  NULL is ignored. */
+void fka_plan_destroy(fka_plan *plan);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FORKATTN_H */

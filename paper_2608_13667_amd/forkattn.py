@@ -1,0 +1,205 @@
+"""ctypes binding of libforkattn.so (include/forkattn.h), argument marshalling only.
+
+Every step of the computation runs in the library's HIP kernels; this module
+turns torch device tensors into raw pointers and the current torch stream into a
+hipStream_t.  Importing it fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libforkattn.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built: run paper_2608_13667_amd.build.build() "
+                      "(or __graft_entry__.build()) first")
+_lib = C.CDLL(LIB_PATH)
+
+FKA_OK, FKA_ERR_INVALID_ARG, FKA_ERR_UNSUPPORTED, FKA_ERR_HIP, FKA_ERR_NOMEM = 0, -1, -2, -3, -4
+ERR_SUFFIX_CLAMPED, ERR_APPEND_NO_ROOM, ERR_BAD_PAGE = 1, 2, 4
+
+
+class Heads(C.Structure):
+    _fields_ = [("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("softmax_scale", C.c_float)]
+
+
+class ContigDesc(C.Structure):
+    _fields_ = [("n_branches", C.c_int32), ("prefix_len", C.c_int32), ("suffix_cap", C.c_int32),
+                ("max_suffix_len", C.c_int32), ("share_prefix", C.c_int32), ("split_tokens", C.c_int32)]
+
+
+class PagedDesc(C.Structure):
+    _fields_ = [("n_seqs", C.c_int32), ("n_groups", C.c_int32), ("page_size", C.c_int32),
+                ("max_pages_per_seq", C.c_int32), ("n_pool_pages", C.c_int32), ("max_suffix_len", C.c_int32),
+                ("share_prefix", C.c_int32), ("split_tokens", C.c_int32)]
+
+
+class PlanInfo(C.Structure):
+    _fields_ = [("split_tokens", C.c_int32), ("suffix_split_tokens", C.c_int32), ("max_prefix_parts", C.c_int32),
+                ("n_suffix_parts", C.c_int32), ("n_items", C.c_int32), ("workspace_bytes", C.c_size_t)]
+
+
+_vp = C.c_void_p
+_sig = {
+    "fka_version": ([], C.c_int),
+    "fka_last_error": ([], C.c_char_p),
+    "fka_plan_create_contig": ([C.POINTER(Heads), C.POINTER(ContigDesc), C.POINTER(_vp)], C.c_int),
+    "fka_plan_create_paged": ([C.POINTER(Heads), C.POINTER(PagedDesc), _vp, _vp, C.POINTER(_vp)], C.c_int),
+    "fka_fork_decode": ([_vp] * 10, C.c_int),
+    "fka_append_kv": ([_vp] * 7, C.c_int),
+    "fka_fork_step": ([_vp] * 12, C.c_int),
+    "fka_fork_decode_paged": ([_vp] * 9, C.c_int),
+    "fka_append_kv_paged": ([_vp] * 8, C.c_int),
+    "fka_gather_paged": ([_vp, C.c_int32, _vp, _vp, _vp, C.c_int32, _vp, _vp, _vp], C.c_int),
+    "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
+    "fka_partials": ([_vp] * 10, C.c_int),
+    "fka_lse_merge": ([C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp], C.c_int),
+    "fka_plan_device_error": ([_vp, C.POINTER(C.c_int32)], C.c_int),
+    "fka_plan_destroy": ([_vp], None),
+}
+for _name, (_args, _res) in _sig.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+EXPORTED = tuple(_sig)
+
+
+class FkaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+def _check(status: int):
+    if status != FKA_OK:
+        raise FkaError(status, _lib.fka_last_error().decode())
+
+
+def last_error() -> str:
+    return _lib.fka_last_error().decode()
+
+
+def version() -> int:
+    return _lib.fka_version()
+
+
+def _p(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return _vp(t.data_ptr())
+
+
+def _stream(stream) -> _vp:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return _vp(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+class Plan:
+    """A fork plan: the work split and the device workspace (see fka_plan_create_*)."""
+
+    def __init__(self, handle: int, paged: bool, heads: Heads, n_seqs: int):
+        self._h = _vp(handle)
+        self.paged = paged
+        self.heads = heads
+        self.n_seqs = n_seqs
+
+    @classmethod
+    def contig(cls, n_q_heads, n_kv_heads, head_dim, n_branches, prefix_len, suffix_cap, max_suffix_len,
+               share_prefix=True, split_tokens=0, softmax_scale=0.0) -> "Plan":
+        h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
+        d = ContigDesc(n_branches, prefix_len, suffix_cap, max_suffix_len, int(bool(share_prefix)), split_tokens)
+        out = _vp()
+        _check(_lib.fka_plan_create_contig(C.byref(h), C.byref(d), C.byref(out)))
+        return cls(out.value, False, h, n_branches)
+
+    @classmethod
+    def paged_plan(cls, n_q_heads, n_kv_heads, head_dim, group_start, group_prefix_len, max_pages_per_seq,
+                   n_pool_pages, max_suffix_len, share_prefix=True, split_tokens=0, softmax_scale=0.0,
+                   page_size=16) -> "Plan":
+        import numpy as np
+        gs = np.ascontiguousarray(group_start, np.int32)
+        gl = np.ascontiguousarray(group_prefix_len, np.int32)
+        h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
+        d = PagedDesc(int(gs[-1]), len(gl), page_size, max_pages_per_seq, n_pool_pages, max_suffix_len,
+                      int(bool(share_prefix)), split_tokens)
+        out = _vp()
+        _check(_lib.fka_plan_create_paged(C.byref(h), C.byref(d), gs.ctypes.data_as(_vp), gl.ctypes.data_as(_vp),
+                                          C.byref(out)))
+        return cls(out.value, True, h, int(gs[-1]))
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            _lib.fka_plan_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def handle(self):
+        return self._h
+
+    def info(self) -> PlanInfo:
+        i = PlanInfo()
+        _check(_lib.fka_plan_get_info(self._h, C.byref(i)))
+        return i
+
+    def device_error(self) -> int:
+        v = C.c_int32(0)
+        _check(_lib.fka_plan_device_error(self._h, C.byref(v)))
+        return v.value
+
+    # ---- contiguous
+    def decode(self, q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, out, out_lse=None, stream=None):
+        _check(_lib.fka_fork_decode(self._h, _p(q), _p(prefix_k), _p(prefix_v), _p(suffix_k), _p(suffix_v),
+                                    _p(suffix_len), _p(out), _p(out_lse), _stream(stream)))
+
+    def append(self, k_new, v_new, suffix_k, suffix_v, suffix_len, stream=None):
+        _check(_lib.fka_append_kv(self._h, _p(k_new), _p(v_new), _p(suffix_k), _p(suffix_v), _p(suffix_len),
+                                  _stream(stream)))
+
+    def step(self, q, k_new, v_new, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, out, out_lse=None,
+             stream=None):
+        _check(_lib.fka_fork_step(self._h, _p(q), _p(k_new), _p(v_new), _p(prefix_k), _p(prefix_v), _p(suffix_k),
+                                  _p(suffix_v), _p(suffix_len), _p(out), _p(out_lse), _stream(stream)))
+
+    def partials(self, q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, part_o, part_lse, stream=None):
+        _check(_lib.fka_partials(self._h, _p(q), _p(prefix_k), _p(prefix_v), _p(suffix_k), _p(suffix_v),
+                                 _p(suffix_len), _p(part_o), _p(part_lse), _stream(stream)))
+
+    # ---- paged
+    def decode_paged(self, q, k_pool, v_pool, page_table, suffix_len, out, out_lse=None, stream=None):
+        _check(_lib.fka_fork_decode_paged(self._h, _p(q), _p(k_pool), _p(v_pool), _p(page_table), _p(suffix_len),
+                                          _p(out), _p(out_lse), _stream(stream)))
+
+    def append_paged(self, k_new, v_new, k_pool, v_pool, page_table, suffix_len, stream=None):
+        _check(_lib.fka_append_kv_paged(self._h, _p(k_new), _p(v_new), _p(k_pool), _p(v_pool), _p(page_table),
+                                        _p(suffix_len), _stream(stream)))
+
+    def gather_paged(self, seq, k_pool, v_pool, page_table, out_len, k_out, v_out, stream=None):
+        _check(_lib.fka_gather_paged(self._h, int(seq), _p(k_pool), _p(v_pool), _p(page_table), int(out_len),
+                                     _p(k_out), _p(v_out), _stream(stream)))
+
+
+def lse_merge(part_o, part_lse, out, out_lse=None, stream=None):
+    """part_o fp32 [P][R][d], part_lse fp32 [P][R] -> out fp32 [R][d], out_lse fp32 [R]."""
+    P, R, d = part_o.shape
+    _check(_lib.fka_lse_merge(R, P, d, _p(part_o), _p(part_lse), _p(out), _p(out_lse), _stream(stream)))
+
+
+def raw_call(name: str, *args) -> int:
+    """Call an exported function with raw ctypes arguments; returns its status (for ABI tests)."""
+    return getattr(_lib, name)(*args)

@@ -308,7 +308,8 @@ def make_paged(spec: Spec) -> PagedWorkload:
     n_suf = [-(-(int(L) + spec.page_headroom) // P) for L in suffix_len]
     n_pages = sum(n_pre) + sum(n_suf)
     perm = np.random.Generator(np.random.PCG64(streams[_S_PAGES])).permutation(n_pages).astype(np.int32)
-    max_pages = max(n_pre[t] + n_suf[t * B + b] for t in range(T) for b in range(B))
+    # wide enough for any task's prefix plus the longest suffix (plus headroom) of any sequence
+    max_pages = max(n_pre) + max(n_suf)
     page_table = np.full((S, max(1, max_pages)), -1, np.int32)
     suffix_pages = np.full((S, max(1, max(n_suf) if n_suf else 1)), -1, np.int32)
     cursor = 0

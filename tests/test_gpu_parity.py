@@ -1,0 +1,342 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle on the same seeded inputs.
+
+Bar (tests/gates.py): max-abs error <= 2e-3 and max-rel error (floored at the output
+RMS) <= 1e-2 on the attention output; |lse error| <= 2e-3; bit-exact for gathers.
+All five workloads run at their full sizes with every output row checked.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13667_amd import workloads as W
+from tests import gates
+from tests.gpu_util import (contig_plan, dev_bf16, dev_i32, paged_plan, run_contig, run_paged, to_dev_contig,
+                            to_dev_paged)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fa():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_13667_amd import forkattn
+    return forkattn
+
+
+def _check_contig(fa, w, **plan_kw):
+    ref, ref_lse = oracle.decode_workload(w)
+    plan = contig_plan(fa, w, **plan_kw)
+    out, lse = run_contig(plan, to_dev_contig(w), w.spec.n_q_heads)
+    m = gates.assert_gates(out, ref, what=w.spec.name)
+    gates.assert_lse(lse, ref_lse, what=w.spec.name)
+    assert plan.device_error() == 0
+    return m
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny-unscaled", "mid", "long", "very-long"])
+def test_config_parity(fa, name):
+    spec = W.CONFIGS[name].replace(steps=0)
+    print(f"[parity] {name}", flush=True)
+    m = _check_contig(fa, W.make(spec))
+    print(f"[parity] {name} {m}", flush=True)
+
+
+def test_paged_config_parity(fa):
+    w = W.make("paged")
+    print("[parity] paged", flush=True)
+    ref, ref_lse = oracle.decode_workload(w)
+    plan = paged_plan(fa, w)
+    out, lse = run_paged(plan, to_dev_paged(w))
+    m = gates.assert_gates(out, ref, what="paged")
+    gates.assert_lse(lse, ref_lse, what="paged")
+    assert plan.device_error() == 0
+    print(f"[parity] paged {m}", flush=True)
+
+
+def test_long_decode_loop_with_appends(fa):
+    """Long agent context: 256 steps, each appending one token per branch then attending."""
+    w = W.make("long")
+    s = w.spec
+    plan = contig_plan(fa, w)
+    dv = to_dev_contig(w)
+    N, Hq, d = w.q.shape
+    out = torch.empty((N, Hq, d), device="cuda")
+    lse = torch.empty((N, Hq), device="cuda")
+    kn, vn, qn = dev_bf16(w.step_k), dev_bf16(w.step_v), dev_bf16(w.step_q)
+    check = {0, 1, 127, 255}
+    for t in range(s.steps):
+        plan.step(qn[t], kn[t], vn[t], dv["prefix_k"], dv["prefix_v"], dv["suffix_k"], dv["suffix_v"],
+                  dv["suffix_len"], out, lse)
+        # host mirror of the append for the oracle
+        for b in range(N):
+            L = int(w.suffix_len[b])
+            w.suffix_k[b, :, L] = w.step_k[t, b]
+            w.suffix_v[b, :, L] = w.step_v[t, b]
+            w.suffix_len[b] = L + 1
+        if t in check:
+            torch.cuda.synchronize()
+            ref, ref_lse = oracle.decode_contig(w.step_q[t], w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v,
+                                                w.suffix_len, s.softmax_scale)
+            print(f"[parity] long step {t}", flush=True)
+            gates.assert_gates(out.cpu().numpy(), ref, what=f"long step {t}")
+            gates.assert_lse(lse.cpu().numpy(), ref_lse, what=f"long step {t}")
+    assert np.array_equal(dv["suffix_len"].cpu().numpy(), w.suffix_len)
+    # the device suffix buffers hold exactly the appended rows
+    L0 = w.suffix_len - s.steps
+    for b in range(N):
+        got = dv["suffix_k"][b, :, L0[b]:w.suffix_len[b]].view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, w.suffix_k[b, :, L0[b]:w.suffix_len[b]])
+    assert plan.device_error() == 0
+
+
+@pytest.mark.parametrize("name", ["mid", "tiny-unscaled"])
+def test_naive_per_branch_baseline(fa, name):
+    _check_contig(fa, W.make(name), share_prefix=False)
+
+
+@pytest.mark.parametrize("case", [
+    dict(prefix_len=0),                                   # no shared prefix at all
+    dict(suffix_range=(0, 0)),                            # every suffix empty
+    dict(prefix_len=1000),                                # prefix not a multiple of the tile
+    dict(prefix_len=1, suffix_range=(0, 3)),              # one prefix token
+    dict(n_branches=1),                                   # a single sequence (plain decode)
+    dict(n_branches=8, n_q_heads=64, n_kv_heads=8),       # 64 rows per KV head (4 row tiles)
+    dict(n_branches=3, n_q_heads=48, n_kv_heads=8),       # 18 rows (2 row tiles, ragged)
+    dict(n_q_heads=8, n_kv_heads=8),                      # G = 1 (multi-head attention)
+    dict(n_q_heads=24, n_kv_heads=8, n_branches=2),       # 6 rows per KV head
+])
+def test_edge_cases(fa, case):
+    spec = W.CONFIGS["mid"].replace(prefix_len=2048, suffix_range=(0, 300), seed=77).replace(**case)
+    print(f"[edge] {case}", flush=True)
+    _check_contig(fa, W.make(spec))
+
+
+@pytest.mark.parametrize("split", [128, 384, 4096])
+def test_explicit_split_sizes(fa, split):
+    spec = W.CONFIGS["mid"].replace(prefix_len=3000, seed=78)
+    _check_contig(fa, W.make(spec), split_tokens=split)
+
+
+def test_head_dim_64_full_rows(fa):
+    spec = W.CONFIGS["tiny-unscaled"].replace(prefix_len=5000, suffix_range=(100, 700), seed=79)
+    _check_contig(fa, W.make(spec))
+
+
+def test_all_sequences_empty(fa):
+    spec = W.CONFIGS["tiny"].replace(prefix_len=0, suffix_range=(0, 0))
+    w = W.make(spec)
+    plan = contig_plan(fa, w)
+    out, lse = run_contig(plan, to_dev_contig(w), spec.n_q_heads)
+    assert np.array_equal(out, np.zeros_like(out)) and np.all(np.isneginf(lse))
+
+
+def test_identical_queries_empty_suffixes_identical_outputs(fa):
+    w = W.make("mid", suffix_range=(0, 0))
+    w.q[:] = w.q[0:1]
+    out, lse = run_contig(contig_plan(fa, w), to_dev_contig(w), 32)
+    for b in range(1, w.n_branches):
+        assert np.array_equal(out[b], out[0]) and np.array_equal(lse[b], lse[0])
+
+
+def test_branch_isolation(fa):
+    w = W.make("mid")
+    plan = contig_plan(fa, w)
+    out, _ = run_contig(plan, to_dev_contig(w), 32)
+    rng = np.random.default_rng(3)
+    w.q[2] = W.bf16_bits(rng.standard_normal(w.q[2].shape).astype(np.float32))
+    w.suffix_v[2, :, :w.suffix_len[2]] = W.bf16_bits(
+        rng.standard_normal(w.suffix_v[2, :, :w.suffix_len[2]].shape).astype(np.float32))
+    out2, _ = run_contig(plan, to_dev_contig(w), 32)
+    for b in range(w.n_branches):
+        if b != 2:
+            assert np.array_equal(out2[b], out[b])
+
+
+def test_deterministic(fa):
+    w = W.make("mid")
+    plan = contig_plan(fa, w)
+    dv = to_dev_contig(w)
+    a, al = run_contig(plan, dv, 32)
+    b, bl = run_contig(plan, dv, 32)
+    assert np.array_equal(a, b) and np.array_equal(al, bl)
+
+
+def test_partials_stage(fa):
+    """Each first-stage partial equals the oracle's attention over that part's key range."""
+    w = W.make("mid", prefix_len=5000, seed=81)
+    plan = contig_plan(fa, w, split_tokens=1024)
+    info = plan.info()
+    dv = to_dev_contig(w)
+    N, Hq, d = w.q.shape
+    slots = info.max_prefix_parts + info.n_suffix_parts
+    po = torch.full((slots, N, Hq, d), float("nan"), device="cuda")
+    pl = torch.full((slots, N, Hq), float("nan"), device="cuda")
+    plan.partials(dv["q"], dv["prefix_k"], dv["prefix_v"], dv["suffix_k"], dv["suffix_v"], dv["suffix_len"], po, pl)
+    torch.cuda.synchronize()
+    po, pl = po.cpu().numpy(), pl.cpu().numpy()
+    sp, ss = info.split_tokens, info.suffix_split_tokens
+    assert info.max_prefix_parts == -(-5000 // sp)
+    for p in range(info.max_prefix_parts):
+        ref, ref_lse = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, w.suffix_len,
+                                            w.spec.softmax_scale, prefix_range=(p * sp, (p + 1) * sp),
+                                            suffix_range=(0, 0))
+        gates.assert_gates(po[p], ref, what=f"prefix part {p}")
+        gates.assert_lse(pl[p], ref_lse, what=f"prefix part {p}")
+    for s in range(info.n_suffix_parts):
+        ref, ref_lse = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, w.suffix_len,
+                                            w.spec.softmax_scale, prefix_range=(0, 0),
+                                            suffix_range=(s * ss, (s + 1) * ss))
+        for b in range(N):
+            if s * ss < w.suffix_len[b]:
+                gates.assert_gates(po[info.max_prefix_parts + s, b], ref[b], what=f"suffix part {s} branch {b}")
+                gates.assert_lse(pl[info.max_prefix_parts + s, b], ref_lse[b], what=f"suffix part {s}")
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_lse_merge_stage(fa, d):
+    rng = np.random.default_rng(d)
+    P, R = 13, 37
+    o = rng.standard_normal((P, R, d)).astype(np.float32)
+    l = rng.uniform(-30, 30, (P, R)).astype(np.float32)
+    l[rng.random((P, R)) < 0.3] = -np.inf
+    l[:, 5] = -np.inf           # a row with no keys at all
+    o[:, 5] = 0
+    out = torch.empty((R, d), device="cuda")
+    lse = torch.empty((R,), device="cuda")
+    fa.lse_merge(torch.from_numpy(o).cuda(), torch.from_numpy(l).cuda(), out, lse)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.lse_merge(o.transpose(1, 0, 2).astype(np.float64), l.T.astype(np.float64))
+    np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=1e-5, atol=1e-5)
+    got_lse = lse.cpu().numpy()
+    assert np.isneginf(got_lse[5]) and np.array_equal(out.cpu().numpy()[5], np.zeros(d, np.float32))
+    fin = np.isfinite(ref_lse)
+    np.testing.assert_allclose(got_lse[fin], ref_lse[fin], rtol=1e-6, atol=1e-5)
+
+
+def _small_paged(headroom=0, seed=90):
+    return W.make(W.CONFIGS["paged"].replace(n_tasks=5, prefix_range=(1, 3000), suffix_range=(0, 400),
+                                             page_headroom=headroom, seed=seed))
+
+
+def test_paged_small_parity_and_naive(fa):
+    w = _small_paged()
+    ref, ref_lse = oracle.decode_workload(w)
+    dv = to_dev_paged(w)
+    for share in (True, False):
+        out, lse = run_paged(paged_plan(fa, w, share_prefix=share), dv)
+        gates.assert_gates(out, ref, what=f"paged share={share}")
+        gates.assert_lse(lse, ref_lse, what=f"paged share={share}")
+
+
+def test_paged_equals_contiguous_on_same_data(fa):
+    """The paged path and the contiguous path agree on one task's gathered data."""
+    w = _small_paged(seed=91)
+    dv = to_dev_paged(w)
+    outp, _ = run_paged(paged_plan(fa, w), dv)
+    t = 2
+    s0, s1 = int(w.group_start[t]), int(w.group_start[t + 1])
+    Lp = int(w.prefix_len[t])
+    Ls = w.suffix_len[s0:s1]
+    cap = max(1, int(Ls.max()))
+    K = np.full((s1 - s0, w.spec.n_kv_heads, cap, w.spec.head_dim), W.BF16_NAN, np.uint16)
+    V = K.copy()
+    pk = pv = None
+    for j, i in enumerate(range(s0, s1)):
+        ko, vo = oracle.gather_paged(w.k_pool, w.v_pool, w.page_table, i, Lp, int(Ls[j]))
+        pk, pv = ko[:, :Lp], vo[:, :Lp]
+        K[j, :, :Ls[j]] = ko[:, Lp:]
+        V[j, :, :Ls[j]] = vo[:, Lp:]
+    cw = W.ContigWorkload(w.spec.replace(paged=False, n_branches=s1 - s0), w.q[s0:s1], np.ascontiguousarray(pk),
+                          np.ascontiguousarray(pv), K, V, Ls.astype(np.int32))
+    outc, _ = run_contig(contig_plan(fa, cw), to_dev_contig(cw), w.spec.n_q_heads)
+    gates.assert_gates(outp[s0:s1], outc.astype(np.float64), what="paged vs contiguous")
+
+
+def test_gather_bit_exact(fa):
+    w = _small_paged(seed=92)
+    plan = paged_plan(fa, w)
+    dv = to_dev_paged(w)
+    for i in range(w.n_seqs):
+        t = i // w.spec.n_branches
+        Lp, Ls = int(w.prefix_len[t]), int(w.suffix_len[i])
+        L = Lp + Ls
+        ko = torch.empty((w.spec.n_kv_heads, max(L, 1), w.spec.head_dim), dtype=torch.bfloat16, device="cuda")
+        vo = torch.empty_like(ko)
+        plan.gather_paged(i, dv["k_pool"], dv["v_pool"], dv["page_table"], L, ko, vo)
+        torch.cuda.synchronize()
+        rk, rv = oracle.gather_paged(w.k_pool, w.v_pool, w.page_table, i, Lp, Ls)
+        assert np.array_equal(ko.view(torch.int16).cpu().numpy().view(np.uint16)[:, :L], rk)
+        assert np.array_equal(vo.view(torch.int16).cpu().numpy().view(np.uint16)[:, :L], rv)
+
+
+def test_gather_bit_exact_full_paged_sample(fa):
+    w = W.make("paged")
+    plan = paged_plan(fa, w)
+    dv = to_dev_paged(w)
+    for i in (0, 7, 41, 79):
+        t = i // w.spec.n_branches
+        Lp, Ls = int(w.prefix_len[t]), int(w.suffix_len[i])
+        L = Lp + Ls
+        ko = torch.empty((w.spec.n_kv_heads, L, w.spec.head_dim), dtype=torch.bfloat16, device="cuda")
+        vo = torch.empty_like(ko)
+        plan.gather_paged(i, dv["k_pool"], dv["v_pool"], dv["page_table"], L, ko, vo)
+        torch.cuda.synchronize()
+        rk, rv = oracle.gather_paged(w.k_pool, w.v_pool, w.page_table, i, Lp, Ls)
+        assert np.array_equal(ko.view(torch.int16).cpu().numpy().view(np.uint16), rk)
+        assert np.array_equal(vo.view(torch.int16).cpu().numpy().view(np.uint16), rv)
+
+
+def test_paged_append_then_decode(fa):
+    w = _small_paged(headroom=40, seed=93)
+    plan = paged_plan(fa, w)
+    dv = to_dev_paged(w)
+    rng = np.random.default_rng(4)
+    S, Hkv, d = w.n_seqs, w.spec.n_kv_heads, w.spec.head_dim
+    P = w.spec.page_size
+    for step in range(20):
+        kn = W.bf16_bits(rng.standard_normal((S, Hkv, d)).astype(np.float32))
+        vn = W.bf16_bits(rng.standard_normal((S, Hkv, d)).astype(np.float32))
+        plan.append_paged(dev_bf16(kn), dev_bf16(vn), dv["k_pool"], dv["v_pool"], dv["page_table"], dv["suffix_len"])
+        for i in range(S):
+            t = i // w.spec.n_branches
+            u = int(w.suffix_len[i])
+            page = w.page_table[i, -(-int(w.prefix_len[t]) // P) + u // P]
+            w.k_pool[page, :, u % P] = kn[i]
+            w.v_pool[page, :, u % P] = vn[i]
+            w.suffix_len[i] = u + 1
+    torch.cuda.synchronize()
+    assert np.array_equal(dv["suffix_len"].cpu().numpy(), w.suffix_len)
+    assert np.array_equal(dv["k_pool"].view(torch.int16).cpu().numpy().view(np.uint16), w.k_pool)
+    ref, _ = oracle.decode_workload(w)
+    out, _ = run_paged(plan, dv)
+    gates.assert_gates(out, ref, what="paged after appends")
+    assert plan.device_error() == 0
+
+
+def test_append_past_capacity_is_flagged_not_written(fa):
+    w = W.make("tiny", suffix_range=(0, 8))
+    plan = contig_plan(fa, w, max_suffix_len=8)
+    dv = to_dev_contig(w)
+    dv["suffix_len"].fill_(8)
+    before = dv["suffix_k"].clone()
+    kn = torch.zeros((w.n_branches, 2, 64), dtype=torch.bfloat16, device="cuda")
+    plan.append(kn, kn, dv["suffix_k"], dv["suffix_v"], dv["suffix_len"])
+    torch.cuda.synchronize()
+    assert torch.equal(dv["suffix_len"].cpu(), torch.full((w.n_branches,), 8, dtype=torch.int32))
+    assert torch.equal(before.view(torch.int16), dv["suffix_k"].view(torch.int16))
+    assert plan.device_error() & 2
+    assert plan.device_error() == 0   # reading clears the flag
+
+
+def test_suffix_length_above_bound_is_clamped_and_flagged(fa):
+    w = W.make("tiny", suffix_range=(10, 20))
+    plan = contig_plan(fa, w, max_suffix_len=12)
+    dv = to_dev_contig(w)
+    dv["suffix_len"].fill_(40)
+    out, _ = run_contig(plan, dv, 8)
+    w.suffix_len[:] = 12
+    ref, _ = oracle.decode_workload(w)
+    gates.assert_gates(out, ref, what="clamped lengths")
+    assert plan.device_error() & 1
