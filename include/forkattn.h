@@ -125,8 +125,12 @@ fka_status fka_fork_decode(const fka_plan *plan, const void *q, const void *pref
 fka_status fka_append_kv(const fka_plan *plan, const void *k_new, const void *v_new, void *suffix_k,
                          void *suffix_v, int32_t *suffix_len, void *stream);
 
-/* Append (as fka_append_kv) and then decode (as fka_fork_decode) in one call:
- * the decode sees the appended token. */
+/* Append (as fka_append_kv) and then decode (as fka_fork_decode), fused into two
+ * kernel launches: the merge stage scores each branch's new K/V row straight from
+ * k_new / v_new as one more part of the log-sum-exp merge, then stores it at
+ * suffix_len[b] and increments suffix_len[b].  The caches and lengths end up as
+ * after fka_append_kv; the outputs equal fka_append_kv + fka_fork_decode up to the
+ * order of the fp32 sums. */
 fka_status fka_fork_step(const fka_plan *plan, const void *q, const void *k_new, const void *v_new,
                          const void *prefix_k, const void *prefix_v, void *suffix_k, void *suffix_v,
                          int32_t *suffix_len, float *out, float *out_lse, void *stream);
@@ -182,6 +186,11 @@ fka_status fka_fork_decode_paged(const fka_plan *plan, const void *q, const void
  *   k_new, v_new bf16 [S][Hkv][d]. */
 fka_status fka_append_kv_paged(const fka_plan *plan, const void *k_new, const void *v_new, void *k_pool,
                                void *v_pool, const int32_t *page_table, int32_t *suffix_len, void *stream);
+
+/* Fused append + decode over the paged pool (as fka_fork_step). */
+fka_status fka_fork_step_paged(const fka_plan *plan, const void *q, const void *k_new, const void *v_new,
+                               void *k_pool, void *v_pool, const int32_t *page_table, int32_t *suffix_len,
+                               float *out, float *out_lse, void *stream);
 
 /* Copy logical positions [0, out_len) of sequence `seq` out of the pool into
  * contiguous k_out / v_out bf16 [Hkv][out_len][d] (bit copies).  out_len counts

@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libforkattn.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "kernels.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "kernels.hip", "partials.hip")]
 ARCH = "gfx950"
 
 
@@ -45,6 +45,9 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + ["-o", tmp]
     subprocess.check_call(cmd)
+    # refuse a library with unresolved symbols (e.g. a kernel whose launch stub was not emitted)
+    import ctypes
+    ctypes.CDLL(tmp, mode=os.RTLD_NOW | os.RTLD_LOCAL)
     os.replace(tmp, LIB)
     return LIB
 

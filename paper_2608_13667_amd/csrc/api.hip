@@ -37,6 +37,11 @@ struct fka_plan {
     int32_t *seq_prefix_parts = nullptr;
     int32_t *seq_prefix_len = nullptr;
     int32_t *err = nullptr;
+    int32_t *counter = nullptr;  // fused-step completion counter, zero between launches
+    int32_t *queue = nullptr;    // work-queue head of the partial kernel, zero between launches
+    int32_t *done = nullptr;     // finished blocks of the partial kernel, zero between launches
+    void *zero_page = nullptr;   // 4 KiB of zeros
+    int32_t n_blocks = 0;        // persistent blocks of the partial kernel
     float *part_o = nullptr;
     float *part_lse = nullptr;
 };
@@ -92,11 +97,12 @@ fka_status check_heads(const fka_heads *h)
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
-// Prefix tokens per work item: enough items to give every compute unit about
-// two, in whole 128-token tiles, between 128 and 8192 tokens.
+// Prefix tokens per work item: about one item per compute unit (256 on MI355X),
+// in whole 128-token tiles, between 128 and 8192 tokens; the suffix items fill in
+// behind them from the device queue.
 int32_t auto_split(int64_t prefix_token_heads)
 {
-    const int64_t target_items = 512;
+    const int64_t target_items = 256;
     int64_t s = (prefix_token_heads + target_items - 1) / target_items;
     s = ((s + fka::kTileTokens - 1) / fka::kTileTokens) * fka::kTileTokens;
     return (int32_t)std::min<int64_t>(8192, std::max<int64_t>(fka::kTileTokens, s));
@@ -122,9 +128,10 @@ fka_status finish_plan(fka_plan *p, const std::vector<WorkItem> &items, const st
     const size_t b_spp = up(std::max<size_t>(1, spp.size()) * sizeof(int32_t));
     const size_t b_spl = up(std::max<size_t>(1, spl.size()) * sizeof(int32_t));
     const size_t b_err = 256;
+    const size_t b_zero = 4096;
     const size_t b_po = up(std::max<size_t>(1, (size_t)p->slots * n_rows * p->d) * sizeof(float));
     const size_t b_pl = up(std::max<size_t>(1, (size_t)p->slots * n_rows) * sizeof(float));
-    const size_t total = b_items + b_spp + b_spl + b_err + b_po + b_pl;
+    const size_t total = b_items + b_spp + b_spl + b_err + b_zero + b_po + b_pl;
     e = hipMalloc(&p->mem, total);
     if (e != hipSuccess) {
         p->mem = nullptr;
@@ -140,6 +147,8 @@ fka_status finish_plan(fka_plan *p, const std::vector<WorkItem> &items, const st
     m += b_spl;
     p->err = reinterpret_cast<int32_t *>(m);
     m += b_err;
+    p->zero_page = m;
+    m += b_zero;
     p->part_o = reinterpret_cast<float *>(m);
     m += b_po;
     p->part_lse = reinterpret_cast<float *>(m);
@@ -154,7 +163,15 @@ fka_status finish_plan(fka_plan *p, const std::vector<WorkItem> &items, const st
     if ((e = hipMemcpy(p->seq_prefix_len, spl.data(), spl.size() * sizeof(int32_t), hipMemcpyHostToDevice)) !=
         hipSuccess)
         return hip_fail(e, "hipMemcpy(prefix lengths)");
-    if ((e = hipMemset(p->err, 0, sizeof(int32_t))) != hipSuccess) return hip_fail(e, "hipMemset(error flag)");
+    if ((e = hipMemset(p->err, 0, b_err + b_zero)) != hipSuccess) return hip_fail(e, "hipMemset(flags)");
+    p->counter = p->err + 16;
+    p->queue = p->err + 32;
+    p->done = p->err + 48;
+    int cus = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
+        return hip_fail(e, "hipDeviceGetAttribute");
+    // one four-wave block per compute unit; never more blocks than items
+    p->n_blocks = std::max(1, std::min<int32_t>(p->n_items, cus));
     return FKA_OK;
 }
 
@@ -192,6 +209,9 @@ fka::AttnArgs attn_args(const fka_plan *p)
     a.max_pages = p->max_pages;
     a.n_pool_pages = p->n_pool_pages;
     a.paged = p->paged ? 1 : 0;
+    a.n_items = p->n_items;
+    a.queue = p->queue;
+    a.done = p->done;
     return a;
 }
 
@@ -207,19 +227,28 @@ fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *o
     m.n_parts = 0;
     m.seq_prefix_parts = p->seq_prefix_parts;
     m.max_prefix_parts = p->max_prefix_parts;
-    m.suffix_len = suffix_len;
+    m.suffix_len = const_cast<int32_t *>(suffix_len);  // only a fused step writes it
     m.suffix_split = p->ssplit;
     m.max_suffix_len = p->max_suffix_len;
     m.err = p->err;
+    m.counter = p->counter;
+    m.seq_prefix_len = p->seq_prefix_len;
+    m.suffix_cap = p->suffix_cap;
+    m.max_pages = p->max_pages;
+    m.n_pool_pages = p->n_pool_pages;
+    m.n_kv_heads = p->Hkv;
+    m.paged = p->paged ? 1 : 0;
+    m.scale = p->scale;
+    m.group = p->G;
     return m;
 }
 
 fka_status run_decode(const fka_plan *p, const fka::AttnArgs &a, const int32_t *suffix_len, float *out,
-                      float *out_lse, hipStream_t s)
+                      float *out_lse, hipStream_t s, const fka::MergeArgs *step = nullptr)
 {
-    hipError_t e = fka::launch_partials(a, p->n_items, p->d, p->row_tiles, s);
+    hipError_t e = fka::launch_partials(a, p->n_blocks, p->d, p->row_tiles, s);
     if (e != hipSuccess) return hip_fail(e, "partials kernel launch");
-    e = fka::launch_merge(merge_args(p, suffix_len, out, out_lse), p->d, s);
+    e = fka::launch_merge(step ? *step : merge_args(p, suffix_len, out, out_lse), p->d, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
     return ok();
 }
@@ -455,7 +484,7 @@ fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, 
     a.suffix_len = suffix_len;
     a.part_o = part_o;
     a.part_lse = part_lse;
-    hipError_t e = fka::launch_partials(a, p->n_items, p->d, p->row_tiles, static_cast<hipStream_t>(stream));
+    hipError_t e = fka::launch_partials(a, p->n_blocks, p->d, p->row_tiles, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "partials kernel launch");
     return ok();
 }
@@ -492,16 +521,64 @@ fka_status fka_fork_step(const fka_plan *p, const void *q, const void *k_new, co
                          int32_t *suffix_len, float *out, float *out_lse, void *stream)
 {
     REQUIRE(p != nullptr, "plan is null");
-    REQUIRE(!p->paged, "plan is paged");
+    REQUIRE(!p->paged, "plan is paged: use fka_fork_step_paged");
     REQUIRE_PTR16(q);
-    REQUIRE_PTR16(out);
+    REQUIRE_PTR16(k_new);
+    REQUIRE_PTR16(v_new);
     if (p->prefix_len > 0) {
         REQUIRE_PTR16(prefix_k);
         REQUIRE_PTR16(prefix_v);
     }
-    fka_status st = fka_append_kv(p, k_new, v_new, suffix_k, suffix_v, suffix_len, stream);
-    if (st != FKA_OK) return st;
-    return fka_fork_decode(p, q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, out, out_lse, stream);
+    REQUIRE_PTR16(suffix_k);
+    REQUIRE_PTR16(suffix_v);
+    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR16(out);
+    fka::AttnArgs a = attn_args(p);
+    a.q = static_cast<const uint16_t *>(q);
+    a.prefix_k = static_cast<const uint16_t *>(prefix_k);
+    a.prefix_v = static_cast<const uint16_t *>(prefix_v);
+    a.suffix_k = static_cast<const uint16_t *>(suffix_k);
+    a.suffix_v = static_cast<const uint16_t *>(suffix_v);
+    a.suffix_len = suffix_len;
+    fka::MergeArgs m = merge_args(p, suffix_len, out, out_lse);
+    m.step_mode = 1;
+    m.q = a.q;
+    m.k_new = static_cast<const uint16_t *>(k_new);
+    m.v_new = static_cast<const uint16_t *>(v_new);
+    m.k_dst = static_cast<uint16_t *>(suffix_k);
+    m.v_dst = static_cast<uint16_t *>(suffix_v);
+    return run_decode(p, a, suffix_len, out, out_lse, static_cast<hipStream_t>(stream), &m);
+}
+
+fka_status fka_fork_step_paged(const fka_plan *p, const void *q, const void *k_new, const void *v_new, void *k_pool,
+                               void *v_pool, const int32_t *page_table, int32_t *suffix_len, float *out,
+                               float *out_lse, void *stream)
+{
+    REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(p->paged, "plan is contiguous: use fka_fork_step");
+    REQUIRE_PTR16(q);
+    REQUIRE_PTR16(k_new);
+    REQUIRE_PTR16(v_new);
+    REQUIRE_PTR16(k_pool);
+    REQUIRE_PTR16(v_pool);
+    REQUIRE(page_table != nullptr, "page_table is null");
+    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR16(out);
+    fka::AttnArgs a = attn_args(p);
+    a.q = static_cast<const uint16_t *>(q);
+    a.k_pool = static_cast<const uint16_t *>(k_pool);
+    a.v_pool = static_cast<const uint16_t *>(v_pool);
+    a.page_table = page_table;
+    a.suffix_len = suffix_len;
+    fka::MergeArgs m = merge_args(p, suffix_len, out, out_lse);
+    m.step_mode = 1;
+    m.q = a.q;
+    m.k_new = static_cast<const uint16_t *>(k_new);
+    m.v_new = static_cast<const uint16_t *>(v_new);
+    m.k_dst = static_cast<uint16_t *>(k_pool);
+    m.v_dst = static_cast<uint16_t *>(v_pool);
+    m.page_table = page_table;
+    return run_decode(p, a, suffix_len, out, out_lse, static_cast<hipStream_t>(stream), &m);
 }
 
 fka_status fka_fork_decode_paged(const fka_plan *p, const void *q, const void *k_pool, const void *v_pool,

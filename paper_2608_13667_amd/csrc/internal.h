@@ -15,7 +15,7 @@ enum ItemKind : int32_t {
 // One block of the partial-attention kernel: query rows of sequences
 // [seq0, seq0 + nseq) x the G query heads of kv_head, over keys
 // [tok_begin, tok_end) of the item's source; result goes to partial slot `part`.
-struct WorkItem {
+struct WorkItem {  // eight int32 fields, read field by field on the device
     int32_t kind;
     int32_t seq0;
     int32_t nseq;
@@ -50,6 +50,10 @@ struct AttnArgs {
     float *part_o;     // [slots][S][Hq][d]
     float *part_lse;   // [slots][S][Hq]
     int32_t *err;
+    // persistent scheduling
+    int32_t n_items;
+    int32_t *queue;          // next item to hand out; zero between launches
+    int32_t *done;           // blocks finished; zero between launches
 };
 
 struct MergeArgs {
@@ -66,10 +70,26 @@ struct MergeArgs {
     // max_prefix_parts + j for j < ceil(min(suffix_len[s], max_suffix_len) / suffix_split)
     const int32_t *seq_prefix_parts;
     int32_t max_prefix_parts;
-    const int32_t *suffix_len;
+    int32_t *suffix_len;  // written only by a fused step
     int32_t suffix_split;
     int32_t max_suffix_len;
     int32_t *err;
+    // fused step: the token in k_new / v_new (not yet in the cache) joins each row as one
+    // more part; the last block then appends it and advances suffix_len
+    int32_t step_mode;
+    const uint16_t *q;  // [S][Hq][d]
+    float scale;        // softmax scale (natural-log units)
+    int32_t group;      // G = Hq / Hkv
+    int32_t *counter;               // zero between launches
+    const uint16_t *k_new, *v_new;  // [S][Hkv][d]
+    uint16_t *k_dst, *v_dst;        // suffix buffers or pools
+    const int32_t *page_table;
+    const int32_t *seq_prefix_len;
+    int32_t suffix_cap;
+    int32_t max_pages;
+    int32_t n_pool_pages;
+    int32_t n_kv_heads;
+    int32_t paged;
 };
 
 struct AppendArgs {
@@ -107,11 +127,11 @@ constexpr int32_t kErrSuffixClamped = 1;
 constexpr int32_t kErrAppendNoRoom = 2;
 constexpr int32_t kErrBadPage = 4;
 
-constexpr int kTileTokens = 128;  // tokens staged in LDS per iteration of the partial kernel
+constexpr int kTileTokens = 128;  // split sizes are whole multiples of this many tokens
 constexpr int kPageSize = 16;
 constexpr int kMaxRows = 64;      // query rows (sequences x G) per KV head that one item can hold
 
-hipError_t launch_partials(const AttnArgs &a, int n_items, int head_dim, int row_tiles, hipStream_t s);
+hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);

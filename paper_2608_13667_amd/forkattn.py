@@ -55,6 +55,7 @@ _sig = {
     "fka_append_kv": ([_vp] * 7, C.c_int),
     "fka_fork_step": ([_vp] * 12, C.c_int),
     "fka_fork_decode_paged": ([_vp] * 9, C.c_int),
+    "fka_fork_step_paged": ([_vp] * 11, C.c_int),
     "fka_append_kv_paged": ([_vp] * 8, C.c_int),
     "fka_gather_paged": ([_vp, C.c_int32, _vp, _vp, _vp, C.c_int32, _vp, _vp, _vp], C.c_int),
     "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
@@ -184,6 +185,10 @@ class Plan:
     def decode_paged(self, q, k_pool, v_pool, page_table, suffix_len, out, out_lse=None, stream=None):
         _check(_lib.fka_fork_decode_paged(self._h, _p(q), _p(k_pool), _p(v_pool), _p(page_table), _p(suffix_len),
                                           _p(out), _p(out_lse), _stream(stream)))
+
+    def step_paged(self, q, k_new, v_new, k_pool, v_pool, page_table, suffix_len, out, out_lse=None, stream=None):
+        _check(_lib.fka_fork_step_paged(self._h, _p(q), _p(k_new), _p(v_new), _p(k_pool), _p(v_pool),
+                                        _p(page_table), _p(suffix_len), _p(out), _p(out_lse), _stream(stream)))
 
     def append_paged(self, k_new, v_new, k_pool, v_pool, page_table, suffix_len, stream=None):
         _check(_lib.fka_append_kv_paged(self._h, _p(k_new), _p(v_new), _p(k_pool), _p(v_pool), _p(page_table),

@@ -340,3 +340,75 @@ def test_suffix_length_above_bound_is_clamped_and_flagged(fa):
     ref, _ = oracle.decode_workload(w)
     gates.assert_gates(out, ref, what="clamped lengths")
     assert plan.device_error() & 1
+
+
+def test_fused_step_equals_append_then_decode(fa):
+    """fka_fork_step (append fused into the decode) matches append + decode: identical caches and
+    lengths, outputs equal up to fp32 summation order (the new token is merged as its own part)."""
+    w = W.make("mid", steps=8)
+    plan = contig_plan(fa, w)
+    a, b = to_dev_contig(w), to_dev_contig(w)
+    N, Hq, d = w.q.shape
+    oa, la = torch.empty((N, Hq, d), device="cuda"), torch.empty((N, Hq), device="cuda")
+    ob, lb = torch.empty_like(oa), torch.empty_like(la)
+    kn, vn, qn = dev_bf16(w.step_k), dev_bf16(w.step_v), dev_bf16(w.step_q)
+    for t in range(8):
+        plan.step(qn[t], kn[t], vn[t], a["prefix_k"], a["prefix_v"], a["suffix_k"], a["suffix_v"], a["suffix_len"],
+                  oa, la)
+        plan.append(kn[t], vn[t], b["suffix_k"], b["suffix_v"], b["suffix_len"])
+        plan.decode(qn[t], b["prefix_k"], b["prefix_v"], b["suffix_k"], b["suffix_v"], b["suffix_len"], ob, lb)
+        torch.cuda.synchronize()
+        torch.testing.assert_close(oa, ob, rtol=1e-5, atol=1e-6, msg=f"step {t}")
+        torch.testing.assert_close(la, lb, rtol=1e-6, atol=1e-5, msg=f"step {t}")
+    assert torch.equal(a["suffix_len"], b["suffix_len"])
+    assert torch.equal(a["suffix_k"].view(torch.int16), b["suffix_k"].view(torch.int16))
+    assert torch.equal(a["suffix_v"].view(torch.int16), b["suffix_v"].view(torch.int16))
+    assert plan.device_error() == 0
+
+
+def test_fused_step_paged_equals_append_then_decode(fa):
+    w = _small_paged(headroom=24, seed=94)
+    plan = paged_plan(fa, w)
+    a, b = to_dev_paged(w), to_dev_paged(w)
+    S, Hq, d = w.q.shape
+    rng = np.random.default_rng(5)
+    oa, ob = torch.empty((S, Hq, d), device="cuda"), torch.empty((S, Hq, d), device="cuda")
+    for t in range(20):
+        kn = dev_bf16(W.bf16_bits(rng.standard_normal((S, w.spec.n_kv_heads, d)).astype(np.float32)))
+        vn = dev_bf16(W.bf16_bits(rng.standard_normal((S, w.spec.n_kv_heads, d)).astype(np.float32)))
+        q = dev_bf16(W.bf16_bits(rng.standard_normal((S, Hq, d)).astype(np.float32)))
+        plan.step_paged(q, kn, vn, a["k_pool"], a["v_pool"], a["page_table"], a["suffix_len"], oa)
+        plan.append_paged(kn, vn, b["k_pool"], b["v_pool"], b["page_table"], b["suffix_len"])
+        plan.decode_paged(q, b["k_pool"], b["v_pool"], b["page_table"], b["suffix_len"], ob)
+        torch.cuda.synchronize()
+        torch.testing.assert_close(oa, ob, rtol=1e-5, atol=1e-6, msg=f"step {t}")
+    assert torch.equal(a["suffix_len"], b["suffix_len"])
+    assert torch.equal(a["k_pool"].view(torch.int16), b["k_pool"].view(torch.int16))
+    assert plan.device_error() == 0
+
+
+def test_fused_step_at_capacity_is_flagged(fa):
+    w = W.make("tiny", suffix_range=(8, 8))          # every suffix already at the bound
+    plan = contig_plan(fa, w, max_suffix_len=8)
+    dv = to_dev_contig(w)
+    kn = torch.zeros((w.n_branches, 2, 64), dtype=torch.bfloat16, device="cuda")
+    out = torch.empty((w.n_branches, 8, 64), device="cuda")
+    plan.step(dv["q"], kn, kn, dv["prefix_k"], dv["prefix_v"], dv["suffix_k"], dv["suffix_v"], dv["suffix_len"], out)
+    torch.cuda.synchronize()
+    assert torch.equal(dv["suffix_len"].cpu(), torch.full((w.n_branches,), 8, dtype=torch.int32))
+    assert plan.device_error() & 2
+    ref, _ = oracle.decode_workload(w)       # the full buffers, without the token that did not fit
+    gates.assert_gates(out.cpu().numpy(), ref, what="step at capacity")
+
+
+def test_nan_input_propagates_to_its_branch_only(fa):
+    w = W.make("mid", seed=95)
+    w.suffix_v[3, 2, 5] = W.BF16_NAN            # one value row of branch 3, KV head 2
+    out, lse = run_contig(contig_plan(fa, w), to_dev_contig(w), 32)
+    G = w.spec.group
+    bad = np.zeros(out.shape[:2], bool)
+    bad[3, 2 * G:3 * G] = True
+    assert np.all(np.isnan(out[bad]).any(axis=-1))
+    assert np.all(np.isfinite(out[~bad]))
+    ref, _ = oracle.decode_workload(w)
+    gates.assert_gates(out[~bad], ref[~bad], what="rows without the NaN")
