@@ -23,6 +23,7 @@
 // The waves' (max, sum, accumulator) are combined through LDS at the end of the
 // item and one normalised partial (o, lse) per row is written.
 #include <type_traits>
+#include <utility>
 
 #include "internal.h"
 
@@ -39,7 +40,11 @@ typedef __attribute__((address_space(4))) const int32_t const_i32;
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kSlice = 32;      // tokens per wave step
-constexpr int kVStages = 4;     // V slices held per wave (three in flight)
+#ifndef FKA_PIPELINE_DEPTH
+#define FKA_PIPELINE_DEPTH 1
+#endif
+constexpr int kDepth = FKA_PIPELINE_DEPTH;  // K and V slices in flight ahead of the one being scored
+constexpr int kStages = kDepth + 1;         // V ring stages and K register sets per wave
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr float kRescaleGap = 8.0f;  // log2 units: accumulate with p <= 2^8 before moving the max
 
@@ -82,6 +87,18 @@ __device__ inline void wait_vm()
 {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Calls f(std::integral_constant<int, i>{}) for i = 0 .. N-1 (compile-time unrolled).
+template <typename F, int... I>
+__device__ inline void static_for_impl(F &&f, std::integer_sequence<int, I...>)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ inline void static_for(F &&f)
+{
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
 // Reductions over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the four 16-lane rows of
@@ -145,10 +162,10 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
     constexpr int KLOADS = 2 * NC;              // K loads per lane per slice
     static_assert(VDMA == KLOADS, "one wait count per slice");
     constexpr int OSTRIDE = HD + 4;             // padded row stride of the output staging (floats)
-    static_assert(kWaves * 16 * OSTRIDE * 4 <= kWaves * kVStages * SLICE_CHUNKS * 16, "staging fits");
+    static_assert(kWaves * 16 * OSTRIDE * 4 <= kWaves * kStages * SLICE_CHUNKS * 16, "staging fits");
 
-    // per wave: kVStages V slices; chunk c of slice token T sits at T*CPR + (c ^ swz(T))
-    __shared__ uint4 vring[kWaves][kVStages][SLICE_CHUNKS];
+    // per wave: kStages V slices; chunk c of slice token T sits at T*CPR + (c ^ swz(T))
+    __shared__ uint4 vring[kWaves][kStages][SLICE_CHUNKS];
     __shared__ float red_m[kWaves][NT][16];
     __shared__ float red_l[kWaves][NT][16];
     __shared__ int s_item;
@@ -394,37 +411,26 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
             }
         };
 
-        // Pipeline: V three slices ahead through the four-stage ring (slice k uses stage k % 4),
-        // K one slice ahead in two register sets.  Loads are issued for every step (slices past
-        // this wave's last one read the zero page), so the issue order is fixed:
-        // V0 V1 V2 K0 | V3 K1 | V4 K2 | ...  Before computing slice k the loads issued after K(k)
-        // are V(k+3) and K(k+1); V(k) precedes K(k).
-        using S0 = std::integral_constant<int, 0>;
-        using S1 = std::integral_constant<int, 1>;
-        using S2 = std::integral_constant<int, 2>;
-        using S3 = std::integral_constant<int, 3>;
-        bf16x8 ka[2][NC], kb[2][NC];
-        issue_v(0, S0{});
-        issue_v(1, S1{});
-        issue_v(2, S2{});
-        load_k(0, ka);
-        for (int k = 0; k < ns; k += 4) {
-            issue_v(k + 3, S3{});
-            load_k(k + 1, kb);
-            wait_vm<2 * KLOADS>();
-            compute(k, ka, S0{});
-            issue_v(k + 4, S0{});
-            load_k(k + 2, ka);
-            wait_vm<2 * KLOADS>();
-            if (k + 1 < ns) compute(k + 1, kb, S1{});
-            issue_v(k + 5, S1{});
-            load_k(k + 3, kb);
-            wait_vm<2 * KLOADS>();
-            if (k + 2 < ns) compute(k + 2, ka, S2{});
-            issue_v(k + 6, S2{});
-            load_k(k + 4, ka);
-            wait_vm<2 * KLOADS>();
-            if (k + 3 < ns) compute(k + 3, kb, S3{});
+        // Pipeline: K and V kDepth slices ahead, slice k in V ring stage and K register set
+        // k % kStages.  Loads are issued for every step (slices past this wave's last one have
+        // empty buffer resources and move no data), so the issue order is fixed:
+        // V0 K0 V1 K1 ... | V(k+kDepth) K(k+kDepth) before computing slice k.  The loads issued
+        // after K(k) are then V(k+1), K(k+1), ..., V(k+kDepth), K(k+kDepth); V(k) precedes K(k).
+        bf16x8 kbuf[kStages][2][NC];
+        static_for<kDepth>([&](auto J) {
+            constexpr int j = decltype(J)::value;
+            issue_v(j, std::integral_constant<int, j>{});
+            load_k(j, kbuf[j]);
+        });
+        for (int k = 0; k < ns; k += kStages) {
+            static_for<kStages>([&](auto PH) {
+                constexpr int ph = decltype(PH)::value;
+                constexpr int ahead = (ph + kDepth) % kStages;
+                issue_v(k + ph + kDepth, std::integral_constant<int, ahead>{});
+                load_k(k + ph + kDepth, kbuf[ahead]);
+                wait_vm<2 * kDepth * KLOADS>();
+                if (ph == 0 || k + ph < ns) compute(k + ph, kbuf[ph], PH);
+            });
         }
 
         // combine the four waves' (max, sum, accumulator) per row and write the partial
