@@ -71,7 +71,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--replicas", type=int, default=0, help="layer replicas (0: enough for >= 1 GiB)")
-    ap.add_argument("--split", type=int, default=0, help="prefix tokens per work item (0: automatic)")
+    ap.add_argument("--rounds", type=int, default=0, help="schedule rounds of the resident waves (0: automatic)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-naive", action="store_true", help="skip the naive per-branch GPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -119,7 +119,7 @@ def main():
         def mk_plan(share):
             return fa.Plan.paged_plan(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.group_start, w.prefix_len,
                                       w.page_table.shape[1], w.k_pool.shape[0], int(w.suffix_len.max()),
-                                      share_prefix=share, split_tokens=args.split)
+                                      share_prefix=share, rounds=args.rounds)
     else:
         base = dict(q=dev(w.q), prefix_k=dev(w.prefix_k), prefix_v=dev(w.prefix_v), suffix_k=dev(w.suffix_k),
                     suffix_v=dev(w.suffix_v), suffix_len=torch.from_numpy(w.suffix_len).cuda())
@@ -127,7 +127,7 @@ def main():
 
         def mk_plan(share):
             return fa.Plan.contig(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.n_branches, w.prefix_len,
-                                  w.suffix_cap, w.suffix_cap, share_prefix=share, split_tokens=args.split)
+                                  w.suffix_cap, w.suffix_cap, share_prefix=share, rounds=args.rounds)
     n_seq = w.q.shape[0]
     out = torch.empty((n_seq, spec.n_q_heads, spec.head_dim), device="cuda")
     lse = torch.empty((n_seq, spec.n_q_heads), device="cuda")
@@ -184,9 +184,8 @@ def main():
     log(f"[bench] fork-aware: {K / secs:.1f} steps/s, {secs / K * 1e6:.2f} us/step, {gbps:.0f} GB/s")
 
     # dominant kernel alone: the partial-attention kernel, timed on the stream it runs on
-    n_slots = info.max_prefix_parts + info.n_suffix_parts
-    po = torch.empty((max(1, n_slots), n_seq, spec.n_q_heads, spec.head_dim), device="cuda")
-    pl = torch.empty((max(1, n_slots), n_seq, spec.n_q_heads), device="cuda")
+    po = torch.empty((info.n_slots, info.slot_rows, spec.head_dim), device="cuda")
+    pl = torch.empty((info.n_slots, info.slot_rows), device="cuda")
     reset()
     kp = max(50, min(K, 400))
     if not paged:
@@ -273,8 +272,8 @@ def main():
         log(f"[bench] cpu oracle: {n / cs:.3f} steps/s on {cpu['cores']} threads")
 
     cfg = {"workload": DESCRIPTIONS[args.workload], "name": args.workload, "replicas": R,
-           "working_set_gib": R * kvb["total"] / 2**30, "split_tokens": info.split_tokens,
-           "suffix_split_tokens": info.suffix_split_tokens, "work_items": info.n_items}
+           "working_set_gib": R * kvb["total"] / 2**30, "blocks": info.n_blocks,
+           "waves_per_block": info.waves_per_block, "rounds": info.rounds, "work_items": info.n_items}
     res = {
         "metric": "fork-decode attention steps/s and effective KV GB/s (% of HBM peak), 1 GPU",
         "value": K / secs,

@@ -25,8 +25,8 @@
  *     and return without synchronising.  Results are valid once the stream has
  *     reached that point.
  *   - Calls never allocate, free or synchronise, except fka_plan_create_*
- *     (allocates the plan's device workspace and work list, copies the work
- *     list to the device), fka_plan_destroy (frees them) and
+ *     (allocates the plan's device workspace and schedule tables, copies the
+ *     tables to the device), fka_plan_destroy (frees them) and
  *     fka_plan_device_error (reads the device error word).
  *   - A plan owns a workspace for partial results, so it may be used by one
  *     stream at a time.  Plans are independent of each other.
@@ -72,8 +72,8 @@ typedef struct {
     float softmax_scale; /* scores are scale * q.k; 0 selects 1 / sqrt(head_dim) */
 } fka_heads;
 
-/* Opaque plan: the split of the work into tiles, a device work list and the
- * workspace for partial (o, lse) results.  Built once per fork (the prefix
+/* Opaque plan: the static part of the work schedule (prefix items), the grid, and
+ * the workspace for partial (o, lse) results.  Built once per fork (the prefix
  * length is fixed at the fork instant), reused for every decode step. */
 typedef struct fka_plan fka_plan;
 
@@ -88,15 +88,16 @@ typedef struct {
     int32_t max_suffix_len; /* upper bound on suffix_len[b] over the plan's lifetime, <= suffix_cap */
     int32_t share_prefix;   /* 1: fork-aware (prefix tiles read once for all N branches);
                                0: naive baseline, every branch re-reads the prefix on its own */
-    int32_t split_tokens;   /* prefix tokens per work item (multiple of 128); 0 = automatic */
+    int32_t rounds;         /* 0 = automatic; k in [1, 64] = spread the keys over at least k
+                               rounds of the resident waves (more, smaller partial results) */
 } fka_contig_desc;
 
-/* Build a plan for the contiguous layout.  Allocates device memory (work list,
- * workspace, error flag) on the current device.  *out receives the plan, owned by
- * the caller until fka_plan_destroy.  Errors: FKA_ERR_INVALID_ARG (null pointer,
- * non-positive sizes, Hq % Hkv != 0, max_suffix_len > suffix_cap),
- * FKA_ERR_UNSUPPORTED (head_dim not 64/128, more than 64 rows N*G per KV head),
- * FKA_ERR_NOMEM, FKA_ERR_HIP. */
+/* Build a plan for the contiguous layout.  Allocates device memory (schedule
+ * tables, workspace, error flag) on the current device.  *out receives the plan,
+ * owned by the caller until fka_plan_destroy.  Errors: FKA_ERR_INVALID_ARG (null
+ * pointer, non-positive sizes, Hq % Hkv != 0, max_suffix_len > suffix_cap, rounds
+ * outside [0, 64]), FKA_ERR_UNSUPPORTED (head_dim not 64/128, more than 64 rows N*G
+ * per KV head, more than 512 sequences), FKA_ERR_NOMEM, FKA_ERR_HIP. */
 fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc *desc, fka_plan **out);
 
 /*
@@ -127,8 +128,8 @@ fka_status fka_append_kv(const fka_plan *plan, const void *k_new, const void *v_
 
 /* Append (as fka_append_kv) and then decode (as fka_fork_decode), fused into two
  * kernel launches: the merge stage scores each branch's new K/V row straight from
- * k_new / v_new as one more part of the log-sum-exp merge, then stores it at
- * suffix_len[b] and increments suffix_len[b].  The caches and lengths end up as
+ * k_new / v_new as one more part of the log-sum-exp merge, and one block per branch
+ * stores it at suffix_len[b] and increments suffix_len[b].  The caches and lengths end up as
  * after fka_append_kv; the outputs equal fka_append_kv + fka_fork_decode up to the
  * order of the fp32 sums. */
 fka_status fka_fork_step(const fka_plan *plan, const void *q, const void *k_new, const void *v_new,
@@ -148,7 +149,7 @@ typedef struct {
     int32_t n_pool_pages;      /* pages in k_pool / v_pool; page ids outside [0, n_pool_pages) are never read */
     int32_t max_suffix_len;    /* upper bound on suffix_len[i] over the plan's lifetime */
     int32_t share_prefix;      /* 1 fork-aware, 0 naive baseline (as in fka_contig_desc) */
-    int32_t split_tokens;      /* prefix tokens per work item (multiple of 128); 0 = automatic */
+    int32_t rounds;            /* as in fka_contig_desc */
 } fka_paged_desc;
 
 /*
@@ -200,31 +201,57 @@ fka_status fka_gather_paged(const fka_plan *plan, int32_t seq, const void *k_poo
 
 /* -------------------------------------------------------------- stage entry points */
 
-/* Split geometry of a plan: the prefix of group t is cut into work items of
- * split_tokens tokens (the last one shorter); suffixes into items of
- * suffix_split_tokens.  max_prefix_parts is the largest number of prefix items of
- * any group, n_suffix_parts the number of suffix items per sequence. */
+/* Schedule geometry of a plan.  The keys are cut into items: one per (prefix unit,
+ * KV head) -- a unit is a sequence group sharing its prefix, or one sequence in the
+ * naive baseline -- and one per (sequence, KV head) for the suffixes.  Every decode
+ * spreads the slices (32 keys) of all items evenly over n_blocks * rounds *
+ * waves_per_block waves, using the suffix lengths it finds on the device; the waves of
+ * one block that work on the same item share their slices and write one partial result
+ * to a slot. */
 typedef struct {
-    int32_t split_tokens;
-    int32_t suffix_split_tokens;
-    int32_t max_prefix_parts;
-    int32_t n_suffix_parts;
-    int32_t n_items;           /* work items launched per decode */
+    int32_t n_items;           /* prefix items + n_seqs * n_kv_heads suffix items */
+    int32_t n_prefix_items;
+    int32_t waves_per_block;   /* waves of one block of the partial kernel */
+    int32_t n_blocks;          /* blocks of the partial kernel resident at once */
+    int32_t rounds;            /* the kernel runs n_blocks * rounds blocks */
+    int32_t n_slots;           /* partial-result slots in the workspace */
+    int32_t slot_rows;         /* rows per slot: the largest item's query rows */
     size_t workspace_bytes;    /* device bytes held by the plan */
 } fka_plan_info;
 
 fka_status fka_plan_get_info(const fka_plan *plan, fka_plan_info *info);
 
+/* One partial result written by the first stage: rows of sequences [seq0, seq0 + nseq)
+ * x the G query heads of kv_head (row r = (s - seq0) * G + h % G), attended over key
+ * positions [tok_begin, tok_end) of the item's keys (prefix positions for kind 0,
+ * positions in sequence seq0's suffix for kind 1).  n_tok is the item's key count. */
+typedef struct {
+    int32_t slot;
+    int32_t kind;
+    int32_t seq0;
+    int32_t nseq;
+    int32_t kv_head;
+    int32_t rows;
+    int32_t tok_begin;
+    int32_t tok_end;
+    int32_t n_tok;
+} fka_slot;
+
+/* The slots a decode writes when the device holds the suffix lengths
+ * host_suffix_len (host int32 [n_seqs]), computed on the host with the same
+ * arithmetic as the kernels.  Fills up to `capacity` entries of `slots` and sets
+ * *n_slots to the number of slots (which may exceed capacity). */
+fka_status fka_plan_slots(const fka_plan *plan, const int32_t *host_suffix_len, fka_slot *slots, int32_t capacity,
+                          int32_t *n_slots);
+
 /*
  * Partial results of the first stage (test hook; the decode calls write the same
- * values to the plan's workspace).  Part p of sequence b (contiguous plans) is the
- * attention of q[b] over prefix tokens [p*split, min((p+1)*split, Lp)) for
- * p < max_prefix_parts, and over suffix tokens [s*ssplit, min((s+1)*ssplit, len_b))
- * for p = max_prefix_parts + s.  o is normalised; lse is the natural-log
- * log-sum-exp of the scaled scores; a part with no tokens is (0, -inf) or left
- * unwritten when its range is empty on the device (suffix parts past len_b).
- *   part_o   fp32 [max_prefix_parts + n_suffix_parts][N][Hq][d]
- *   part_lse fp32 [max_prefix_parts + n_suffix_parts][N][Hq]
+ * values to the plan's workspace).  For every slot listed by fka_plan_slots, rows
+ * [0, rows) of slot `slot` hold the attention of those rows over the slot's key
+ * range: o normalised, lse the natural-log log-sum-exp of the scaled scores, (0, -inf)
+ * for a range without keys.  Other slots and rows are left unwritten.
+ *   part_o   fp32 [n_slots][slot_rows][d]
+ *   part_lse fp32 [n_slots][slot_rows]
  */
 fka_status fka_partials(const fka_plan *plan, const void *q, const void *prefix_k, const void *prefix_v,
                         const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *part_o,

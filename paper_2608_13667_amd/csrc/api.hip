@@ -1,6 +1,7 @@
-// C ABI of libforkattn.so: argument validation, plans (work lists and
+// C ABI of libforkattn.so: argument validation, plans (schedule tables and
 // workspaces) and kernel launches.  Declared in include/forkattn.h.
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -10,8 +11,6 @@
 
 #include "forkattn.h"
 #include "internal.h"
-
-using fka::WorkItem;
 
 struct fka_plan {
     bool paged = false;
@@ -25,23 +24,29 @@ struct fka_plan {
     // paged
     int32_t n_groups = 0, page_size = 0, max_pages = 0, n_pool_pages = 0;
     std::vector<int32_t> group_start, group_prefix_len;
-    // split geometry
-    int32_t split = 0, ssplit = 0, max_prefix_parts = 0, n_suffix_parts = 0, slots = 0;
+    // schedule (see the work schedule in internal.h)
+    std::vector<fka::PrefixItem> pre;      // static prefix items, unit-major, KV head minor
+    std::vector<int32_t> seq_pre_item;     // prefix item of (s, head 0), -1 if none
+    std::vector<int32_t> seq_pre_row;      // first row of s within its prefix item
+    std::vector<int32_t> seq_prefix_len;   // prefix length of s's unit
+    int32_t pre_slices = 0, pre_nonempty = 0;
+    int32_t n_items = 0;       // prefix items + n_seqs * Hkv suffix items
+    int32_t slot_rows = 0;     // rows of the largest item
     int32_t row_tiles = 1;
-    int32_t n_items = 0;
+    int32_t waves = 0;         // waves per block of the partial kernel
+    int32_t n_blocks = 0;      // blocks resident at once on the device
+    int32_t rounds = 1;        // launches n_blocks * rounds blocks
+    int32_t n_slots = 0;       // partial-result slots in the workspace
     size_t workspace_bytes = 0;
     int device = 0;
     // device memory (one allocation, carved)
     void *mem = nullptr;
-    WorkItem *items = nullptr;
-    int32_t *seq_prefix_parts = nullptr;
-    int32_t *seq_prefix_len = nullptr;
+    fka::PrefixItem *d_pre = nullptr;
+    int32_t *d_seq_pre_item = nullptr;
+    int32_t *d_seq_pre_row = nullptr;
+    int32_t *d_seq_prefix_len = nullptr;
     int32_t *err = nullptr;
-    int32_t *counter = nullptr;  // fused-step completion counter, zero between launches
-    int32_t *queue = nullptr;    // work-queue head of the partial kernel, zero between launches
-    int32_t *done = nullptr;     // finished blocks of the partial kernel, zero between launches
-    void *zero_page = nullptr;   // 4 KiB of zeros
-    int32_t n_blocks = 0;        // persistent blocks of the partial kernel
+    int32_t *sched = nullptr;
     float *part_o = nullptr;
     float *part_lse = nullptr;
 };
@@ -97,84 +102,6 @@ fka_status check_heads(const fka_heads *h)
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
-// Prefix tokens per work item: about one item per compute unit (256 on MI355X),
-// in whole 128-token tiles, between 128 and 8192 tokens; the suffix items fill in
-// behind them from the device queue.
-int32_t auto_split(int64_t prefix_token_heads)
-{
-    const int64_t target_items = 256;
-    int64_t s = (prefix_token_heads + target_items - 1) / target_items;
-    s = ((s + fka::kTileTokens - 1) / fka::kTileTokens) * fka::kTileTokens;
-    return (int32_t)std::min<int64_t>(8192, std::max<int64_t>(fka::kTileTokens, s));
-}
-
-int32_t auto_suffix_split(int32_t max_suffix_len)
-{
-    // whole tiles; short suffixes stay in one item
-    if (max_suffix_len <= 512) return std::max(fka::kTileTokens, ceil_div(std::max(max_suffix_len, 1), 128) * 128);
-    return 512;
-}
-
-// Allocate device memory for the work list, per-sequence tables, error flag and
-// workspace, and upload the tables.
-fka_status finish_plan(fka_plan *p, const std::vector<WorkItem> &items, const std::vector<int32_t> &spp,
-                       const std::vector<int32_t> &spl)
-{
-    hipError_t e = hipGetDevice(&p->device);
-    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-    const size_t n_rows = (size_t)p->n_seqs * p->Hq;
-    const size_t b_items = up(std::max<size_t>(1, items.size()) * sizeof(WorkItem));
-    const size_t b_spp = up(std::max<size_t>(1, spp.size()) * sizeof(int32_t));
-    const size_t b_spl = up(std::max<size_t>(1, spl.size()) * sizeof(int32_t));
-    const size_t b_err = 256;
-    const size_t b_zero = 4096;
-    const size_t b_po = up(std::max<size_t>(1, (size_t)p->slots * n_rows * p->d) * sizeof(float));
-    const size_t b_pl = up(std::max<size_t>(1, (size_t)p->slots * n_rows) * sizeof(float));
-    const size_t total = b_items + b_spp + b_spl + b_err + b_zero + b_po + b_pl;
-    e = hipMalloc(&p->mem, total);
-    if (e != hipSuccess) {
-        p->mem = nullptr;
-        (void)hipGetLastError();
-        return fail(FKA_ERR_NOMEM, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
-    }
-    char *m = static_cast<char *>(p->mem);
-    p->items = reinterpret_cast<WorkItem *>(m);
-    m += b_items;
-    p->seq_prefix_parts = reinterpret_cast<int32_t *>(m);
-    m += b_spp;
-    p->seq_prefix_len = reinterpret_cast<int32_t *>(m);
-    m += b_spl;
-    p->err = reinterpret_cast<int32_t *>(m);
-    m += b_err;
-    p->zero_page = m;
-    m += b_zero;
-    p->part_o = reinterpret_cast<float *>(m);
-    m += b_po;
-    p->part_lse = reinterpret_cast<float *>(m);
-    p->workspace_bytes = total;
-    p->n_items = (int32_t)items.size();
-    if (!items.empty() && (e = hipMemcpy(p->items, items.data(), items.size() * sizeof(WorkItem),
-                                         hipMemcpyHostToDevice)) != hipSuccess)
-        return hip_fail(e, "hipMemcpy(work list)");
-    if ((e = hipMemcpy(p->seq_prefix_parts, spp.data(), spp.size() * sizeof(int32_t), hipMemcpyHostToDevice)) !=
-        hipSuccess)
-        return hip_fail(e, "hipMemcpy(prefix parts)");
-    if ((e = hipMemcpy(p->seq_prefix_len, spl.data(), spl.size() * sizeof(int32_t), hipMemcpyHostToDevice)) !=
-        hipSuccess)
-        return hip_fail(e, "hipMemcpy(prefix lengths)");
-    if ((e = hipMemset(p->err, 0, b_err + b_zero)) != hipSuccess) return hip_fail(e, "hipMemset(flags)");
-    p->counter = p->err + 16;
-    p->queue = p->err + 32;
-    p->done = p->err + 48;
-    int cus = 0;
-    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
-        return hip_fail(e, "hipDeviceGetAttribute");
-    // one four-wave block per compute unit; never more blocks than items
-    p->n_blocks = std::max(1, std::min<int32_t>(p->n_items, cus));
-    return FKA_OK;
-}
-
 void init_heads(fka_plan *p, const fka_heads *h)
 {
     p->Hq = h->n_q_heads;
@@ -184,17 +111,129 @@ void init_heads(fka_plan *p, const fka_heads *h)
     p->scale = h->softmax_scale > 0.f ? h->softmax_scale : 1.0f / std::sqrt((float)h->head_dim);
 }
 
-fka_status check_split(int32_t split)
+fka_status check_rounds(int32_t rounds)
 {
-    REQUIRE(split >= 0 && split % fka::kTileTokens == 0, "split_tokens (%d) must be a non-negative multiple of %d",
-            split, fka::kTileTokens);
+    REQUIRE(rounds >= 0 && rounds <= 64, "rounds (%d) must be in [0, 64]", rounds);
+    return FKA_OK;
+}
+
+// Prefix units in order: unit u covers sequences [seq0, seq0 + nseq) that share a prefix of
+// n_tok tokens.  Builds the static prefix items (one per unit and KV head), the
+// per-sequence tables, the slot geometry, the grid and the round count.
+fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>> &units, int32_t rounds_req)
+{
+    p->pre.clear();
+    p->seq_pre_item.assign(p->n_seqs, -1);
+    p->seq_pre_row.assign(p->n_seqs, 0);
+    p->seq_prefix_len.assign(p->n_seqs, 0);
+    int64_t c = 0;
+    int32_t k = 0, max_nseq = 1;
+    for (size_t u = 0; u < units.size(); ++u) {
+        const int32_t seq0 = units[u][0], nseq = units[u][1], n_tok = units[u][2];
+        max_nseq = std::max(max_nseq, nseq);
+        for (int32_t i = seq0; i < seq0 + nseq; ++i) {
+            p->seq_pre_item[i] = (int32_t)(u * p->Hkv);
+            p->seq_pre_row[i] = (i - seq0) * p->G;
+            p->seq_prefix_len[i] = n_tok;
+        }
+        for (int32_t g = 0; g < p->Hkv; ++g) {
+            fka::PrefixItem it{};
+            it.seq0 = seq0;
+            it.nseq = nseq;
+            it.kv_head = g;
+            it.n_tok = n_tok;
+            it.c0 = (int32_t)c;
+            it.k0 = k;
+            p->pre.push_back(it);
+            const int32_t sz = fka::slices_of(n_tok);
+            c += sz;
+            k += sz > 0;
+        }
+    }
+    if (c > (int64_t)1 << 30) return fail(FKA_ERR_UNSUPPORTED, "prefix of %lld slices is too long", (long long)c);
+    p->pre_slices = (int32_t)c;
+    p->pre_nonempty = k;
+    p->n_items = (int32_t)p->pre.size() + p->n_seqs * p->Hkv;
+    p->slot_rows = max_nseq * p->G;
+    p->row_tiles = ceil_div(p->slot_rows, 16);
+
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    int cus = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
+        return hip_fail(e, "hipDeviceGetAttribute");
+    const int per_cu = fka::partials_blocks_per_cu(p->d, p->row_tiles, p->paged);
+    p->waves = fka::partials_waves_per_block(p->d, p->row_tiles);
+    if (per_cu <= 0 || p->waves <= 0) return fail(FKA_ERR_HIP, "occupancy query of the partial kernel failed");
+    p->n_blocks = cus * per_cu;
+    // at least two workers per item, so that A = workers - non-empty items stays >= half
+    const int32_t per_round = p->n_blocks * p->waves;
+    const int32_t need = ceil_div(2 * (int64_t)p->n_items, per_round);
+    p->rounds = std::max<int32_t>(std::max<int32_t>(1, need), rounds_req);
+    p->n_slots = p->n_blocks * p->rounds + p->n_items;
+    return FKA_OK;
+}
+
+// Allocate device memory for the schedule tables, error flag, snapshot and workspace,
+// and upload the tables.
+fka_status finish_plan(fka_plan *p)
+{
+    hipError_t e;
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    const size_t b_pre = up(std::max<size_t>(1, p->pre.size()) * sizeof(fka::PrefixItem));
+    const size_t b_seq = up((size_t)p->n_seqs * sizeof(int32_t));
+    const size_t b_err = 256;
+    const size_t b_sched = up((size_t)fka::sched_words(p->n_seqs) * sizeof(int32_t));
+    const size_t b_po = up((size_t)p->n_slots * p->slot_rows * p->d * sizeof(float));
+    const size_t b_pl = up((size_t)p->n_slots * p->slot_rows * sizeof(float));
+    const size_t total = b_pre + 3 * b_seq + b_err + b_sched + b_po + b_pl;
+    e = hipMalloc(&p->mem, total);
+    if (e != hipSuccess) {
+        p->mem = nullptr;
+        (void)hipGetLastError();
+        return fail(FKA_ERR_NOMEM, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
+    }
+    char *m = static_cast<char *>(p->mem);
+    p->d_pre = reinterpret_cast<fka::PrefixItem *>(m);
+    m += b_pre;
+    p->d_seq_pre_item = reinterpret_cast<int32_t *>(m);
+    m += b_seq;
+    p->d_seq_pre_row = reinterpret_cast<int32_t *>(m);
+    m += b_seq;
+    p->d_seq_prefix_len = reinterpret_cast<int32_t *>(m);
+    m += b_seq;
+    p->err = reinterpret_cast<int32_t *>(m);
+    m += b_err;
+    p->sched = reinterpret_cast<int32_t *>(m);
+    m += b_sched;
+    p->part_o = reinterpret_cast<float *>(m);
+    m += b_po;
+    p->part_lse = reinterpret_cast<float *>(m);
+    p->workspace_bytes = total;
+    auto put = [&](void *dst, const void *src, size_t bytes, const char *what) -> fka_status {
+        if (bytes == 0) return FKA_OK;
+        const hipError_t r = hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice);
+        return r == hipSuccess ? FKA_OK : hip_fail(r, what);
+    };
+    fka_status st;
+    if ((st = put(p->d_pre, p->pre.data(), p->pre.size() * sizeof(fka::PrefixItem), "hipMemcpy(prefix items)")) != FKA_OK ||
+        (st = put(p->d_seq_pre_item, p->seq_pre_item.data(), b_seq, "hipMemcpy(sequence tables)")) != FKA_OK ||
+        (st = put(p->d_seq_pre_row, p->seq_pre_row.data(), b_seq, "hipMemcpy(sequence tables)")) != FKA_OK ||
+        (st = put(p->d_seq_prefix_len, p->seq_prefix_len.data(), b_seq, "hipMemcpy(sequence tables)")) != FKA_OK)
+        return st;
+    if ((e = hipMemset(p->err, 0, b_err + b_sched)) != hipSuccess) return hip_fail(e, "hipMemset(flags)");
     return FKA_OK;
 }
 
 fka::AttnArgs attn_args(const fka_plan *p)
 {
     fka::AttnArgs a{};
-    a.items = p->items;
+    a.pre_items = p->d_pre;
+    a.n_pre = (int32_t)p->pre.size();
+    a.pre_slices = p->pre_slices;
+    a.pre_nonempty = p->pre_nonempty;
+    a.seq_prefix_len = p->d_seq_prefix_len;
+    a.sched = p->sched;
     a.max_suffix_len = p->max_suffix_len;
     a.n_seqs = p->n_seqs;
     a.n_q_heads = p->Hq;
@@ -203,15 +242,14 @@ fka::AttnArgs attn_args(const fka_plan *p)
     a.scale_log2 = p->scale * 1.4426950408889634f;
     a.part_o = p->part_o;
     a.part_lse = p->part_lse;
+    a.slot_rows = p->slot_rows;
+    a.n_slots = p->n_slots;
     a.err = p->err;
     a.prefix_len = p->prefix_len;
     a.suffix_cap = p->suffix_cap;
     a.max_pages = p->max_pages;
     a.n_pool_pages = p->n_pool_pages;
     a.paged = p->paged ? 1 : 0;
-    a.n_items = p->n_items;
-    a.queue = p->queue;
-    a.done = p->done;
     return a;
 }
 
@@ -225,14 +263,19 @@ fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *o
     m.rows = p->n_seqs * p->Hq;
     m.n_q_heads = p->Hq;
     m.n_parts = 0;
-    m.seq_prefix_parts = p->seq_prefix_parts;
-    m.max_prefix_parts = p->max_prefix_parts;
+    m.sched = p->sched;
+    m.pre_items = p->d_pre;
+    m.seq_pre_item = p->d_seq_pre_item;
+    m.seq_pre_row = p->d_seq_pre_row;
+    m.n_pre = (int32_t)p->pre.size();
+    m.pre_slices = p->pre_slices;
+    m.pre_nonempty = p->pre_nonempty;
+    m.waves = p->waves;
+    m.slot_rows = p->slot_rows;
     m.suffix_len = const_cast<int32_t *>(suffix_len);  // only a fused step writes it
-    m.suffix_split = p->ssplit;
     m.max_suffix_len = p->max_suffix_len;
     m.err = p->err;
-    m.counter = p->counter;
-    m.seq_prefix_len = p->seq_prefix_len;
+    m.seq_prefix_len = p->d_seq_prefix_len;
     m.suffix_cap = p->suffix_cap;
     m.max_pages = p->max_pages;
     m.n_pool_pages = p->n_pool_pages;
@@ -246,7 +289,7 @@ fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *o
 fka_status run_decode(const fka_plan *p, const fka::AttnArgs &a, const int32_t *suffix_len, float *out,
                       float *out_lse, hipStream_t s, const fka::MergeArgs *step = nullptr)
 {
-    hipError_t e = fka::launch_partials(a, p->n_blocks, p->d, p->row_tiles, s);
+    hipError_t e = fka::launch_partials(a, p->n_blocks * p->rounds, p->d, p->row_tiles, s);
     if (e != hipSuccess) return hip_fail(e, "partials kernel launch");
     e = fka::launch_merge(step ? *step : merge_args(p, suffix_len, out, out_lse), p->d, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
@@ -257,7 +300,7 @@ fka_status run_decode(const fka_plan *p, const fka::AttnArgs &a, const int32_t *
 
 extern "C" {
 
-int fka_version(void) { return 10000; }
+int fka_version(void) { return 20000; }
 
 const char *fka_last_error(void) { return g_err; }
 
@@ -274,7 +317,9 @@ fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc 
     REQUIRE(desc->max_suffix_len >= 0 && desc->max_suffix_len <= desc->suffix_cap,
             "max_suffix_len (%d) must be in [0, suffix_cap=%d]", desc->max_suffix_len, desc->suffix_cap);
     REQUIRE(desc->share_prefix == 0 || desc->share_prefix == 1, "share_prefix must be 0 or 1");
-    if ((st = check_split(desc->split_tokens)) != FKA_OK) return st;
+    if ((st = check_rounds(desc->rounds)) != FKA_OK) return st;
+    if (desc->n_branches > fka::kMaxSeqs)
+        return fail(FKA_ERR_UNSUPPORTED, "%d sequences exceed the limit of %d", desc->n_branches, fka::kMaxSeqs);
     const int G = heads->n_q_heads / heads->n_kv_heads;
     const int rows = (desc->share_prefix ? desc->n_branches : 1) * G;
     if (G > fka::kMaxRows || rows > fka::kMaxRows)
@@ -288,32 +333,12 @@ fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc 
     p->prefix_len = desc->prefix_len;
     p->suffix_cap = desc->suffix_cap;
     p->max_suffix_len = desc->max_suffix_len;
-    const int64_t reads = (int64_t)desc->prefix_len * p->Hkv * (desc->share_prefix ? 1 : desc->n_branches);
-    p->split = desc->split_tokens ? desc->split_tokens : auto_split(reads);
-    p->ssplit = auto_suffix_split(desc->max_suffix_len);
-    p->max_prefix_parts = desc->prefix_len > 0 ? ceil_div(desc->prefix_len, p->split) : 0;
-    p->n_suffix_parts = desc->max_suffix_len > 0 ? ceil_div(desc->max_suffix_len, p->ssplit) : 0;
-    p->slots = p->max_prefix_parts + p->n_suffix_parts;
-    p->row_tiles = ceil_div(rows, 16);
-
-    std::vector<WorkItem> items;
-    const int N = desc->n_branches;
-    for (int part = 0; part < p->max_prefix_parts; ++part)
-        for (int g = 0; g < p->Hkv; ++g) {
-            const int b0 = part * p->split, b1 = std::min(desc->prefix_len, b0 + p->split);
-            if (desc->share_prefix)
-                items.push_back({fka::kPrefix, 0, N, g, b0, b1, part, desc->prefix_len});
-            else
-                for (int b = 0; b < N; ++b) items.push_back({fka::kPrefix, b, 1, g, b0, b1, part, desc->prefix_len});
-        }
-    for (int s = 0; s < p->n_suffix_parts; ++s)
-        for (int b = 0; b < N; ++b)
-            for (int g = 0; g < p->Hkv; ++g)
-                items.push_back({fka::kSuffix, b, 1, g, s * p->ssplit, (s + 1) * p->ssplit, p->max_prefix_parts + s,
-                                 desc->prefix_len});
-    std::vector<int32_t> spp(N, p->max_prefix_parts), spl(N, desc->prefix_len);
-    st = finish_plan(p, items, spp, spl);
-    if (st != FKA_OK) {
+    std::vector<std::array<int32_t, 3>> units;
+    if (desc->share_prefix)
+        units.push_back({0, desc->n_branches, desc->prefix_len});
+    else
+        for (int b = 0; b < desc->n_branches; ++b) units.push_back({b, 1, desc->prefix_len});
+    if ((st = build_schedule(p, units, desc->rounds)) != FKA_OK || (st = finish_plan(p)) != FKA_OK) {
         fka_plan_destroy(p);
         return st;
     }
@@ -336,12 +361,11 @@ fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *d
     REQUIRE(desc->n_pool_pages >= 1, "n_pool_pages must be >= 1");
     REQUIRE(desc->max_suffix_len >= 0, "max_suffix_len must be >= 0");
     REQUIRE(desc->share_prefix == 0 || desc->share_prefix == 1, "share_prefix must be 0 or 1");
-    if ((st = check_split(desc->split_tokens)) != FKA_OK) return st;
+    if ((st = check_rounds(desc->rounds)) != FKA_OK) return st;
     REQUIRE(host_group_start[0] == 0 && host_group_start[desc->n_groups] == desc->n_seqs,
             "group_start must begin at 0 and end at n_seqs");
     const int G = heads->n_q_heads / heads->n_kv_heads;
     int max_group = 0;
-    int64_t reads = 0;
     for (int t = 0; t < desc->n_groups; ++t) {
         const int n = host_group_start[t + 1] - host_group_start[t];
         REQUIRE(n >= 1, "group %d is empty", t);
@@ -351,8 +375,9 @@ fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *d
         REQUIRE(pages <= desc->max_pages_per_seq, "group %d needs %lld pages, max_pages_per_seq is %d", t,
                 (long long)pages, desc->max_pages_per_seq);
         max_group = std::max(max_group, n);
-        reads += (int64_t)lp * heads->n_kv_heads * (desc->share_prefix ? 1 : n);
     }
+    if (desc->n_seqs > fka::kMaxSeqs)
+        return fail(FKA_ERR_UNSUPPORTED, "%d sequences exceed the limit of %d", desc->n_seqs, fka::kMaxSeqs);
     const int rows = (desc->share_prefix ? max_group : 1) * G;
     if (G > fka::kMaxRows || rows > fka::kMaxRows)
         return fail(FKA_ERR_UNSUPPORTED, "%d query rows per KV head exceed the limit of %d", rows, fka::kMaxRows);
@@ -370,51 +395,15 @@ fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *d
     p->max_suffix_len = desc->max_suffix_len;
     p->group_start.assign(host_group_start, host_group_start + desc->n_groups + 1);
     p->group_prefix_len.assign(host_group_prefix_len, host_group_prefix_len + desc->n_groups);
-    p->split = desc->split_tokens ? desc->split_tokens : auto_split(reads);
-    p->ssplit = auto_suffix_split(desc->max_suffix_len);
-    int maxp = 0;
-    for (int t = 0; t < desc->n_groups; ++t)
-        maxp = std::max(maxp, p->group_prefix_len[t] > 0 ? ceil_div(p->group_prefix_len[t], p->split) : 0);
-    p->max_prefix_parts = maxp;
-    p->n_suffix_parts = desc->max_suffix_len > 0 ? ceil_div(desc->max_suffix_len, p->ssplit) : 0;
-    p->slots = p->max_prefix_parts + p->n_suffix_parts;
-    p->row_tiles = ceil_div(rows, 16);
-
-    std::vector<WorkItem> items;
-    std::vector<int32_t> spp(desc->n_seqs), spl(desc->n_seqs);
-    // prefix items, longest groups first so that the tail of the grid holds short items
-    std::vector<int> order(desc->n_groups);
-    for (int t = 0; t < desc->n_groups; ++t) order[t] = t;
-    std::stable_sort(order.begin(), order.end(),
-                     [&](int x, int y) { return p->group_prefix_len[x] > p->group_prefix_len[y]; });
-    for (int part = 0; part < maxp; ++part)
-        for (int t : order) {
-            const int lp = p->group_prefix_len[t];
-            const int b0 = part * p->split;
-            if (b0 >= lp) continue;
-            const int b1 = std::min(lp, b0 + p->split);
-            const int s0 = p->group_start[t], s1 = p->group_start[t + 1];
-            for (int g = 0; g < p->Hkv; ++g) {
-                if (desc->share_prefix)
-                    items.push_back({fka::kPrefix, s0, s1 - s0, g, b0, b1, part, lp});
-                else
-                    for (int i = s0; i < s1; ++i) items.push_back({fka::kPrefix, i, 1, g, b0, b1, part, lp});
-            }
-        }
-    for (int t = 0; t < desc->n_groups; ++t)
-        for (int i = p->group_start[t]; i < p->group_start[t + 1]; ++i) {
-            const int lp = p->group_prefix_len[t];
-            spp[i] = lp > 0 ? ceil_div(lp, p->split) : 0;
-            spl[i] = lp;
-        }
-    for (int s = 0; s < p->n_suffix_parts; ++s)
-        for (int t = 0; t < desc->n_groups; ++t)
-            for (int i = p->group_start[t]; i < p->group_start[t + 1]; ++i)
-                for (int g = 0; g < p->Hkv; ++g)
-                    items.push_back({fka::kSuffix, i, 1, g, s * p->ssplit, (s + 1) * p->ssplit,
-                                     p->max_prefix_parts + s, p->group_prefix_len[t]});
-    st = finish_plan(p, items, spp, spl);
-    if (st != FKA_OK) {
+    std::vector<std::array<int32_t, 3>> units;
+    for (int t = 0; t < desc->n_groups; ++t) {
+        const int s0 = p->group_start[t], s1 = p->group_start[t + 1], lp = p->group_prefix_len[t];
+        if (desc->share_prefix)
+            units.push_back({s0, s1 - s0, lp});
+        else
+            for (int i = s0; i < s1; ++i) units.push_back({i, 1, lp});
+    }
+    if ((st = build_schedule(p, units, desc->rounds)) != FKA_OK || (st = finish_plan(p)) != FKA_OK) {
         fka_plan_destroy(p);
         return st;
     }
@@ -425,12 +414,80 @@ fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *d
 fka_status fka_plan_get_info(const fka_plan *p, fka_plan_info *info)
 {
     REQUIRE(p != nullptr && info != nullptr, "null argument");
-    info->split_tokens = p->split;
-    info->suffix_split_tokens = p->ssplit;
-    info->max_prefix_parts = p->max_prefix_parts;
-    info->n_suffix_parts = p->n_suffix_parts;
     info->n_items = p->n_items;
+    info->n_prefix_items = (int32_t)p->pre.size();
+    info->waves_per_block = p->waves;
+    info->n_blocks = p->n_blocks;
+    info->rounds = p->rounds;
+    info->n_slots = p->n_slots;
+    info->slot_rows = p->slot_rows;
     info->workspace_bytes = p->workspace_bytes;
+    return ok();
+}
+
+fka_status fka_plan_slots(const fka_plan *p, const int32_t *host_suffix_len, fka_slot *slots, int32_t capacity,
+                          int32_t *n_slots)
+{
+    REQUIRE(p != nullptr && host_suffix_len != nullptr && n_slots != nullptr, "null argument");
+    REQUIRE(capacity >= 0 && (capacity == 0 || slots != nullptr), "slots is null");
+    const int N = p->n_seqs, Hkv = p->Hkv;
+    std::vector<int32_t> len(N), cs(N), ne(N);
+    int64_t c = 0, k = 0;
+    for (int s = 0; s < N; ++s) {
+        len[s] = std::min(std::max(host_suffix_len[s], 0), p->max_suffix_len);
+        cs[s] = (int32_t)c;
+        ne[s] = (int32_t)k;
+        c += (int64_t)fka::slices_of(len[s]) * Hkv;
+        k += len[s] > 0 ? Hkv : 0;
+    }
+    const int64_t T = p->pre_slices + c, NNE = p->pre_nonempty + k;
+    const int64_t NV = (int64_t)p->n_blocks * p->rounds * p->waves;
+    const uint64_t R = T > 0 ? fka::sched_ratio(NV - NNE, T) : 0;
+    int32_t count = 0;
+    const int n_pre = (int)p->pre.size();
+    for (int i = 0; T > 0 && i < p->n_items; ++i) {
+        fka_slot base{};
+        int32_t C, K, size;
+        if (i < n_pre) {
+            const fka::PrefixItem &it = p->pre[i];
+            size = fka::slices_of(it.n_tok);
+            C = it.c0;
+            K = it.k0;
+            base.kind = 0;
+            base.seq0 = it.seq0;
+            base.nseq = it.nseq;
+            base.kv_head = it.kv_head;
+            base.n_tok = it.n_tok;
+        } else {
+            const int j = i - n_pre, s = j / Hkv, g = j % Hkv;
+            size = fka::slices_of(len[s]);
+            C = p->pre_slices + cs[s] + g * size;
+            K = p->pre_nonempty + ne[s] + (size > 0 ? g : 0);
+            base.kind = 1;
+            base.seq0 = s;
+            base.nseq = 1;
+            base.kv_head = g;
+            base.n_tok = len[s];
+        }
+        if (size == 0) continue;
+        const int32_t ws0 = fka::worker_start(C, K, R), ws1 = fka::worker_start(C + size, K + 1, R);
+        for (int32_t vb = ws0 / p->waves; vb <= (ws1 - 1) / p->waves; ++vb) {
+            const int32_t lo = std::max(ws0, vb * p->waves), hi = std::min(ws1, (vb + 1) * p->waves);
+            int32_t a0, a1, b0, b1;
+            fka::worker_range(lo - ws0, ws1 - ws0, size, a0, a1);
+            fka::worker_range(hi - 1 - ws0, ws1 - ws0, size, b0, b1);
+            if (count < capacity) {
+                fka_slot sl = base;
+                sl.slot = vb + i;
+                sl.rows = base.nseq * p->G;
+                sl.tok_begin = std::min(a0 * fka::kSlice, base.n_tok);
+                sl.tok_end = std::min(b1 * fka::kSlice, base.n_tok);
+                slots[count] = sl;
+            }
+            ++count;
+        }
+    }
+    *n_slots = count;
     return ok();
 }
 
@@ -484,7 +541,7 @@ fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, 
     a.suffix_len = suffix_len;
     a.part_o = part_o;
     a.part_lse = part_lse;
-    hipError_t e = fka::launch_partials(a, p->n_blocks, p->d, p->row_tiles, static_cast<hipStream_t>(stream));
+    hipError_t e = fka::launch_partials(a, p->n_blocks * p->rounds, p->d, p->row_tiles, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "partials kernel launch");
     return ok();
 }
@@ -619,7 +676,7 @@ fka_status fka_append_kv_paged(const fka_plan *p, const void *k_new, const void 
     a.k_dst = static_cast<uint16_t *>(k_pool);
     a.v_dst = static_cast<uint16_t *>(v_pool);
     a.page_table = page_table;
-    a.seq_prefix_len = p->seq_prefix_len;
+    a.seq_prefix_len = p->d_seq_prefix_len;
     a.suffix_len = suffix_len;
     a.max_pages = p->max_pages;
     a.n_pool_pages = p->n_pool_pages;

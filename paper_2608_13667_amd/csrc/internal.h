@@ -6,28 +6,82 @@
 
 namespace fka {
 
-// Where a work item's keys come from.
-enum ItemKind : int32_t {
-    kPrefix = 0,  // shared prefix of the item's sequence group
-    kSuffix = 1,  // own suffix of sequence seq0 (nseq == 1); clipped by suffix_len at run time
+constexpr int kSlice = 32;      // tokens a wave scores per step; work is balanced in whole slices
+constexpr int kPageSize = 16;
+constexpr int kMaxRows = 64;    // query rows (sequences x G) per KV head that one item can hold
+constexpr int kMaxSeqs = 512;   // sequences per plan (per-sequence schedule tables live in LDS)
+
+// ---------------------------------------------------------------------------------------
+// Work schedule shared by the partial kernel, the merge kernel and the host.
+//
+// The keys are cut into items, in this fixed order:
+//   prefix items  i = u * Hkv + g            (u = prefix unit: a sequence group when the
+//                                              prefix is shared, else one sequence)
+//   suffix items  i = n_pre + s * Hkv + g    (sequence s, KV head g)
+// Item i holds size_i = ceil(tokens_i / kSlice) slices; C_i is the number of slices of the
+// items before it and K_i the number of non-empty items before it.  Suffix sizes follow
+// the suffix lengths on the device, so the schedule is rebuilt by every launch.
+//
+// The launch has NV workers (waves), NV = waves per block x virtual blocks.  With
+// T = total slices, A = NV - (non-empty items) and the 32.32 fixed-point ratio
+// R = floor(A * 2^32 / T), item i owns workers [WS(i), WS(i+1)) with
+// WS(i) = floor(C_i * R / 2^32) + K_i: an empty item owns none, every other item at least
+// one and about size_i * A / T of them; the items end at WS(n_items), NV - 1 or NV, and a
+// worker past that end has no work.  Worker j of an item with w workers scores slices
+// [floor(j*size/w), floor((j+1)*size/w)).
+//
+// The waves of block vb are workers [vb*NW, (vb+1)*NW).  They combine their
+// results per item, and the partial of (vb, item i) goes to slot vb + i: along the
+// order of work each step advances vb, i or both, so slots are distinct and fewer than
+// (blocks + items).  The merge reads, for an item, the slots of every block that owns
+// one of its workers; each of those blocks writes its slot, empty or not.
+// ---------------------------------------------------------------------------------------
+struct PrefixItem {  // eight int32 fields, read field by field on the device
+    int32_t seq0;     // first sequence of the item's rows
+    int32_t nseq;     // sequences of the item's rows (rows = nseq * G)
+    int32_t kv_head;
+    int32_t n_tok;    // prefix length of the unit
+    int32_t c0;       // slices of the prefix items before this one
+    int32_t k0;       // non-empty prefix items before this one
+    int32_t pad0, pad1;
 };
 
-// One block of the partial-attention kernel: query rows of sequences
-// [seq0, seq0 + nseq) x the G query heads of kv_head, over keys
-// [tok_begin, tok_end) of the item's source; result goes to partial slot `part`.
-struct WorkItem {  // eight int32 fields, read field by field on the device
-    int32_t kind;
-    int32_t seq0;
-    int32_t nseq;
-    int32_t kv_head;
-    int32_t tok_begin;
-    int32_t tok_end;
-    int32_t part;
-    int32_t prefix_len;  // prefix length of the sequence group (paged suffix page offset)
-};
+// Per-launch schedule snapshot written by the partial kernel (block 0) for the merge.
+// int32 words: [0] T, [1] non-empty items, [2] NV, [3] unused, then for sequence s:
+// [4 + 3s] clamped suffix length, [5 + 3s] CS(s), [6 + 3s] NE(s), where CS(s) and NE(s)
+// count the slices and the non-empty items of the suffix items of sequences before s.
+constexpr int kSchedHeader = 4;
+__host__ __device__ inline int sched_words(int n_seqs) { return kSchedHeader + 3 * n_seqs; }
+
+__host__ __device__ inline int32_t slices_of(int32_t tokens) { return (tokens + kSlice - 1) / kSlice; }
+
+// Fixed-point ratio workers per slice, R = floor(A * 2^32 / T) (A < 2^31, T > 0).
+__host__ __device__ inline uint64_t sched_ratio(int64_t A, int64_t T)
+{
+    return ((uint64_t)A << 32) / (uint64_t)T;
+}
+
+// First worker of an item that starts at slice C (C <= T, so C * R < 2^63) with K
+// non-empty items before it.
+__host__ __device__ inline int32_t worker_start(int64_t C, int64_t K, uint64_t R)
+{
+    return (int32_t)(((uint64_t)C * R) >> 32) + (int32_t)K;
+}
+
+// Slice range [lo, hi) of worker j of an item with `size` slices and w workers.
+__host__ __device__ inline void worker_range(int32_t j, int32_t w, int32_t size, int32_t &lo, int32_t &hi)
+{
+    lo = (int32_t)((int64_t)j * size / w);
+    hi = (int32_t)((int64_t)(j + 1) * size / w);
+}
 
 struct AttnArgs {
-    const WorkItem *items;
+    const PrefixItem *pre_items;  // [n_pre]
+    int32_t n_pre;
+    int32_t pre_slices;   // sum of the prefix items' slices
+    int32_t pre_nonempty; // non-empty prefix items
+    const int32_t *seq_prefix_len;  // [S] prefix length of each sequence's unit (paged page offsets)
+    int32_t *sched;       // per-launch snapshot for the merge
     const uint16_t *q;  // [S][Hq][d]
     // contiguous layout
     const uint16_t *prefix_k, *prefix_v;  // [Hkv][Lp][d]
@@ -47,40 +101,41 @@ struct AttnArgs {
     int32_t n_kv_heads;
     int32_t group;
     float scale_log2;  // softmax scale * log2(e)
-    float *part_o;     // [slots][S][Hq][d]
-    float *part_lse;   // [slots][S][Hq]
+    float *part_o;     // [slots][slot_rows][d]
+    float *part_lse;   // [slots][slot_rows]
+    int32_t slot_rows;
+    int32_t n_slots;
     int32_t *err;
-    // persistent scheduling
-    int32_t n_items;
-    int32_t *queue;          // next item to hand out; zero between launches
-    int32_t *done;           // blocks finished; zero between launches
 };
 
 struct MergeArgs {
-    const float *part_o;    // [slots][rows][d]
-    const float *part_lse;  // [slots][rows]
+    const float *part_o;    // explicit mode [n_parts][rows][d]; plan mode [slots][slot_rows][d]
+    const float *part_lse;  // explicit mode [n_parts][rows];    plan mode [slots][slot_rows]
     float *out;             // [rows][d]
     float *out_lse;         // [rows] or null
     int32_t rows;
-    int32_t n_q_heads;       // rows of one sequence (plan-driven mode)
-    // explicit mode: every row merges parts 0..n_parts-1
+    int32_t n_q_heads;       // rows of one sequence (plan mode)
+    // explicit mode (sched == null): every row merges parts 0..n_parts-1
     int32_t n_parts;
-    // plan-driven mode (seq_prefix_parts != null): row of sequence s merges its
-    // group's prefix parts 0..seq_prefix_parts[s]-1 and suffix parts
-    // max_prefix_parts + j for j < ceil(min(suffix_len[s], max_suffix_len) / suffix_split)
-    const int32_t *seq_prefix_parts;
-    int32_t max_prefix_parts;
-    int32_t *suffix_len;  // written only by a fused step
-    int32_t suffix_split;
-    int32_t max_suffix_len;
+    // plan mode: row (s, h) merges the slots of its prefix item and of its suffix item
+    const int32_t *sched;         // snapshot written by the partial kernel
+    const PrefixItem *pre_items;
+    const int32_t *seq_pre_item;  // [S] prefix item of (s, head 0), -1 if none
+    const int32_t *seq_pre_row;   // [S] first row of s within its prefix item
+    int32_t n_pre;
+    int32_t pre_slices;
+    int32_t pre_nonempty;
+    int32_t waves;          // NW: workers per virtual block
+    int32_t slot_rows;
     int32_t *err;
     // fused step: the token in k_new / v_new (not yet in the cache) joins each row as one
-    // more part; the last block then appends it and advances suffix_len
+    // more part; block (s, head 0) then stores it and advances suffix_len[s]
     int32_t step_mode;
+    int32_t *suffix_len;  // written only by a fused step
+    int32_t max_suffix_len;
     const uint16_t *q;  // [S][Hq][d]
     float scale;        // softmax scale (natural-log units)
     int32_t group;      // G = Hq / Hkv
-    int32_t *counter;               // zero between launches
     const uint16_t *k_new, *v_new;  // [S][Hkv][d]
     uint16_t *k_dst, *v_dst;        // suffix buffers or pools
     const int32_t *page_table;
@@ -127,11 +182,11 @@ constexpr int32_t kErrSuffixClamped = 1;
 constexpr int32_t kErrAppendNoRoom = 2;
 constexpr int32_t kErrBadPage = 4;
 
-constexpr int kTileTokens = 128;  // split sizes are whole multiples of this many tokens
-constexpr int kPageSize = 16;
-constexpr int kMaxRows = 64;      // query rows (sequences x G) per KV head that one item can hold
-
 hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);
+// Resident blocks per compute unit of the partial kernel for this shape (0 on error).
+int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged);
+// Waves per block of the partial kernel for this shape.
+int partials_waves_per_block(int head_dim, int row_tiles);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);

@@ -19,40 +19,69 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
     constexpr int SL = 256 / CH;        // part slices
     constexpr int MAXP = 1024;          // parts weighed per pass
     __shared__ float s_w[MAXP];
-    __shared__ int s_p[MAXP];
+    __shared__ int s_off[MAXP];
     __shared__ f32x4 s_acc[SL][CH];
     __shared__ float s_red[4];
     __shared__ float s_new;
-    __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int chunk = tid % CH, slice = tid / CH;
     const int row = blockIdx.x;
-    const size_t rows = (size_t)a.rows;
 
-    int npre, nsuf, suf0;
+    // Parts of this row, as offsets (part index * row stride + row) into part_o / part_lse:
+    // parts [0, np) start at p_first with stride p_step; parts [np, n) at s_first.
+    int np = 0, n = 0;
+    int64_t p_first = 0, p_step = 0, s_first = 0;
+    int L = 0;
     bool with_new = false;  // fused step: the appended token is one more part, read from k_new / v_new
-    if (a.seq_prefix_parts) {
-        const int seq = row / a.n_q_heads;
-        npre = a.seq_prefix_parts[seq];
-        const int Lraw = a.suffix_len[seq];
-        const int L = min(max(Lraw, 0), a.max_suffix_len);
-        if (!a.step_mode && L != Lraw && tid == 0 && row % a.n_q_heads == 0) atomicOr(a.err, kErrSuffixClamped);
-        nsuf = (L + a.suffix_split - 1) / a.suffix_split;
-        suf0 = a.max_prefix_parts;
+    int seq = 0, g = 0;
+    if (a.sched) {
+        seq = row / a.n_q_heads;
+        const int h = row % a.n_q_heads;
+        g = h / a.group;
+        const int hr = h % a.group;
+        const int T = a.sched[0], NNE = a.sched[1], NV = a.sched[2];
+        const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
+        L = a.sched[kSchedHeader + 3 * seq];
+        const int CS = a.sched[kSchedHeader + 3 * seq + 1], NE = a.sched[kSchedHeader + 3 * seq + 2];
+        const int64_t stride = a.slot_rows;
+        if (T > 0) {
+            const int ip0 = a.seq_pre_item[seq];
+            if (ip0 >= 0) {
+                const int ip = ip0 + g;
+                const PrefixItem pi = a.pre_items[ip];
+                const int size = slices_of(pi.n_tok);
+                if (size > 0) {
+                    const int ws0 = worker_start(pi.c0, pi.k0, R), ws1 = worker_start(pi.c0 + size, pi.k0 + 1, R);
+                    const int vb0 = ws0 / a.waves, vb1 = (ws1 - 1) / a.waves;
+                    np = vb1 - vb0 + 1;
+                    p_first = (int64_t)(vb0 + ip) * stride + a.seq_pre_row[seq] + hr;
+                }
+            }
+            const int ns = slices_of(L);
+            n = np;
+            if (ns > 0) {
+                const int is = a.n_pre + seq * a.n_kv_heads + g;
+                const int C = a.pre_slices + CS + g * ns, K = a.pre_nonempty + NE + g;
+                const int ws0 = worker_start(C, K, R), ws1 = worker_start(C + ns, K + 1, R);
+                const int vb0 = ws0 / a.waves, vb1 = (ws1 - 1) / a.waves;
+                n = np + vb1 - vb0 + 1;
+                s_first = (int64_t)(vb0 + is) * stride + hr;
+            }
+        }
+        p_step = stride;
         with_new = a.step_mode && L < a.max_suffix_len;
     } else {
-        npre = a.n_parts;
-        nsuf = 0;
-        suf0 = 0;
+        np = n = a.n_parts;
+        p_first = row;
+        p_step = a.rows;
     }
-    const int n = npre + nsuf;
+    auto part_off = [&](int j) -> int64_t { return j < np ? p_first + j * p_step : s_first + (j - np) * p_step; };
 
     // the appended token alone: o = v_new, lse = its scaled score (wave 0 forms the dot product)
     float lse_new = -INFINITY;
     if (with_new) {
         if (wave == 0) {
-            const int seq = row / a.n_q_heads, h = row % a.n_q_heads, g = h / a.group;
             const uint16_t *qr = a.q + (size_t)row * HD;
             const uint16_t *kr = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
             float dot = 0.f;
@@ -68,10 +97,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 
     // block max of the parts' log-sum-exp values
     float M = lse_new;
-    for (int i = tid; i < n; i += 256) {
-        const int p = i < npre ? i : suf0 + (i - npre);
-        M = fmaxf(M, a.part_lse[(size_t)p * rows + row]);
-    }
+    for (int i = tid; i < n; i += 256) M = fmaxf(M, a.part_lse[part_off(i)]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
     if (lane == 0) s_red[wave] = M;
@@ -85,19 +111,17 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
         for (int base = 0; base < n; base += MAXP) {
             const int cnt = min(MAXP, n - base);
             for (int i = tid; i < cnt; i += 256) {
-                const int j = base + i;
-                const int p = j < npre ? j : suf0 + (j - npre);
-                const float l = a.part_lse[(size_t)p * rows + row];
+                const int64_t off = part_off(base + i);
+                const float l = a.part_lse[off];
                 s_w[i] = (l == -INFINITY) ? 0.f : exp2f((l - M) * kLog2e);
-                s_p[i] = p;
+                s_off[i] = (int)off;
             }
             __syncthreads();
             for (int i = slice; i < cnt; i += SL) {
                 const float w = s_w[i];
                 if (chunk == 0) wsum += w;
                 if (w != 0.f) {
-                    const f32x4 o = *reinterpret_cast<const f32x4 *>(a.part_o + ((size_t)s_p[i] * rows + row) * HD +
-                                                                     4 * chunk);
+                    const f32x4 o = *reinterpret_cast<const f32x4 *>(a.part_o + (size_t)s_off[i] * HD + 4 * chunk);
                     acc += w * o;
                 }
             }
@@ -105,7 +129,6 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
         }
     }
     if (with_new && slice == 0 && M != -INFINITY) {
-        const int seq = row / a.n_q_heads, g = (row % a.n_q_heads) / a.group;
         const uint16_t *vr = a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk;
         const float w = exp2f((lse_new - M) * kLog2e);
         if (chunk == 0) wsum += w;
@@ -128,51 +151,35 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
     }
     if (a.out_lse && tid == 0) a.out_lse[row] = (W == 0.f) ? -INFINITY : M + logf(W);
 
-    if (!a.step_mode) return;
-    // Fused step: the last block to finish stores the token each sequence appended
-    // (already attended to from k_new / v_new) and advances the suffix lengths.
-    // Every block has read the lengths before it increments the counter.
-    __syncthreads();
+    // Fused step: block (s, head 0) stores the token sequence s appended (already attended
+    // to from k_new / v_new) and advances suffix_len[s].  No block of this kernel reads the
+    // suffix cache or suffix_len (the lengths come from the snapshot), so nothing races.
+    if (!a.step_mode || row % a.n_q_heads != 0) return;
+    bool ok = L < a.max_suffix_len;
+    int page = 0;
+    if (ok && a.paged) {
+        const int pidx = (a.seq_prefix_len[seq] + kPageSize - 1) / kPageSize + L / kPageSize;
+        page = pidx < a.max_pages ? a.page_table[(size_t)seq * a.max_pages + pidx] : -1;
+        ok = page >= 0 && page < a.n_pool_pages;
+    }
+    if (ok) {
+        constexpr int cpr = HD / 8;
+        for (int c = tid; c < a.n_kv_heads * cpr; c += 256) {
+            const int gg = c / cpr, cc = c % cpr;
+            const size_t src = ((size_t)seq * a.n_kv_heads + gg) * HD + 8 * cc;
+            const size_t dst =
+                a.paged ? (((size_t)page * a.n_kv_heads + gg) * kPageSize + L % kPageSize) * HD + 8 * cc
+                        : (((size_t)seq * a.n_kv_heads + gg) * a.suffix_cap + L) * HD + 8 * cc;
+            *reinterpret_cast<uint4 *>(a.k_dst + dst) = *reinterpret_cast<const uint4 *>(a.k_new + src);
+            *reinterpret_cast<uint4 *>(a.v_dst + dst) = *reinterpret_cast<const uint4 *>(a.v_new + src);
+        }
+    }
     if (tid == 0) {
-        __threadfence();
-        s_last = (atomicAdd(a.counter, 1) == (int)gridDim.x - 1);
+        if (ok)
+            a.suffix_len[seq] = L + 1;
+        else
+            atomicOr(a.err, kErrAppendNoRoom);
     }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    const int cpr = HD / 8;
-    const int n_seqs = a.rows / a.n_q_heads;
-    for (int seq = 0; seq < n_seqs; ++seq) {
-        const int Lraw = __atomic_load_n(&a.suffix_len[seq], __ATOMIC_RELAXED);
-        const int L = min(max(Lraw, 0), a.max_suffix_len);
-        bool ok = L < a.max_suffix_len;
-        int page = 0;
-        if (ok && a.paged) {
-            const int pidx = (a.seq_prefix_len[seq] + kPageSize - 1) / kPageSize + L / kPageSize;
-            page = pidx < a.max_pages ? a.page_table[(size_t)seq * a.max_pages + pidx] : -1;
-            ok = page >= 0 && page < a.n_pool_pages;
-        }
-        if (ok) {
-            for (int c = tid; c < a.n_kv_heads * cpr; c += 256) {
-                const int g = c / cpr, cc = c % cpr;
-                const size_t src = ((size_t)seq * a.n_kv_heads + g) * HD + 8 * cc;
-                const size_t dst =
-                    a.paged ? (((size_t)page * a.n_kv_heads + g) * kPageSize + L % kPageSize) * HD + 8 * cc
-                            : (((size_t)seq * a.n_kv_heads + g) * a.suffix_cap + L) * HD + 8 * cc;
-                *reinterpret_cast<uint4 *>(a.k_dst + dst) = *reinterpret_cast<const uint4 *>(a.k_new + src);
-                *reinterpret_cast<uint4 *>(a.v_dst + dst) = *reinterpret_cast<const uint4 *>(a.v_new + src);
-            }
-        }
-        __syncthreads();
-        if (tid == 0) {
-            if (ok)
-                a.suffix_len[seq] = L + 1;
-            else
-                atomicOr(a.err, kErrAppendNoRoom);
-            if (L != Lraw) atomicOr(a.err, kErrSuffixClamped);
-        }
-    }
-    if (tid == 0) *a.counter = 0;
 }
 
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a)

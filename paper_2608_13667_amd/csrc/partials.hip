@@ -1,17 +1,18 @@
 // Partial attention over key ranges: the streaming stage of fork-aware decode
 // attention on gfx950 (CDNA4, wave64).
 //
-// Work items (see WorkItem) are pulled from a device queue by persistent blocks of
-// four waves.  An item covers one KV head and one key range and holds every query
-// row that reads those keys: for a shared-prefix item, all sequences of the fork x
-// the G query heads of the KV head, so each prefix K/V byte is fetched from HBM
-// once for all branches (paper, Sec. 3.3: the prefix cache is reused by all
-// decoding streams).  The block's four waves split the item into 32-token slices
-// and stream them independently:
+// Every launch first rebuilds the work schedule (internal.h) from the suffix lengths on
+// the device: the 32-token slices of the shared prefix items and of the suffix items are
+// spread evenly over all waves of the grid.  The waves of a block that share an item take
+// the slices of their joint range one at a time from an LDS counter, so the block streams
+// one contiguous region and its waves finish together.  An item holds every query row that reads its keys: for a
+// shared-prefix item, all sequences of the fork x the G query heads of the KV head, so
+// each prefix K/V byte is fetched from HBM once for all branches (paper, Sec. 3.3: the
+// prefix cache is reused by all decoding streams).  Within a wave:
 //   * K rows are loaded straight into registers in the MFMA A-operand layout
 //     (16 tokens x 4 lanes x 16 bytes per instruction) one slice ahead;
 //   * V rows are copied by LDS DMA (buffer_load_dwordx4 ... lds) into a wave-private
-//     ring of four slices, three slices ahead, and read back transposed with
+//     ring of two slices, one slice ahead, and read back transposed with
 //     ds_read_b64_tr_b16;
 //   * loads go through buffer resources sized to the rows that exist, so rows past the
 //     end of a key range read as zeros without any per-lane test;
@@ -20,8 +21,10 @@
 //     second product as two bf16 terms (hi + lo), which keeps it accurate to ~2^-16;
 //   * the running maximum is only moved when a score exceeds it by more than 2^8,
 //     so the accumulator is rarely rescaled.
-// The waves' (max, sum, accumulator) are combined through LDS at the end of the
-// item and one normalised partial (o, lse) per row is written.
+// At the end the waves of a block that worked on the same item combine their
+// (max, sum, accumulator) through LDS and write one normalised partial (o, lse) per row.
+// Blocks of eight waves (two per SIMD) where the registers allow it: d = 64, or at most
+// 32 query rows of d = 128; four waves otherwise.
 #include <type_traits>
 #include <utility>
 
@@ -37,14 +40,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(4))) const int32_t const_i32;
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
-constexpr int kSlice = 32;      // tokens per wave step
-#ifndef FKA_PIPELINE_DEPTH
-#define FKA_PIPELINE_DEPTH 1
-#endif
-constexpr int kDepth = FKA_PIPELINE_DEPTH;  // K and V slices in flight ahead of the one being scored
-constexpr int kStages = kDepth + 1;         // V ring stages and K register sets per wave
+constexpr int kStages = 2;  // V ring stages and K register sets per wave: one slice ahead
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr float kRescaleGap = 8.0f;  // log2 units: accumulate with p <= 2^8 before moving the max
 
@@ -144,6 +140,22 @@ __device__ inline void lds_wait_all(vtr_t (&v)[NE][2])
     for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v[e][0]), "+v"(v[e][1]));
 }
 
+// Lane id computed at the point of use (the asm cannot be hoisted or merged with an
+// earlier copy).
+__device__ inline int opaque_lane_id()
+{
+    int v;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(v));
+    return v;
+}
+
+// Block barrier for LDS hand-offs: waits for this wave's LDS operations only, so global
+// stores and prefetches in flight stay in flight (__syncthreads would wait for them too).
+__device__ inline void lds_barrier()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 __device__ inline bf16x8 join_tr16(vtr_t lo, vtr_t hi)
 {
     const s16x4 a = __builtin_bit_cast(s16x4, lo), b = __builtin_bit_cast(s16x4, hi);
@@ -151,9 +163,22 @@ __device__ inline bf16x8 join_tr16(vtr_t lo, vtr_t hi)
     return __builtin_bit_cast(bf16x8, v);
 }
 
-template <int HD, int NT, bool PAGED>
-__global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
+// Waves per SIMD the register budget is built for: two (<= 256 VGPRs each) unless the
+// accumulators of three or four 16-row tiles of d = 128 need the whole register file.
+// Waves per SIMD the register budget is built for: two (<= 256 VGPRs each) unless the
+// accumulators of three or four 16-row tiles of d = 128 need the whole register file.
+template <int HD, int NT>
+constexpr int waves_per_simd()
 {
+    return (HD <= 64 || NT <= 2) ? 2 : 1;
+}
+
+template <int HD, int NT, bool PAGED>
+__global__ __launch_bounds__((256 * waves_per_simd<HD, NT>()))
+__attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_kernel(AttnArgs a)
+{
+    constexpr int NW = 4 * waves_per_simd<HD, NT>();  // waves per block
+    constexpr int NTH = 64 * NW;
     constexpr int CPR = HD / 8;                 // 16-byte chunks per K/V row
     constexpr int NC = HD / 32;                 // MFMA k-steps of q.k
     constexpr int NE = HD / 16;                 // MFMA d-tiles of p.v
@@ -161,88 +186,227 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
     constexpr int VDMA = SLICE_CHUNKS / 64;     // LDS DMA instructions per V slice
     constexpr int KLOADS = 2 * NC;              // K loads per lane per slice
     static_assert(VDMA == KLOADS, "one wait count per slice");
-    constexpr int OSTRIDE = HD + 4;             // padded row stride of the output staging (floats)
-    static_assert(kWaves * 16 * OSTRIDE * 4 <= kWaves * kStages * SLICE_CHUNKS * 16, "staging fits");
+    constexpr int ROWB = HD * 2;                // bytes per K/V row
 
     // per wave: kStages V slices; chunk c of slice token T sits at T*CPR + (c ^ swz(T))
-    __shared__ uint4 vring[kWaves][kStages][SLICE_CHUNKS];
-    __shared__ float red_m[kWaves][NT][16];
-    __shared__ float red_l[kWaves][NT][16];
-    __shared__ int s_item;
+    __shared__ uint4 vring[NW][kStages][SLICE_CHUNKS];
+    __shared__ float red_m[NW][NT][16];
+    __shared__ float red_l[NW][NT][16];
+    __shared__ int32_t s_len[kMaxSeqs], s_cs[kMaxSeqs], s_ne[kMaxSeqs];
+    __shared__ int32_t s_wsum[2][NW];
+    __shared__ int32_t s_spl[PAGED ? kMaxSeqs : 1];  // prefix length of each sequence's unit
+    // each wave's item: item, seq0, nseq, kv head, keys, and its group (the block's waves on the
+    // same item): first wave, first slice, end slice, end wave
+    __shared__ int32_t s_wf[NW][9];
+    __shared__ int32_t s_ctr[NW];    // next slice of the group led by this wave
+    __shared__ int32_t s_grp[NW][4];  // the block's groups: first wave, end wave, rows, item
+    __shared__ int32_t s_ngrp;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
     const int l16 = lane & 15, q4 = lane >> 4;
-    const int G = a.group;
+    const int G = a.group, Hkv = a.n_kv_heads, N = a.n_seqs;
 
-    for (;;) {
-        if (tid == 0) s_item = atomicAdd(a.queue, 1);
-        __syncthreads();
-        const int item = __builtin_amdgcn_readfirstlane(s_item);
-        __syncthreads();  // s_item is rewritten at the next fetch
-        if (item >= a.n_items) break;
-
-        WorkItem it;  // scalar loads: every field is uniform across the block
-        {
-            const int32_t *ip = reinterpret_cast<const int32_t *>(a.items + item);
-            it.kind = scalar_load(ip + 0);
-            it.seq0 = scalar_load(ip + 1);
-            it.nseq = scalar_load(ip + 2);
-            it.kv_head = scalar_load(ip + 3);
-            it.tok_begin = scalar_load(ip + 4);
-            it.tok_end = scalar_load(ip + 5);
-            it.part = scalar_load(ip + 6);
-            it.prefix_len = scalar_load(ip + 7);
+    // ---- schedule inputs in one round trip: the suffix lengths (and, paged, the prefix
+    // lengths of the sequences' units) and the static prefix item of this thread's first item
+    int32_t my_pre[6] = {0, 0, 0, 0, 0, 0};  // seq0, nseq, kv_head, n_tok, c0, k0
+    if (tid < a.n_pre) {
+        const int32_t *ip = reinterpret_cast<const int32_t *>(a.pre_items + tid);
+#pragma unroll
+        for (int f = 0; f < 6; ++f) my_pre[f] = ip[f];
+    }
+    // per-sequence suffix tables: clamped length, CS(s), NE(s) (exclusive scans)
+    int carry_cs = 0, carry_ne = 0;
+    bool clamped = false;
+    for (int base = 0; base < N; base += NTH) {
+        const int s = base + tid;
+        int L = 0;
+        if (s < N) {
+            const int raw = a.suffix_len[s];
+            L = min(max(raw, 0), a.max_suffix_len);
+            clamped |= (L != raw);
+            if (PAGED) s_spl[s] = a.seq_prefix_len[s];
         }
-        const int kvh = it.kv_head;
-        const int rows = it.nseq * G;
+        const int xs = slices_of(L) * Hkv, xe = (L > 0) ? Hkv : 0;
+        int x = xs, y = xe;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int ux = __shfl_up(x, off), uy = __shfl_up(y, off);
+            if (lane >= off) {
+                x += ux;
+                y += uy;
+            }
+        }
+        if (lane == 63) {
+            s_wsum[0][wave] = x;
+            s_wsum[1][wave] = y;
+        }
+        lds_barrier();
+        int px = carry_cs, py = carry_ne;
+        for (int w = 0; w < NW; ++w) {
+            if (w < wave) {
+                px += s_wsum[0][w];
+                py += s_wsum[1][w];
+            }
+            carry_cs += s_wsum[0][w];
+            carry_ne += s_wsum[1][w];
+        }
+        if (s < N) {
+            s_len[s] = L;
+            s_cs[s] = px + x - xs;
+            s_ne[s] = py + y - xe;
+        }
+        lds_barrier();
+    }
+    const int T = a.pre_slices + carry_cs;       // total slices of this launch
+    const int NNE = a.pre_nonempty + carry_ne;   // non-empty items
+    const int NV = (int)gridDim.x * NW;  // workers: every block is one virtual block
+    const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
+    const int n_items = a.n_pre + N * Hkv;
+
+    if (blockIdx.x == 0) {  // the snapshot the merge reads
+        for (int s = tid; s < N; s += NTH) {
+            a.sched[kSchedHeader + 3 * s] = s_len[s];
+            a.sched[kSchedHeader + 3 * s + 1] = s_cs[s];
+            a.sched[kSchedHeader + 3 * s + 2] = s_ne[s];
+        }
+        if (tid == 0) {
+            a.sched[0] = T;
+            a.sched[1] = NNE;
+            a.sched[2] = NV;
+            a.sched[3] = 0;
+        }
+        if (clamped) atomicOr(a.err, kErrSuffixClamped);
+    }
+
+    {
+        const int vb = (int)blockIdx.x;
+        const int w_lo = vb * NW;
+        if (tid < NW) s_wf[tid][0] = -1;
+        lds_barrier();
+        // every thread places its items' workers of this block
+        if (T > 0) {
+            for (int i = tid; i < n_items; i += NTH) {
+                int f[6];
+                int size, C, K;
+                if (i < a.n_pre) {
+                    if (i == tid) {  // loaded at the start
+#pragma unroll
+                        for (int k = 0; k < 6; ++k) f[k] = my_pre[k];
+                    } else {
+                        const int32_t *ip = reinterpret_cast<const int32_t *>(a.pre_items + i);
+#pragma unroll
+                        for (int k = 0; k < 6; ++k) f[k] = ip[k];
+                    }
+                    size = slices_of(f[3]);
+                    C = f[4];
+                    K = f[5];
+                } else {
+                    const int j = i - a.n_pre, sq = j / Hkv, g = j % Hkv;
+                    f[0] = sq;
+                    f[1] = 1;
+                    f[2] = g;
+                    f[3] = s_len[sq];
+                    size = slices_of(f[3]);
+                    C = a.pre_slices + s_cs[sq] + g * size;
+                    K = a.pre_nonempty + s_ne[sq] + (size > 0 ? g : 0);
+                }
+                if (size == 0) continue;
+                const int ws0 = worker_start(C, K, R), ws1 = worker_start(C + size, K + 1, R);
+                const int lo = max(ws0, w_lo), hi = min(ws1, w_lo + NW);
+                if (lo >= hi) continue;
+                // the block's workers [lo, hi) of this item form one group over the union of
+                // their slice ranges; its waves take the slices one by one
+                int glo, ghi, dummy;
+                worker_range(lo - ws0, ws1 - ws0, size, glo, dummy);
+                worker_range(hi - 1 - ws0, ws1 - ws0, size, dummy, ghi);
+                s_ctr[lo - w_lo] = glo;
+                for (int gw = lo; gw < hi; ++gw) {
+                    int32_t *d = s_wf[gw - w_lo];
+                    d[0] = i;
+                    d[1] = f[0];
+                    d[2] = f[1];
+                    d[3] = f[2];
+                    d[4] = f[3];
+                    d[5] = lo - w_lo;
+                    d[6] = glo;
+                    d[7] = ghi;
+                    d[8] = hi - w_lo;
+                }
+            }
+        }
+        lds_barrier();
+        const int item = __builtin_amdgcn_readfirstlane(s_wf[wave][0]);
+        if (tid == 0) {  // the block's groups, in wave order (read after the combine barrier)
+            int n = 0;
+            for (int w = 0; w < NW; ++w) {
+                if (s_wf[w][0] < 0 || s_wf[w][5] != w) continue;
+                s_grp[n][0] = w;
+                s_grp[n][1] = s_wf[w][8];
+                s_grp[n][2] = s_wf[w][2] * G;
+                s_grp[n][3] = s_wf[w][0];
+                ++n;
+            }
+            s_ngrp = n;
+        }
+
+        // ---- this wave's item and group (all values uniform)
+        bool suffix = false;
+        int seq0 = 0, nseq = 0, kvh = 0, tok_end = 0, unit_prefix = 0;
+        int wa = wave, wb = wave + 1, ghi = 0;
+        if (item >= 0) {
+            seq0 = __builtin_amdgcn_readfirstlane(s_wf[wave][1]);
+            nseq = __builtin_amdgcn_readfirstlane(s_wf[wave][2]);
+            kvh = __builtin_amdgcn_readfirstlane(s_wf[wave][3]);
+            tok_end = __builtin_amdgcn_readfirstlane(s_wf[wave][4]);
+            wa = __builtin_amdgcn_readfirstlane(s_wf[wave][5]);
+            ghi = __builtin_amdgcn_readfirstlane(s_wf[wave][7]);
+            wb = __builtin_amdgcn_readfirstlane(s_wf[wave][8]);
+            suffix = item >= a.n_pre;
+            if (PAGED && suffix) unit_prefix = __builtin_amdgcn_readfirstlane(s_spl[seq0]);
+        }
+        const int rows = nseq * G;
         const int nt_act = (rows + 15) >> 4;
+        // keys of the group end at tok_lim: loads past it (the prefetch beyond the last slice)
+        // move no data, and scores past it are masked
+        const int tok_lim = min(tok_end, ghi * kSlice);
+        // next slice of the group (LDS counter shared by the group's waves; one lane adds)
+        auto grab = [&]() -> int {
+            int k = 0;
+            if (lane == 0) k = atomicAdd(&s_ctr[wa], 1);
+            return __builtin_amdgcn_readfirstlane(k);
+        };
 
         // key source of the item
-        const char *kbase, *vbase;
-        const int32_t *ptab = nullptr;
+        const char *kbase = reinterpret_cast<const char *>(a.q), *vbase = kbase;
+        const int32_t *ptab = a.page_table;
         int page_off = 0;
-        int tok_end = it.tok_end;
-        if (it.kind == kSuffix) {
-            tok_end = min(tok_end, min(max(scalar_load(a.suffix_len + it.seq0), 0), a.max_suffix_len));
+        if (item >= 0) {
             if (PAGED) {
                 kbase = reinterpret_cast<const char *>(a.k_pool);
                 vbase = reinterpret_cast<const char *>(a.v_pool);
-                ptab = a.page_table + (size_t)it.seq0 * a.max_pages;
-                page_off = (it.prefix_len + kPageSize - 1) / kPageSize;
-            } else {
-                const size_t base = ((size_t)it.seq0 * a.n_kv_heads + kvh) * (size_t)a.suffix_cap * HD * 2;
+                ptab = a.page_table + (size_t)seq0 * a.max_pages;
+                if (suffix) page_off = (unit_prefix + kPageSize - 1) / kPageSize;
+            } else if (suffix) {
+                const size_t base = ((size_t)seq0 * Hkv + kvh) * (size_t)a.suffix_cap * HD * 2;
                 kbase = reinterpret_cast<const char *>(a.suffix_k) + base;
                 vbase = reinterpret_cast<const char *>(a.suffix_v) + base;
-            }
-        } else {
-            if (PAGED) {
-                kbase = reinterpret_cast<const char *>(a.k_pool);
-                vbase = reinterpret_cast<const char *>(a.v_pool);
-                ptab = a.page_table + (size_t)it.seq0 * a.max_pages;
             } else {
                 const size_t base = (size_t)kvh * (size_t)a.prefix_len * HD * 2;
                 kbase = reinterpret_cast<const char *>(a.prefix_k) + base;
                 vbase = reinterpret_cast<const char *>(a.prefix_v) + base;
             }
         }
-        const int n_tok = tok_end - it.tok_begin;
-        if (n_tok <= 0) continue;  // a suffix part past the branch's length: the merge does not read it
+        auto slice_tok0 = [&](int k) { return k * kSlice; };
 
-        // this wave's slices: w, w + 4, w + 8, ... of the item
-        const int n_slices = (n_tok + kSlice - 1) / kSlice;
-        const int ns = n_slices > wave ? (n_slices - wave + kWaves - 1) / kWaves : 0;
-        auto slice_tok0 = [&](int k) { return it.tok_begin + (wave + kWaves * k) * kSlice; };
-        constexpr int ROWB = HD * 2;  // bytes per K/V row
-
-        // Buffer resource over the 16-row group holding item positions [t, t + 16) (t is a
+        // Buffer resource over the 16-row group holding positions [t, t + 16) (t is a
         // multiple of 16, so a group never straddles a page).  Its size covers only the rows
-        // below tok_end, so loads of rows past the end (or of a group wholly past it, or behind
+        // below tok_lim, so loads of rows past the end (or of a group wholly past it, or behind
         // an out-of-range page id) return zeros.  Uniform.
         bool bad_page = false;
         auto group_rsrc = [&](const char *src, int t) -> __amdgpu_buffer_rsrc_t {
-            const int rows_ok = max(0, min(kPageSize, tok_end - t));
+            const int rows_ok = max(0, min(kPageSize, tok_lim - t));
             const char *base = src;
             if (!PAGED) {
                 base = src + (size_t)t * ROWB;
@@ -252,7 +416,7 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
                     bad_page = true;
                     return make_rsrc(src, 0);
                 }
-                base = src + ((size_t)page * a.n_kv_heads + kvh) * (kPageSize * ROWB);
+                base = src + ((size_t)page * Hkv + kvh) * (kPageSize * ROWB);
             }
             return make_rsrc(base, rows_ok * ROWB);
         };
@@ -265,7 +429,7 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
 #pragma unroll
             for (int c = 0; c < NC; ++c) qb[t][c] = bf16x8{};
             if (r < rows) {
-                const int seq = it.seq0 + r / G, h = kvh * G + r % G;
+                const int seq = seq0 + r / G, h = kvh * G + r % G;
                 const uint16_t *qp = a.q + ((size_t)seq * a.n_q_heads + h) * HD + 8 * q4;
 #pragma unroll
                 for (int c = 0; c < NC; ++c) qb[t][c] = *reinterpret_cast<const bf16x8 *>(qp + 32 * c);
@@ -343,7 +507,7 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
 #pragma unroll
                 for (int h = 0; h < 2; ++h) vr[e][h] = ds_read_tr16<st * SLICE_CHUNKS * 16>(traddr[e][h]);
 
-            const int valid = tok_end - slice_tok0(k);  // keys of this slice that exist (may exceed 32)
+            const int valid = tok_lim - slice_tok0(k);  // keys of this slice in range (may exceed 32)
             const bool full = valid >= kSlice;
             bf16x8 ph[NT], pl[NT];
 #pragma unroll
@@ -360,10 +524,11 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
                 // lane: row 16t + l16, slice tokens 4*q4 + j (s0) and 16 + 4*q4 + j (s1); raw q.k
                 float x[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
                 if (__builtin_expect(!full, 0)) {
+                    const int v4 = valid - 4 * q4;  // keys left from this lane's first token
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        x[j] = (4 * q4 + j < valid) ? x[j] : -INFINITY;
-                        x[4 + j] = (16 + 4 * q4 + j < valid) ? x[4 + j] : -INFINITY;
+                        x[j] = (j < v4) ? x[j] : -INFINITY;
+                        x[4 + j] = (16 + j < v4) ? x[4 + j] : -INFINITY;
                     }
                 }
                 float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
@@ -411,112 +576,141 @@ __global__ __launch_bounds__(kThreads) void partials_kernel(AttnArgs a)
             }
         };
 
-        // Pipeline: K and V kDepth slices ahead, slice k in V ring stage and K register set
-        // k % kStages.  Loads are issued for every step (slices past this wave's last one have
-        // empty buffer resources and move no data), so the issue order is fixed:
-        // V0 K0 V1 K1 ... | V(k+kDepth) K(k+kDepth) before computing slice k.  The loads issued
-        // after K(k) are then V(k+1), K(k+1), ..., V(k+kDepth), K(k+kDepth); V(k) precedes K(k).
-        bf16x8 kbuf[kStages][2][NC];
-        static_for<kDepth>([&](auto J) {
-            constexpr int j = decltype(J)::value;
-            issue_v(j, std::integral_constant<int, j>{});
-            load_k(j, kbuf[j]);
-        });
-        for (int k = 0; k < ns; k += kStages) {
-            static_for<kStages>([&](auto PH) {
-                constexpr int ph = decltype(PH)::value;
-                constexpr int ahead = (ph + kDepth) % kStages;
-                issue_v(k + ph + kDepth, std::integral_constant<int, ahead>{});
-                load_k(k + ph + kDepth, kbuf[ahead]);
-                wait_vm<2 * kDepth * KLOADS>();
-                if (ph == 0 || k + ph < ns) compute(k + ph, kbuf[ph], PH);
-            });
+        // Pipeline, one slice ahead: slice kc sits in V ring stage 0 / K registers 0 while the
+        // next one loads into stage 1, then the roles swap.  Loads are issued at every step
+        // (slices past the group's end have empty buffer resources and move no data), so the
+        // wait count is fixed: V(k), K(k) precede the two loads of the slice behind them.  The
+        // loop is tested at the top (a test in the middle costs the allocator registers).
+        if (item >= 0) {
+            bf16x8 kbuf[kStages][2][NC];
+            int kc = grab();
+            issue_v(kc, std::integral_constant<int, 0>{});
+            load_k(kc, kbuf[0]);
+            while (kc < ghi) {
+                const int kn = grab();
+                issue_v(kn, std::integral_constant<int, 1>{});
+                load_k(kn, kbuf[1]);
+                wait_vm<2 * KLOADS>();
+                compute(kc, kbuf[0], std::integral_constant<int, 0>{});
+                kc = grab();
+                issue_v(kc, std::integral_constant<int, 0>{});
+                load_k(kc, kbuf[0]);
+                wait_vm<2 * KLOADS>();
+                if (kn < ghi)
+                    compute(kn, kbuf[1], std::integral_constant<int, 1>{});
+                else
+                    kc = ghi;
+            }
         }
 
-        // combine the four waves' (max, sum, accumulator) per row and write the partial
+        // ---- combine the (max, sum, accumulator) of the waves that worked on this item.
+        // Lane-derived values are recomputed here from an opaque lane id: values kept from the
+        // kernel start would have been spilled, and their reloads wait for every load in flight.
+        const int lane_c = opaque_lane_id();
+        const int l16c = lane_c & 15, q4c = lane_c >> 4, tid_c = wave * 64 + lane_c;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const float ls = sum_over_rows(l_run[t]);
-            if (q4 == 0) {
-                red_m[wave][t][l16] = m_ref[t];
-                red_l[wave][t][l16] = ls;
+            if (q4c == 0) {
+                red_m[wave][t][l16c] = m_ref[t];
+                red_l[wave][t][l16c] = ls;
             }
         }
-        wait_vm<0>();
-        __syncthreads();  // every wave is done with its ring: it becomes the output staging
-        float *lds_o = reinterpret_cast<float *>(&vring[0][0][0]);  // [kWaves][16][OSTRIDE]
+        wait_vm<0>();  // this wave's ring is idle: it takes the wave's raw accumulators
+        // Staging, per pass two 16-row tiles: wave w's ring holds [tile][row][d] of its own
+        // accumulator (the 16-float blocks of a row XOR-permuted by the row, for the banks).
+        // Threads then own (row, chunk) units of each group: they weigh the group's waves by
+        // exp(max_w - max) and sum.  All global stores of a pass follow its LDS work.
+        static_assert(2 * 16 * HD * 4 <= kStages * SLICE_CHUNKS * 16, "two tiles fit in a wave's ring");
+        constexpr int CH4 = HD / 4;
+        auto stg = [&](int w) { return reinterpret_cast<float *>(&vring[w][0][0]); };
+        auto stg_off = [&](int tt, int r, int c4) {  // float offset of chunk c4 (4 floats)
+            return (tt * 16 + r) * HD + 16 * ((c4 >> 2) ^ (r & (NE - 1))) + 4 * (c4 & 3);
+        };
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            if (t >= nt_act) break;
-            float M = -INFINITY;
+        for (int pass = 0; pass < (NT + 1) / 2; ++pass) {
+            if (pass > 0) lds_barrier();  // the previous pass has read the staging
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red_m[w][t][l16]);
-            const float Mu = (M == -INFINITY) ? 0.f : M;
-            float L = 0.f;
+            for (int tt = 0; tt < 2; ++tt) {
+                const int t = 2 * pass + tt;
+                if (t >= NT) break;
+                if (item >= 0 && t < nt_act) {
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) L += red_l[w][t][l16] * fast_exp2(red_m[w][t][l16] - Mu);
-            // L == 0 only when the item saw no keys; a NaN input keeps propagating
-            const float mine = (m_ref[t] == -INFINITY) ? 0.f : fast_exp2(m_ref[t] - Mu);
-            const float f = (L == 0.f) ? 0.f : mine / L;
-#pragma unroll
-            for (int e = 0; e < NE; ++e)
-                *reinterpret_cast<f32x4 *>(&lds_o[(wave * 16 + l16) * OSTRIDE + 16 * e + 4 * q4]) = acc[t][e] * f;
-            __syncthreads();
-            {
-                constexpr int PER = HD / 16;  // floats per thread: 16 threads cover one row
-                const int r = tid >> 4, d0 = (tid & 15) * PER;
-                const int row = 16 * t + r;
-                if (row < rows) {
-                    const int seq = it.seq0 + row / G, h = kvh * G + row % G;
-                    float o[PER];
-#pragma unroll
-                    for (int k2 = 0; k2 < PER; ++k2) o[k2] = 0.f;
-#pragma unroll
-                    for (int w = 0; w < kWaves; ++w)
-#pragma unroll
-                        for (int k2 = 0; k2 < PER; ++k2) o[k2] += lds_o[(w * 16 + r) * OSTRIDE + d0 + k2];
-                    float *dst = a.part_o + (((size_t)it.part * a.n_seqs + seq) * a.n_q_heads + h) * HD + d0;
-#pragma unroll
-                    for (int k2 = 0; k2 < PER; k2 += 4)
-                        *reinterpret_cast<f32x4 *>(dst + k2) = f32x4{o[k2], o[k2 + 1], o[k2 + 2], o[k2 + 3]};
-                    if ((tid & 15) == 0) {
-                        float Mr = -INFINITY;
-#pragma unroll
-                        for (int w = 0; w < kWaves; ++w) Mr = fmaxf(Mr, red_m[w][t][r]);
-                        const float Mru = (Mr == -INFINITY) ? 0.f : Mr;
-                        float Lr = 0.f;
-#pragma unroll
-                        for (int w = 0; w < kWaves; ++w) Lr += red_l[w][t][r] * fast_exp2(red_m[w][t][r] - Mru);
-                        a.part_lse[((size_t)it.part * a.n_seqs + seq) * a.n_q_heads + h] =
-                            (Lr == 0.f) ? -INFINITY : (Mru + log2f(Lr)) * kLn2;
-                    }
+                    for (int e = 0; e < NE; ++e)
+                        *reinterpret_cast<f32x4 *>(&stg(wave)[stg_off(tt, l16c, 4 * e + q4c)]) = acc[t][e];
                 }
             }
-            __syncthreads();
+            lds_barrier();  // also orders the group table (written by thread 0 before streaming)
+            const int n_grp = min(s_ngrp, NW);
+            for (int g = 0; g < n_grp; ++g) {
+                const int lw = s_grp[g][0], ge = s_grp[g][1], it = s_grp[g][3];
+                if (vb + it >= a.n_slots || it < 0) continue;  // never store outside the workspace
+                const int r0 = 32 * pass, r1 = min(s_grp[g][2], r0 + 32);
+                for (int u = tid_c; u < (r1 - r0) * CH4; u += NTH) {
+                    const int row = r0 + u / CH4, c = u % CH4;
+                    const int t = row >> 4, tt = t - 2 * pass, r = row & 15;
+                    float mw[NW], lw_[NW];
+                    f32x4 v[NW];
+#pragma unroll
+                    for (int w = 0; w < NW; ++w) {
+                        mw[w] = red_m[w][t][r];
+                        lw_[w] = red_l[w][t][r];
+                        v[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, c)]);
+                    }
+                    float M = -INFINITY;
+#pragma unroll
+                    for (int w = 0; w < NW; ++w) M = (w >= lw && w < ge) ? fmaxf(M, mw[w]) : M;
+                    const float Mu = (M == -INFINITY) ? 0.f : M;
+                    float L = 0.f;
+                    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int w = 0; w < NW; ++w) {
+                        // waves outside the group are selected out, not weighted by 0: their
+                        // staging may hold another item's NaN.  A wave of the group that saw no
+                        // keys has max -inf and weight 0 (its accumulator is 0).
+                        const bool in = w >= lw && w < ge;
+                        const float wt = (in && mw[w] != -INFINITY) ? fast_exp2(mw[w] - Mu) : 0.f;
+                        L = in ? L + wt * lw_[w] : L;
+                        o = in ? o + wt * v[w] : o;
+                    }
+                    // L == 0 only when the group saw no keys; a NaN input keeps propagating
+                    const f32x4 res = (L == 0.f) ? f32x4{0.f, 0.f, 0.f, 0.f} : o / L;
+                    const size_t so = (size_t)(vb + it) * a.slot_rows + row;
+                    *reinterpret_cast<f32x4 *>(a.part_o + so * HD + 4 * c) = res;
+                    if (c == 0) a.part_lse[so] = (L == 0.f) ? -INFINITY : (Mu + log2f(L)) * kLn2;
+                }
+            }
         }
-        wait_vm<0>();
         if (bad_page) atomicOr(a.err, kErrBadPage);
     }
+}
 
-    // the last block out re-arms the queue for the next launch
-    if (tid == 0) {
-        __threadfence();
-        if (atomicAdd(a.done, 1) == (int)gridDim.x - 1) {
-            *a.queue = 0;
-            *a.done = 0;
-        }
+template <int HD, bool PAGED>
+int blocks_per_cu_hd(int row_tiles)
+{
+    const void *f = nullptr;
+    int threads = 0;
+    switch (row_tiles) {
+    case 1: f = reinterpret_cast<const void *>(&partials_kernel<HD, 1, PAGED>); threads = 256 * waves_per_simd<HD, 1>(); break;
+    case 2: f = reinterpret_cast<const void *>(&partials_kernel<HD, 2, PAGED>); threads = 256 * waves_per_simd<HD, 2>(); break;
+    case 3: f = reinterpret_cast<const void *>(&partials_kernel<HD, 3, PAGED>); threads = 256 * waves_per_simd<HD, 3>(); break;
+    case 4: f = reinterpret_cast<const void *>(&partials_kernel<HD, 4, PAGED>); threads = 256 * waves_per_simd<HD, 4>(); break;
+    default: return 0;
     }
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, threads, 0) != hipSuccess) return 0;
+    return n;
 }
 
 template <int HD, bool PAGED>
 hipError_t launch_hd(const AttnArgs &a, int n_blocks, int row_tiles, hipStream_t s)
 {
-    const dim3 grid(n_blocks), block(kThreads);
+    const dim3 grid(n_blocks);
     switch (row_tiles) {
-    case 1: partials_kernel<HD, 1, PAGED><<<grid, block, 0, s>>>(a); break;
-    case 2: partials_kernel<HD, 2, PAGED><<<grid, block, 0, s>>>(a); break;
-    case 3: partials_kernel<HD, 3, PAGED><<<grid, block, 0, s>>>(a); break;
-    case 4: partials_kernel<HD, 4, PAGED><<<grid, block, 0, s>>>(a); break;
+    case 1: partials_kernel<HD, 1, PAGED><<<grid, 256 * waves_per_simd<HD, 1>(), 0, s>>>(a); break;
+    case 2: partials_kernel<HD, 2, PAGED><<<grid, 256 * waves_per_simd<HD, 2>(), 0, s>>>(a); break;
+    case 3: partials_kernel<HD, 3, PAGED><<<grid, 256 * waves_per_simd<HD, 3>(), 0, s>>>(a); break;
+    case 4: partials_kernel<HD, 4, PAGED><<<grid, 256 * waves_per_simd<HD, 4>(), 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -524,9 +718,28 @@ hipError_t launch_hd(const AttnArgs &a, int n_blocks, int row_tiles, hipStream_t
 
 }  // namespace
 
+int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged)
+{
+    if (head_dim == 128) return paged ? blocks_per_cu_hd<128, true>(row_tiles) : blocks_per_cu_hd<128, false>(row_tiles);
+    if (head_dim == 64) return paged ? blocks_per_cu_hd<64, true>(row_tiles) : blocks_per_cu_hd<64, false>(row_tiles);
+    return 0;
+}
+
+int partials_waves_per_block(int head_dim, int row_tiles)
+{
+    if (head_dim == 64) return 4 * waves_per_simd<64, 1>();
+    switch (row_tiles) {
+    case 1: return 4 * waves_per_simd<128, 1>();
+    case 2: return 4 * waves_per_simd<128, 2>();
+    case 3: return 4 * waves_per_simd<128, 3>();
+    case 4: return 4 * waves_per_simd<128, 4>();
+    default: return 0;
+    }
+}
+
 hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s)
 {
-    if (a.n_items <= 0 || n_blocks <= 0) return hipSuccess;
+    if (n_blocks <= 0) return hipSuccess;
     if (head_dim == 128) return a.paged ? launch_hd<128, true>(a, n_blocks, row_tiles, s)
                                         : launch_hd<128, false>(a, n_blocks, row_tiles, s);
     if (head_dim == 64) return a.paged ? launch_hd<64, true>(a, n_blocks, row_tiles, s)

@@ -31,18 +31,25 @@ class Heads(C.Structure):
 
 class ContigDesc(C.Structure):
     _fields_ = [("n_branches", C.c_int32), ("prefix_len", C.c_int32), ("suffix_cap", C.c_int32),
-                ("max_suffix_len", C.c_int32), ("share_prefix", C.c_int32), ("split_tokens", C.c_int32)]
+                ("max_suffix_len", C.c_int32), ("share_prefix", C.c_int32), ("rounds", C.c_int32)]
 
 
 class PagedDesc(C.Structure):
     _fields_ = [("n_seqs", C.c_int32), ("n_groups", C.c_int32), ("page_size", C.c_int32),
                 ("max_pages_per_seq", C.c_int32), ("n_pool_pages", C.c_int32), ("max_suffix_len", C.c_int32),
-                ("share_prefix", C.c_int32), ("split_tokens", C.c_int32)]
+                ("share_prefix", C.c_int32), ("rounds", C.c_int32)]
 
 
 class PlanInfo(C.Structure):
-    _fields_ = [("split_tokens", C.c_int32), ("suffix_split_tokens", C.c_int32), ("max_prefix_parts", C.c_int32),
-                ("n_suffix_parts", C.c_int32), ("n_items", C.c_int32), ("workspace_bytes", C.c_size_t)]
+    _fields_ = [("n_items", C.c_int32), ("n_prefix_items", C.c_int32), ("waves_per_block", C.c_int32),
+                ("n_blocks", C.c_int32), ("rounds", C.c_int32), ("n_slots", C.c_int32), ("slot_rows", C.c_int32),
+                ("workspace_bytes", C.c_size_t)]
+
+
+class Slot(C.Structure):
+    _fields_ = [("slot", C.c_int32), ("kind", C.c_int32), ("seq0", C.c_int32), ("nseq", C.c_int32),
+                ("kv_head", C.c_int32), ("rows", C.c_int32), ("tok_begin", C.c_int32), ("tok_end", C.c_int32),
+                ("n_tok", C.c_int32)]
 
 
 _vp = C.c_void_p
@@ -59,6 +66,7 @@ _sig = {
     "fka_append_kv_paged": ([_vp] * 8, C.c_int),
     "fka_gather_paged": ([_vp, C.c_int32, _vp, _vp, _vp, C.c_int32, _vp, _vp, _vp], C.c_int),
     "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
+    "fka_plan_slots": ([_vp, _vp, _vp, C.c_int32, C.POINTER(C.c_int32)], C.c_int),
     "fka_partials": ([_vp] * 10, C.c_int),
     "fka_lse_merge": ([C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp], C.c_int),
     "fka_plan_device_error": ([_vp, C.POINTER(C.c_int32)], C.c_int),
@@ -106,7 +114,7 @@ def _stream(stream) -> _vp:
 
 
 class Plan:
-    """A fork plan: the work split and the device workspace (see fka_plan_create_*)."""
+    """A fork plan: the static work schedule and the device workspace (see fka_plan_create_*)."""
 
     def __init__(self, handle: int, paged: bool, heads: Heads, n_seqs: int):
         self._h = _vp(handle)
@@ -116,23 +124,23 @@ class Plan:
 
     @classmethod
     def contig(cls, n_q_heads, n_kv_heads, head_dim, n_branches, prefix_len, suffix_cap, max_suffix_len,
-               share_prefix=True, split_tokens=0, softmax_scale=0.0) -> "Plan":
+               share_prefix=True, rounds=0, softmax_scale=0.0) -> "Plan":
         h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
-        d = ContigDesc(n_branches, prefix_len, suffix_cap, max_suffix_len, int(bool(share_prefix)), split_tokens)
+        d = ContigDesc(n_branches, prefix_len, suffix_cap, max_suffix_len, int(bool(share_prefix)), rounds)
         out = _vp()
         _check(_lib.fka_plan_create_contig(C.byref(h), C.byref(d), C.byref(out)))
         return cls(out.value, False, h, n_branches)
 
     @classmethod
     def paged_plan(cls, n_q_heads, n_kv_heads, head_dim, group_start, group_prefix_len, max_pages_per_seq,
-                   n_pool_pages, max_suffix_len, share_prefix=True, split_tokens=0, softmax_scale=0.0,
+                   n_pool_pages, max_suffix_len, share_prefix=True, rounds=0, softmax_scale=0.0,
                    page_size=16) -> "Plan":
         import numpy as np
         gs = np.ascontiguousarray(group_start, np.int32)
         gl = np.ascontiguousarray(group_prefix_len, np.int32)
         h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
         d = PagedDesc(int(gs[-1]), len(gl), page_size, max_pages_per_seq, n_pool_pages, max_suffix_len,
-                      int(bool(share_prefix)), split_tokens)
+                      int(bool(share_prefix)), rounds)
         out = _vp()
         _check(_lib.fka_plan_create_paged(C.byref(h), C.byref(d), gs.ctypes.data_as(_vp), gl.ctypes.data_as(_vp),
                                           C.byref(out)))
@@ -157,6 +165,18 @@ class Plan:
         i = PlanInfo()
         _check(_lib.fka_plan_get_info(self._h, C.byref(i)))
         return i
+
+    def slots(self, suffix_len) -> list:
+        """The partial slots a decode writes for these (host) suffix lengths (fka_plan_slots)."""
+        import numpy as np
+        sl = np.ascontiguousarray(suffix_len, np.int32)
+        if sl.shape != (self.n_seqs,):
+            raise ValueError(f"suffix_len must have shape ({self.n_seqs},)")
+        n = C.c_int32(0)
+        _check(_lib.fka_plan_slots(self._h, sl.ctypes.data_as(_vp), None, 0, C.byref(n)))
+        arr = (Slot * max(1, n.value))()
+        _check(_lib.fka_plan_slots(self._h, sl.ctypes.data_as(_vp), C.cast(arr, _vp), n.value, C.byref(n)))
+        return [{f: getattr(arr[i], f) for f, _ in Slot._fields_} for i in range(n.value)]
 
     def device_error(self) -> int:
         v = C.c_int32(0)

@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol(fa):
 
 
 def test_version_and_empty_error(fa):
-    assert fa.version() == 10000
+    assert fa.version() == 20000
     assert isinstance(fa.last_error(), str)
 
 
@@ -61,7 +61,9 @@ def _create(fa, heads, desc):
     ((8, 2, 64), (5, 512, 64, 65, 1, 0), -1, "max_suffix_len"),
     ((8, 2, 64), (5, 512, 0, 0, 1, 0), -1, "suffix_cap"),
     ((8, 2, 64), (5, 512, 64, 64, 2, 0), -1, "share_prefix"),
-    ((8, 2, 64), (5, 512, 64, 64, 1, 100), -1, "split_tokens"),
+    ((8, 2, 64), (5, 512, 64, 64, 1, 100), -1, "rounds"),
+    ((8, 2, 64), (5, 512, 64, 64, 1, -1), -1, "rounds"),
+    ((8, 8, 64), (513, 512, 64, 64, 0, 0), -2, "sequences"),
     ((128, 2, 64), (2, 512, 64, 64, 1, 0), -2, "rows"),
     ((64, 8, 128), (9, 512, 64, 64, 1, 0), -2, "rows"),
 ])
@@ -105,6 +107,7 @@ def test_calls_with_null_plan_are_rejected(fa):
     assert fa.raw_call("fka_append_kv", n, n, n, n, n, n, n) == -1
     assert fa.raw_call("fka_gather_paged", n, 0, n, n, n, 0, n, n, n) == -1
     assert fa.raw_call("fka_plan_get_info", n, n) == -1
+    assert fa.raw_call("fka_plan_slots", n, n, n, 0, n) == -1
     fa.raw_call("fka_plan_destroy", n)   # NULL is ignored
 
 

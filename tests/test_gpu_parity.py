@@ -113,10 +113,11 @@ def test_edge_cases(fa, case):
     _check_contig(fa, W.make(spec))
 
 
-@pytest.mark.parametrize("split", [128, 384, 4096])
-def test_explicit_split_sizes(fa, split):
+@pytest.mark.parametrize("rounds", [1, 3, 64])
+def test_explicit_rounds(fa, rounds):
+    """More rounds: the keys spread over more, smaller partials (64 rounds: ~1 slice per wave)."""
     spec = W.CONFIGS["mid"].replace(prefix_len=3000, seed=78)
-    _check_contig(fa, W.make(spec), split_tokens=split)
+    _check_contig(fa, W.make(spec), rounds=rounds)
 
 
 def test_head_dim_64_full_rows(fa):
@@ -140,7 +141,19 @@ def test_identical_queries_empty_suffixes_identical_outputs(fa):
         assert np.array_equal(out[b], out[0]) and np.array_equal(lse[b], lse[0])
 
 
+def _max_diff(x, y):
+    return float(np.abs(x.astype(np.float64) - y.astype(np.float64)).max())
+
+
+# The waves of a block take an item's slices from a shared counter, so which wave scores
+# which slice (and so the fp32 summation order) can change from launch to launch: repeated
+# results agree to rounding, ~1e-6 of the output scale, not bit for bit.
+REPEAT_TOL = 1e-5
+
+
 def test_branch_isolation(fa):
+    """Changing branch 2's query and suffix values leaves every other branch's output unchanged
+    (to rounding; new random values would move branch 2's output by O(0.1))."""
     w = W.make("mid")
     plan = contig_plan(fa, w)
     out, _ = run_contig(plan, to_dev_contig(w), 32)
@@ -149,49 +162,81 @@ def test_branch_isolation(fa):
     w.suffix_v[2, :, :w.suffix_len[2]] = W.bf16_bits(
         rng.standard_normal(w.suffix_v[2, :, :w.suffix_len[2]].shape).astype(np.float32))
     out2, _ = run_contig(plan, to_dev_contig(w), 32)
+    scale = max(1.0, float(np.abs(out).max()))
     for b in range(w.n_branches):
+        d = _max_diff(out2[b], out[b])
         if b != 2:
-            assert np.array_equal(out2[b], out[b])
+            assert d <= REPEAT_TOL * scale, (b, d)
+        else:
+            assert d > 1e-2 * scale, d
 
 
-def test_deterministic(fa):
+def test_repeatable(fa):
     w = W.make("mid")
     plan = contig_plan(fa, w)
     dv = to_dev_contig(w)
     a, al = run_contig(plan, dv, 32)
-    b, bl = run_contig(plan, dv, 32)
-    assert np.array_equal(a, b) and np.array_equal(al, bl)
+    for _ in range(3):
+        b, bl = run_contig(plan, dv, 32)
+        assert _max_diff(a, b) <= REPEAT_TOL * max(1.0, float(np.abs(a).max()))
+        assert _max_diff(al, bl) <= REPEAT_TOL
 
 
-def test_partials_stage(fa):
-    """Each first-stage partial equals the oracle's attention over that part's key range."""
-    w = W.make("mid", prefix_len=5000, seed=81)
-    plan = contig_plan(fa, w, split_tokens=1024)
+def _check_slots(fa, w, plan, note):
+    """Every slot a decode writes equals the oracle's attention of its rows over its key range."""
     info = plan.info()
     dv = to_dev_contig(w)
     N, Hq, d = w.q.shape
-    slots = info.max_prefix_parts + info.n_suffix_parts
-    po = torch.full((slots, N, Hq, d), float("nan"), device="cuda")
-    pl = torch.full((slots, N, Hq), float("nan"), device="cuda")
+    G = Hq // w.spec.n_kv_heads
+    po = torch.full((info.n_slots, info.slot_rows, d), float("nan"), device="cuda")
+    pl = torch.full((info.n_slots, info.slot_rows), float("nan"), device="cuda")
     plan.partials(dv["q"], dv["prefix_k"], dv["prefix_v"], dv["suffix_k"], dv["suffix_v"], dv["suffix_len"], po, pl)
     torch.cuda.synchronize()
     po, pl = po.cpu().numpy(), pl.cpu().numpy()
-    sp, ss = info.split_tokens, info.suffix_split_tokens
-    assert info.max_prefix_parts == -(-5000 // sp)
-    for p in range(info.max_prefix_parts):
+    slots = plan.slots(w.suffix_len)
+    assert len(slots) > 0
+    seen = set()
+    cover = {}
+    for sl in slots:
+        assert sl["slot"] not in seen and 0 <= sl["slot"] < info.n_slots
+        seen.add(sl["slot"])
+        key = (sl["kind"], sl["seq0"], sl["kv_head"])
+        cover.setdefault(key, []).append((sl["tok_begin"], sl["tok_end"], sl["n_tok"]))
+        if sl["kind"] == 0:
+            pr, sr = (sl["tok_begin"], sl["tok_end"]), (0, 0)
+        else:
+            pr, sr = (0, 0), (sl["tok_begin"], sl["tok_end"])
         ref, ref_lse = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, w.suffix_len,
-                                            w.spec.softmax_scale, prefix_range=(p * sp, (p + 1) * sp),
-                                            suffix_range=(0, 0))
-        gates.assert_gates(po[p], ref, what=f"prefix part {p}")
-        gates.assert_lse(pl[p], ref_lse, what=f"prefix part {p}")
-    for s in range(info.n_suffix_parts):
-        ref, ref_lse = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, w.suffix_len,
-                                            w.spec.softmax_scale, prefix_range=(0, 0),
-                                            suffix_range=(s * ss, (s + 1) * ss))
-        for b in range(N):
-            if s * ss < w.suffix_len[b]:
-                gates.assert_gates(po[info.max_prefix_parts + s, b], ref[b], what=f"suffix part {s} branch {b}")
-                gates.assert_lse(pl[info.max_prefix_parts + s, b], ref_lse[b], what=f"suffix part {s}")
+                                            w.spec.softmax_scale, prefix_range=pr, suffix_range=sr)
+        g = sl["kv_head"]
+        for r in range(sl["rows"]):
+            b = sl["seq0"] + r // G
+            h = g * G + r % G
+            what = f"{note} slot {sl['slot']} kind {sl['kind']} row {r} keys {sl['tok_begin']}:{sl['tok_end']}"
+            if sl["tok_end"] > sl["tok_begin"]:
+                gates.assert_gates(po[sl["slot"], r][None], ref[b, h][None], what=what)
+                gates.assert_lse(pl[sl["slot"], r][None], ref_lse[b, h][None], what=what)
+            else:
+                assert np.all(po[sl["slot"], r] == 0) and np.isneginf(pl[sl["slot"], r]), what
+    # the slots of each item tile its keys exactly
+    for key, ranges in cover.items():
+        ranges.sort()
+        n_tok = ranges[0][2]
+        assert ranges[0][0] == 0 and ranges[-1][1] == n_tok, key
+        for (a0, a1, _), (b0, b1, _) in zip(ranges, ranges[1:]):
+            assert a1 == b0, key
+
+
+@pytest.mark.parametrize("rounds", [0, 5])
+def test_partials_stage(fa, rounds):
+    """Each first-stage partial equals the oracle's attention over that slot's key range."""
+    w = W.make("mid", prefix_len=5000, seed=81)
+    _check_slots(fa, w, contig_plan(fa, w, rounds=rounds), f"rounds={rounds}")
+
+
+def test_partials_stage_naive_plan(fa):
+    w = W.make("tiny-unscaled", prefix_len=700, suffix_range=(0, 90), seed=82)
+    _check_slots(fa, w, contig_plan(fa, w, share_prefix=False), "naive")
 
 
 @pytest.mark.parametrize("d", [64, 128])
@@ -342,9 +387,23 @@ def test_suffix_length_above_bound_is_clamped_and_flagged(fa):
     assert plan.device_error() & 1
 
 
+def _close_to_unfused(oa, la, ob, lb, what):
+    """The fused step and append + decode compute the same sums with different splits of the keys
+    (appending one token moves the balanced schedule), so they agree up to rounding: P carries
+    ~2^-17 relative error per element (hi + lo bf16 terms), which bounds the output difference
+    well below 1e-4 of the output scale; lse agrees to fp32 rounding of the sums."""
+    scale = max(1.0, float(ob.abs().max()))
+    d = float((oa - ob).abs().max())
+    dl = float((la - lb).abs().max())
+    print(f"[fused] {what}: max|fused - unfused| = {d:.3g} (scale {scale:.3g}), lse {dl:.3g}", flush=True)
+    assert d <= 1e-4 * scale, f"{what}: {d}"
+    assert dl <= 1e-5, f"{what}: lse {dl}"
+
+
 def test_fused_step_equals_append_then_decode(fa):
     """fka_fork_step (append fused into the decode) matches append + decode: identical caches and
-    lengths, outputs equal up to fp32 summation order (the new token is merged as its own part)."""
+    lengths; the output matches the oracle on the appended state and the unfused output up to
+    rounding (the new token is merged as its own part)."""
     w = W.make("mid", steps=8)
     plan = contig_plan(fa, w)
     a, b = to_dev_contig(w), to_dev_contig(w)
@@ -358,8 +417,14 @@ def test_fused_step_equals_append_then_decode(fa):
         plan.append(kn[t], vn[t], b["suffix_k"], b["suffix_v"], b["suffix_len"])
         plan.decode(qn[t], b["prefix_k"], b["prefix_v"], b["suffix_k"], b["suffix_v"], b["suffix_len"], ob, lb)
         torch.cuda.synchronize()
-        torch.testing.assert_close(oa, ob, rtol=1e-5, atol=1e-6, msg=f"step {t}")
-        torch.testing.assert_close(la, lb, rtol=1e-6, atol=1e-5, msg=f"step {t}")
+        _close_to_unfused(oa, la, ob, lb, f"contiguous step {t}")
+        if t in (0, 7):
+            sk = b["suffix_k"].view(torch.int16).cpu().numpy().view(np.uint16)
+            sv = b["suffix_v"].view(torch.int16).cpu().numpy().view(np.uint16)
+            ln = b["suffix_len"].cpu().numpy()
+            ref, ref_lse = oracle.decode_contig(w.step_q[t], w.prefix_k, w.prefix_v, sk, sv, ln, w.spec.softmax_scale)
+            gates.assert_gates(oa.cpu().numpy(), ref, what=f"fused step {t}")
+            gates.assert_lse(la.cpu().numpy(), ref_lse, what=f"fused step {t}")
     assert torch.equal(a["suffix_len"], b["suffix_len"])
     assert torch.equal(a["suffix_k"].view(torch.int16), b["suffix_k"].view(torch.int16))
     assert torch.equal(a["suffix_v"].view(torch.int16), b["suffix_v"].view(torch.int16))
@@ -372,16 +437,25 @@ def test_fused_step_paged_equals_append_then_decode(fa):
     a, b = to_dev_paged(w), to_dev_paged(w)
     S, Hq, d = w.q.shape
     rng = np.random.default_rng(5)
-    oa, ob = torch.empty((S, Hq, d), device="cuda"), torch.empty((S, Hq, d), device="cuda")
+    oa, la = torch.empty((S, Hq, d), device="cuda"), torch.empty((S, Hq), device="cuda")
+    ob, lb = torch.empty_like(oa), torch.empty_like(la)
     for t in range(20):
-        kn = dev_bf16(W.bf16_bits(rng.standard_normal((S, w.spec.n_kv_heads, d)).astype(np.float32)))
-        vn = dev_bf16(W.bf16_bits(rng.standard_normal((S, w.spec.n_kv_heads, d)).astype(np.float32)))
-        q = dev_bf16(W.bf16_bits(rng.standard_normal((S, Hq, d)).astype(np.float32)))
-        plan.step_paged(q, kn, vn, a["k_pool"], a["v_pool"], a["page_table"], a["suffix_len"], oa)
+        kn_h = W.bf16_bits(rng.standard_normal((S, w.spec.n_kv_heads, d)).astype(np.float32))
+        vn_h = W.bf16_bits(rng.standard_normal((S, w.spec.n_kv_heads, d)).astype(np.float32))
+        q_h = W.bf16_bits(rng.standard_normal((S, Hq, d)).astype(np.float32))
+        kn, vn, q = dev_bf16(kn_h), dev_bf16(vn_h), dev_bf16(q_h)
+        plan.step_paged(q, kn, vn, a["k_pool"], a["v_pool"], a["page_table"], a["suffix_len"], oa, la)
         plan.append_paged(kn, vn, b["k_pool"], b["v_pool"], b["page_table"], b["suffix_len"])
-        plan.decode_paged(q, b["k_pool"], b["v_pool"], b["page_table"], b["suffix_len"], ob)
+        plan.decode_paged(q, b["k_pool"], b["v_pool"], b["page_table"], b["suffix_len"], ob, lb)
         torch.cuda.synchronize()
-        torch.testing.assert_close(oa, ob, rtol=1e-5, atol=1e-6, msg=f"step {t}")
+        _close_to_unfused(oa, la, ob, lb, f"paged step {t}")
+        if t in (0, 19):
+            kp = b["k_pool"].view(torch.int16).cpu().numpy().view(np.uint16)
+            vp = b["v_pool"].view(torch.int16).cpu().numpy().view(np.uint16)
+            ln = b["suffix_len"].cpu().numpy()
+            ref, ref_lse = oracle.decode_paged(q_h, kp, vp, w.page_table, w.seq_prefix_len, ln, w.spec.softmax_scale)
+            gates.assert_gates(oa.cpu().numpy(), ref, what=f"fused paged step {t}")
+            gates.assert_lse(la.cpu().numpy(), ref_lse, what=f"fused paged step {t}")
     assert torch.equal(a["suffix_len"], b["suffix_len"])
     assert torch.equal(a["k_pool"].view(torch.int16), b["k_pool"].view(torch.int16))
     assert plan.device_error() == 0
