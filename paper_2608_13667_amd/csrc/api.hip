@@ -29,6 +29,7 @@ struct fka_plan {
     std::vector<int32_t> seq_pre_item;     // prefix item of (s, head 0), -1 if none
     std::vector<int32_t> seq_pre_row;      // first row of s within its prefix item
     std::vector<int32_t> seq_prefix_len;   // prefix length of s's unit
+    std::vector<int32_t> row_info;         // [S * Hq][kRowInfo] merge table
     int32_t pre_slices = 0, pre_nonempty = 0;
     int32_t n_items = 0;       // prefix items + n_seqs * Hkv suffix items
     int32_t slot_rows = 0;     // rows of the largest item
@@ -42,8 +43,7 @@ struct fka_plan {
     // device memory (one allocation, carved)
     void *mem = nullptr;
     fka::PrefixItem *d_pre = nullptr;
-    int32_t *d_seq_pre_item = nullptr;
-    int32_t *d_seq_pre_row = nullptr;
+    int32_t *d_row_info = nullptr;
     int32_t *d_seq_prefix_len = nullptr;
     int32_t *err = nullptr;
     int32_t *sched = nullptr;
@@ -153,6 +153,24 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     if (c > (int64_t)1 << 30) return fail(FKA_ERR_UNSUPPORTED, "prefix of %lld slices is too long", (long long)c);
     p->pre_slices = (int32_t)c;
     p->pre_nonempty = k;
+    p->row_info.assign((size_t)p->n_seqs * p->Hq * fka::kRowInfo, 0);
+    for (int s = 0; s < p->n_seqs; ++s)
+        for (int h = 0; h < p->Hq; ++h) {
+            int32_t *ri = &p->row_info[((size_t)s * p->Hq + h) * fka::kRowInfo];
+            const int g = h / p->G;
+            const int ip0 = p->seq_pre_item[s];
+            ri[0] = ip0 >= 0 ? ip0 + g : -1;
+            ri[1] = p->seq_pre_row[s] + h % p->G;
+            if (ip0 >= 0) {
+                const fka::PrefixItem &it = p->pre[ip0 + g];
+                ri[2] = it.c0;
+                ri[3] = it.k0;
+                ri[4] = fka::slices_of(it.n_tok);
+            }
+            ri[5] = s;
+            ri[6] = g;
+            ri[7] = h % p->G;
+        }
     p->n_items = (int32_t)p->pre.size() + p->n_seqs * p->Hkv;
     p->slot_rows = max_nseq * p->G;
     p->row_tiles = ceil_div(p->slot_rows, 16);
@@ -182,11 +200,12 @@ fka_status finish_plan(fka_plan *p)
     auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
     const size_t b_pre = up(std::max<size_t>(1, p->pre.size()) * sizeof(fka::PrefixItem));
     const size_t b_seq = up((size_t)p->n_seqs * sizeof(int32_t));
+    const size_t b_rows = up(p->row_info.size() * sizeof(int32_t));
     const size_t b_err = 256;
     const size_t b_sched = up((size_t)fka::sched_words(p->n_seqs) * sizeof(int32_t));
     const size_t b_po = up((size_t)p->n_slots * p->slot_rows * p->d * sizeof(float));
     const size_t b_pl = up((size_t)p->n_slots * p->slot_rows * sizeof(float));
-    const size_t total = b_pre + 3 * b_seq + b_err + b_sched + b_po + b_pl;
+    const size_t total = b_pre + b_rows + b_seq + b_err + b_sched + b_po + b_pl;
     e = hipMalloc(&p->mem, total);
     if (e != hipSuccess) {
         p->mem = nullptr;
@@ -196,10 +215,8 @@ fka_status finish_plan(fka_plan *p)
     char *m = static_cast<char *>(p->mem);
     p->d_pre = reinterpret_cast<fka::PrefixItem *>(m);
     m += b_pre;
-    p->d_seq_pre_item = reinterpret_cast<int32_t *>(m);
-    m += b_seq;
-    p->d_seq_pre_row = reinterpret_cast<int32_t *>(m);
-    m += b_seq;
+    p->d_row_info = reinterpret_cast<int32_t *>(m);
+    m += b_rows;
     p->d_seq_prefix_len = reinterpret_cast<int32_t *>(m);
     m += b_seq;
     p->err = reinterpret_cast<int32_t *>(m);
@@ -217,9 +234,9 @@ fka_status finish_plan(fka_plan *p)
     };
     fka_status st;
     if ((st = put(p->d_pre, p->pre.data(), p->pre.size() * sizeof(fka::PrefixItem), "hipMemcpy(prefix items)")) != FKA_OK ||
-        (st = put(p->d_seq_pre_item, p->seq_pre_item.data(), b_seq, "hipMemcpy(sequence tables)")) != FKA_OK ||
-        (st = put(p->d_seq_pre_row, p->seq_pre_row.data(), b_seq, "hipMemcpy(sequence tables)")) != FKA_OK ||
-        (st = put(p->d_seq_prefix_len, p->seq_prefix_len.data(), b_seq, "hipMemcpy(sequence tables)")) != FKA_OK)
+        (st = put(p->d_row_info, p->row_info.data(), p->row_info.size() * sizeof(int32_t), "hipMemcpy(row table)")) != FKA_OK ||
+        (st = put(p->d_seq_prefix_len, p->seq_prefix_len.data(), p->seq_prefix_len.size() * sizeof(int32_t),
+                  "hipMemcpy(sequence tables)")) != FKA_OK)
         return st;
     if ((e = hipMemset(p->err, 0, b_err + b_sched)) != hipSuccess) return hip_fail(e, "hipMemset(flags)");
     return FKA_OK;
@@ -264,9 +281,7 @@ fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *o
     m.n_q_heads = p->Hq;
     m.n_parts = 0;
     m.sched = p->sched;
-    m.pre_items = p->d_pre;
-    m.seq_pre_item = p->d_seq_pre_item;
-    m.seq_pre_row = p->d_seq_pre_row;
+    m.row_info = p->d_row_info;
     m.n_pre = (int32_t)p->pre.size();
     m.pre_slices = p->pre_slices;
     m.pre_nonempty = p->pre_nonempty;

@@ -51,6 +51,11 @@ struct PrefixItem {  // eight int32 fields, read field by field on the device
 // [4 + 3s] clamped suffix length, [5 + 3s] CS(s), [6 + 3s] NE(s), where CS(s) and NE(s)
 // count the slices and the non-empty items of the suffix items of sequences before s.
 constexpr int kSchedHeader = 4;
+
+// Static per-row table of the merge (row = s * Hq + h, g = h / G), int32 words:
+// [0] prefix item of the row (-1 if none), [1] the row's row within it, [2] its C, [3] its K,
+// [4] its slices, [5] s, [6] g, [7] h % G (the row within the suffix item (s, g)).
+constexpr int kRowInfo = 8;
 __host__ __device__ inline int sched_words(int n_seqs) { return kSchedHeader + 3 * n_seqs; }
 
 __host__ __device__ inline int32_t slices_of(int32_t tokens) { return (tokens + kSlice - 1) / kSlice; }
@@ -68,11 +73,17 @@ __host__ __device__ inline int32_t worker_start(int64_t C, int64_t K, uint64_t R
     return (int32_t)(((uint64_t)C * R) >> 32) + (int32_t)K;
 }
 
-// Slice range [lo, hi) of worker j of an item with `size` slices and w workers.
+// Slice range [lo, hi) of worker j of an item with `size` slices and w workers (exact floor
+// divisions; 32-bit arithmetic whenever w * size fits, which gives the same result cheaper).
 __host__ __device__ inline void worker_range(int32_t j, int32_t w, int32_t size, int32_t &lo, int32_t &hi)
 {
-    lo = (int32_t)((int64_t)j * size / w);
-    hi = (int32_t)((int64_t)(j + 1) * size / w);
+    if ((uint64_t)w * (uint64_t)size < ((uint64_t)1 << 32)) {
+        lo = (int32_t)((uint32_t)j * (uint32_t)size / (uint32_t)w);
+        hi = (int32_t)((uint32_t)(j + 1) * (uint32_t)size / (uint32_t)w);
+    } else {
+        lo = (int32_t)((int64_t)j * size / w);
+        hi = (int32_t)((int64_t)(j + 1) * size / w);
+    }
 }
 
 struct AttnArgs {
@@ -119,9 +130,7 @@ struct MergeArgs {
     int32_t n_parts;
     // plan mode: row (s, h) merges the slots of its prefix item and of its suffix item
     const int32_t *sched;         // snapshot written by the partial kernel
-    const PrefixItem *pre_items;
-    const int32_t *seq_pre_item;  // [S] prefix item of (s, head 0), -1 if none
-    const int32_t *seq_pre_row;   // [S] first row of s within its prefix item
+    const int32_t *row_info;      // [rows][kRowInfo] static per-row table (see kRowInfo)
     int32_t n_pre;
     int32_t pre_slices;
     int32_t pre_nonempty;

@@ -15,48 +15,56 @@ constexpr float kLog2e = 1.442695040888963407f;
 template <int HD>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 {
-    constexpr int CH = HD / 4;          // float4 chunks per row
-    constexpr int SL = 256 / CH;        // part slices
-    constexpr int MAXP = 1024;          // parts weighed per pass
-    __shared__ float s_w[MAXP];
-    __shared__ int s_off[MAXP];
+    constexpr int CH = HD / 4;    // float4 chunks per row
+    constexpr int SL = 256 / CH;  // part slices: slice k takes parts k, k + SL, ...
+    __shared__ float s_m[SL], s_w[SL];
     __shared__ f32x4 s_acc[SL][CH];
-    __shared__ float s_red[4];
     __shared__ float s_new;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int chunk = tid % CH, slice = tid / CH;
     const int row = blockIdx.x;
 
+    // Everything this block reads first is requested together: the row's static table and the
+    // schedule snapshot (plan mode) and, in a fused step, q and the appended key.
     // Parts of this row, as offsets (part index * row stride + row) into part_o / part_lse:
     // parts [0, np) start at p_first with stride p_step; parts [np, n) at s_first.
-    int np = 0, n = 0;
+    int np = 0, n = 0, L = 0, seq = 0, g = 0;
     int64_t p_first = 0, p_step = 0, s_first = 0;
-    int L = 0;
     bool with_new = false;  // fused step: the appended token is one more part, read from k_new / v_new
-    int seq = 0, g = 0;
+    float dot = 0.f;
+    uint4 app_k = {0, 0, 0, 0}, app_v = {0, 0, 0, 0};  // fused step, block (s, 0): the token to store
+    constexpr int APP = HD / 8;                        // 16-byte chunks of one K/V row
     if (a.sched) {
+        // seq and g from the row index, so the snapshot and the row table load together
         seq = row / a.n_q_heads;
-        const int h = row % a.n_q_heads;
-        g = h / a.group;
-        const int hr = h % a.group;
+        g = (row % a.n_q_heads) / a.group;
+        const int32_t *ri = a.row_info + (size_t)row * kRowInfo;
+        const int ip = ri[0], prow = ri[1], pc0 = ri[2], pk0 = ri[3], psize = ri[4];
+        const int hr = ri[7];
+        if (a.step_mode && row % a.n_q_heads == 0 && tid < a.n_kv_heads * APP) {
+            const size_t src = ((size_t)seq * a.n_kv_heads + tid / APP) * HD + 8 * (tid % APP);
+            app_k = *reinterpret_cast<const uint4 *>(a.k_new + src);
+            app_v = *reinterpret_cast<const uint4 *>(a.v_new + src);
+        }
         const int T = a.sched[0], NNE = a.sched[1], NV = a.sched[2];
-        const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
         L = a.sched[kSchedHeader + 3 * seq];
         const int CS = a.sched[kSchedHeader + 3 * seq + 1], NE = a.sched[kSchedHeader + 3 * seq + 2];
+        with_new = a.step_mode && L < a.max_suffix_len;
+        if (with_new && wave == 0) {  // q . k_new, wave 0
+            const uint16_t *qr = a.q + (size_t)row * HD;
+            const uint16_t *kr = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
+            for (int c = lane; c < HD; c += 64)
+                dot += __uint_as_float((uint32_t)qr[c] << 16) * __uint_as_float((uint32_t)kr[c] << 16);
+        }
         const int64_t stride = a.slot_rows;
         if (T > 0) {
-            const int ip0 = a.seq_pre_item[seq];
-            if (ip0 >= 0) {
-                const int ip = ip0 + g;
-                const PrefixItem pi = a.pre_items[ip];
-                const int size = slices_of(pi.n_tok);
-                if (size > 0) {
-                    const int ws0 = worker_start(pi.c0, pi.k0, R), ws1 = worker_start(pi.c0 + size, pi.k0 + 1, R);
-                    const int vb0 = ws0 / a.waves, vb1 = (ws1 - 1) / a.waves;
-                    np = vb1 - vb0 + 1;
-                    p_first = (int64_t)(vb0 + ip) * stride + a.seq_pre_row[seq] + hr;
-                }
+            const uint64_t R = sched_ratio((int64_t)NV - NNE, T);
+            if (ip >= 0 && psize > 0) {
+                const int ws0 = worker_start(pc0, pk0, R), ws1 = worker_start(pc0 + psize, pk0 + 1, R);
+                const int vb0 = ws0 / a.waves, vb1 = (ws1 - 1) / a.waves;
+                np = vb1 - vb0 + 1;
+                p_first = (int64_t)(vb0 + ip) * stride + prow;
             }
             const int ns = slices_of(L);
             n = np;
@@ -70,7 +78,6 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
             }
         }
         p_step = stride;
-        with_new = a.step_mode && L < a.max_suffix_len;
     } else {
         np = n = a.n_parts;
         p_first = row;
@@ -78,78 +85,74 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
     }
     auto part_off = [&](int j) -> int64_t { return j < np ? p_first + j * p_step : s_first + (j - np) * p_step; };
 
-    // the appended token alone: o = v_new, lse = its scaled score (wave 0 forms the dot product)
-    float lse_new = -INFINITY;
-    if (with_new) {
-        if (wave == 0) {
-            const uint16_t *qr = a.q + (size_t)row * HD;
-            const uint16_t *kr = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
-            float dot = 0.f;
-            for (int c = lane; c < HD; c += 64)
-                dot += __uint_as_float((uint32_t)qr[c] << 16) * __uint_as_float((uint32_t)kr[c] << 16);
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) dot += __shfl_xor(dot, off);
-            if (lane == 0) s_new = dot * a.scale;
-        }
-        __syncthreads();
-        lse_new = s_new;
-    }
-
-    // block max of the parts' log-sum-exp values
-    float M = lse_new;
-    for (int i = tid; i < n; i += 256) M = fmaxf(M, a.part_lse[part_off(i)]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-    if (lane == 0) s_red[wave] = M;
-    __syncthreads();
-    M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
-    __syncthreads();
-
+    // Online merge of this slice's parts: running max m, weight sum w and accumulator (each
+    // part's lse and o are loaded together).  An empty part (lse = -inf) has weight 0; a NaN
+    // lse propagates.
+    float m = -INFINITY, w = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    float wsum = 0.f;  // per-thread share of the weight sum (threads of slice 0..SL-1 split parts)
-    if (M != -INFINITY) {
-        for (int base = 0; base < n; base += MAXP) {
-            const int cnt = min(MAXP, n - base);
-            for (int i = tid; i < cnt; i += 256) {
-                const int64_t off = part_off(base + i);
-                const float l = a.part_lse[off];
-                s_w[i] = (l == -INFINITY) ? 0.f : exp2f((l - M) * kLog2e);
-                s_off[i] = (int)off;
+    constexpr int U = 4;  // parts loaded ahead of their use
+    for (int j0 = slice; j0 < n; j0 += U * SL) {
+        float l[U];
+        f32x4 o[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int j = j0 + u * SL;
+            l[u] = -INFINITY;
+            o[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (j < n) {
+                const int64_t off = part_off(j);
+                l[u] = a.part_lse[off];
+                o[u] = *reinterpret_cast<const f32x4 *>(a.part_o + (size_t)off * HD + 4 * chunk);
             }
-            __syncthreads();
-            for (int i = slice; i < cnt; i += SL) {
-                const float w = s_w[i];
-                if (chunk == 0) wsum += w;
-                if (w != 0.f) {
-                    const f32x4 o = *reinterpret_cast<const f32x4 *>(a.part_o + (size_t)s_off[i] * HD + 4 * chunk);
-                    acc += w * o;
-                }
-            }
-            __syncthreads();
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (l[u] == -INFINITY) continue;
+            const float mn = fmaxf(m, l[u]);
+            const float sc = (m == -INFINITY) ? 0.f : exp2f((m - mn) * kLog2e);
+            const float e = exp2f((l[u] - mn) * kLog2e);
+            w = w * sc + e;
+            acc = acc * sc + e * o[u];
+            m = mn;
         }
     }
-    if (with_new && slice == 0 && M != -INFINITY) {
-        const uint16_t *vr = a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk;
-        const float w = exp2f((lse_new - M) * kLog2e);
-        if (chunk == 0) wsum += w;
-        acc += w * f32x4{__uint_as_float((uint32_t)vr[0] << 16), __uint_as_float((uint32_t)vr[1] << 16),
-                         __uint_as_float((uint32_t)vr[2] << 16), __uint_as_float((uint32_t)vr[3] << 16)};
+    if (chunk == 0) {
+        s_m[slice] = m;
+        s_w[slice] = w;
     }
     s_acc[slice][chunk] = acc;
-    // weight sum: chunk-0 threads of every slice hold a share
+    if (with_new && wave == 0) {
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) wsum += __shfl_xor(wsum, off);
-    if (lane == 0) s_red[wave] = wsum;
+        for (int off = 32; off >= 1; off >>= 1) dot += __shfl_xor(dot, off);
+        if (lane == 0) s_new = dot * a.scale;
+    }
     __syncthreads();
-    const float W = s_red[0] + s_red[1] + s_red[2] + s_red[3];
-    if (slice == 0) {
-        f32x4 t = s_acc[0][chunk];
+    const float lse_new = with_new ? s_new : -INFINITY;
+    float M = lse_new;
 #pragma unroll
-        for (int s2 = 1; s2 < SL; ++s2) t += s_acc[s2][chunk];
+    for (int k = 0; k < SL; ++k) M = fmaxf(M, s_m[k]);
+    if (slice == 0) {
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        float W = 0.f;
+        if (M != -INFINITY) {
+#pragma unroll
+            for (int k = 0; k < SL; ++k) {
+                const float sc = (s_m[k] == -INFINITY) ? 0.f : exp2f((s_m[k] - M) * kLog2e);
+                t += sc * s_acc[k][chunk];
+                W += sc * s_w[k];
+            }
+            if (with_new) {
+                const uint16_t *vr = a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk;
+                const float e = exp2f((lse_new - M) * kLog2e);
+                W += e;
+                t += e * f32x4{__uint_as_float((uint32_t)vr[0] << 16), __uint_as_float((uint32_t)vr[1] << 16),
+                               __uint_as_float((uint32_t)vr[2] << 16), __uint_as_float((uint32_t)vr[3] << 16)};
+            }
+        }
         const f32x4 r = (W == 0.f) ? f32x4{0.f, 0.f, 0.f, 0.f} : t / W;
         *reinterpret_cast<f32x4 *>(a.out + (size_t)row * HD + 4 * chunk) = r;
+        if (a.out_lse && chunk == 0) a.out_lse[row] = (W == 0.f) ? -INFINITY : M + logf(W);
     }
-    if (a.out_lse && tid == 0) a.out_lse[row] = (W == 0.f) ? -INFINITY : M + logf(W);
 
     // Fused step: block (s, head 0) stores the token sequence s appended (already attended
     // to from k_new / v_new) and advances suffix_len[s].  No block of this kernel reads the
@@ -163,15 +166,19 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
         ok = page >= 0 && page < a.n_pool_pages;
     }
     if (ok) {
-        constexpr int cpr = HD / 8;
-        for (int c = tid; c < a.n_kv_heads * cpr; c += 256) {
-            const int gg = c / cpr, cc = c % cpr;
-            const size_t src = ((size_t)seq * a.n_kv_heads + gg) * HD + 8 * cc;
+        for (int c = tid; c < a.n_kv_heads * APP; c += 256) {
+            const int gg = c / APP, cc = c % APP;
             const size_t dst =
                 a.paged ? (((size_t)page * a.n_kv_heads + gg) * kPageSize + L % kPageSize) * HD + 8 * cc
                         : (((size_t)seq * a.n_kv_heads + gg) * a.suffix_cap + L) * HD + 8 * cc;
-            *reinterpret_cast<uint4 *>(a.k_dst + dst) = *reinterpret_cast<const uint4 *>(a.k_new + src);
-            *reinterpret_cast<uint4 *>(a.v_dst + dst) = *reinterpret_cast<const uint4 *>(a.v_new + src);
+            uint4 kk = app_k, vv = app_v;  // loaded at the start (the first 256 chunks)
+            if (c >= 256) {
+                const size_t src = ((size_t)seq * a.n_kv_heads + gg) * HD + 8 * cc;
+                kk = *reinterpret_cast<const uint4 *>(a.k_new + src);
+                vv = *reinterpret_cast<const uint4 *>(a.v_new + src);
+            }
+            *reinterpret_cast<uint4 *>(a.k_dst + dst) = kk;
+            *reinterpret_cast<uint4 *>(a.v_dst + dst) = vv;
         }
     }
     if (tid == 0) {

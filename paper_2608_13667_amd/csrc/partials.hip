@@ -149,6 +149,19 @@ __device__ inline int opaque_lane_id()
     return v;
 }
 
+// Sixteen wait states between MFMAs and the first VALU read of their results.  The wait
+// states the compiler counts before such a read on gfx950 can fall short: the first score
+// registers read after the q.k MFMAs were seen to hold the previous slice's values (the row
+// maximum then came out of stale scores, which showed as rounding-level differences between
+// identical rows of different tiles).  Sixteen covers a 4-pass XDL result with margin; the
+// scheduling barriers keep the MFMAs above the wait and the reads below it.
+__device__ inline void xdl_result_wait()
+{
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 7\n\ts_nop 7" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // Block barrier for LDS hand-offs: waits for this wave's LDS operations only, so global
 // stores and prefetches in flight stay in flight (__syncthreads would wait for them too).
 __device__ inline void lds_barrier()
@@ -216,6 +229,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
 #pragma unroll
         for (int f = 0; f < 6; ++f) my_pre[f] = ip[f];
     }
+    if (tid < NW) s_wf[tid][0] = -1;  // waves the placement below does not reach have no item
     // per-sequence suffix tables: clamped length, CS(s), NE(s) (exclusive scans)
     int carry_cs = 0, carry_ne = 0;
     bool clamped = false;
@@ -259,8 +273,8 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
         }
         lds_barrier();
     }
-    const int T = a.pre_slices + carry_cs;       // total slices of this launch
-    const int NNE = a.pre_nonempty + carry_ne;   // non-empty items
+    const int T = __builtin_amdgcn_readfirstlane(a.pre_slices + carry_cs);      // total slices of this launch
+    const int NNE = __builtin_amdgcn_readfirstlane(a.pre_nonempty + carry_ne);  // non-empty items
     const int NV = (int)gridDim.x * NW;  // workers: every block is one virtual block
     const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
     const int n_items = a.n_pre + N * Hkv;
@@ -283,8 +297,6 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     {
         const int vb = (int)blockIdx.x;
         const int w_lo = vb * NW;
-        if (tid < NW) s_wf[tid][0] = -1;
-        lds_barrier();
         // every thread places its items' workers of this block
         if (T > 0) {
             for (int i = tid; i < n_items; i += NTH) {
@@ -354,7 +366,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
         // ---- this wave's item and group (all values uniform)
         bool suffix = false;
         int seq0 = 0, nseq = 0, kvh = 0, tok_end = 0, unit_prefix = 0;
-        int wa = wave, wb = wave + 1, ghi = 0;
+        int wa = wave, ghi = 0;
         if (item >= 0) {
             seq0 = __builtin_amdgcn_readfirstlane(s_wf[wave][1]);
             nseq = __builtin_amdgcn_readfirstlane(s_wf[wave][2]);
@@ -362,7 +374,6 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
             tok_end = __builtin_amdgcn_readfirstlane(s_wf[wave][4]);
             wa = __builtin_amdgcn_readfirstlane(s_wf[wave][5]);
             ghi = __builtin_amdgcn_readfirstlane(s_wf[wave][7]);
-            wb = __builtin_amdgcn_readfirstlane(s_wf[wave][8]);
             suffix = item >= a.n_pre;
             if (PAGED && suffix) unit_prefix = __builtin_amdgcn_readfirstlane(s_spl[seq0]);
         }
@@ -521,6 +532,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                     s0 = mfma16(kr[0][c], qb[t][c], s0);
                     s1 = mfma16(kr[1][c], qb[t][c], s1);
                 }
+                xdl_result_wait();
                 // lane: row 16t + l16, slice tokens 4*q4 + j (s0) and 16 + 4*q4 + j (s1); raw q.k
                 float x[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
                 if (__builtin_expect(!full, 0)) {
@@ -536,7 +548,10 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                 const bool move = mx > m_ref[t] + kRescaleGap;
                 if (__builtin_expect(__builtin_amdgcn_ballot_w64(move) != 0, 0)) {
                     const float m_new = move ? mx : m_ref[t];
-                    const float alpha = fast_exp2(m_ref[t] - m_new);  // 0 when m_ref was -inf
+                    // exactly 1 for a row that keeps its max (the hardware exp2 of 0 need not be),
+                    // so a row's result does not depend on the other rows of its tile; 0 when
+                    // the row's max was -inf
+                    const float alpha = move ? fast_exp2(m_ref[t] - m_new) : 1.f;
                     l_run[t] *= alpha;
 #pragma unroll
                     for (int e = 0; e < NE; ++e) acc[t][e] *= alpha;
