@@ -30,6 +30,13 @@
  *     fka_plan_device_error (reads the device error word).
  *   - A plan owns a workspace for partial results, so it may be used by one
  *     stream at a time.  Plans are independent of each other.
+ *   - A plan also caches the work schedule: each decode or step builds, on the
+ *     device, the schedule of the next launch for the suffix lengths it expects
+ *     that launch to see, keyed by those lengths.  A launch whose lengths match
+ *     the key skips building its schedule; any other lengths are equally valid
+ *     (the schedule is then built in the launch).  Calls on one plan must be
+ *     ordered on one stream (as above), so each launch sees the previous one's
+ *     cache.
  *   - Arguments are validated on the host before anything is launched; on an
  *     error nothing is enqueued, the call returns a negative fka_status and
  *     fka_last_error() describes it.  Values that live on the device (suffix
@@ -271,7 +278,9 @@ fka_status fka_lse_merge(int32_t rows, int32_t n_parts, int32_t head_dim, const 
 /* Read and clear the plan's device error flag (synchronises with the device):
  * *flags receives a bit mask: 1 = a suffix length above max_suffix_len was
  * clamped, 2 = an append found no room (length at max_suffix_len or no page),
- * 4 = a page id outside the page table bounds was met. */
+ * 4 = a page id outside the page table bounds was met, 8 = a schedule record
+ * in the plan's workspace pointed outside it (only if that memory was written
+ * from outside the library; the record was not followed). */
 fka_status fka_plan_device_error(const fka_plan *plan, int32_t *flags);
 
 /* Release a plan and its device memory.  NULL is ignored. */

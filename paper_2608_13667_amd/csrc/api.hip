@@ -26,10 +26,7 @@ struct fka_plan {
     std::vector<int32_t> group_start, group_prefix_len;
     // schedule (see the work schedule in internal.h)
     std::vector<fka::PrefixItem> pre;      // static prefix items, unit-major, KV head minor
-    std::vector<int32_t> seq_pre_item;     // prefix item of (s, head 0), -1 if none
-    std::vector<int32_t> seq_pre_row;      // first row of s within its prefix item
     std::vector<int32_t> seq_prefix_len;   // prefix length of s's unit
-    std::vector<int32_t> row_info;         // [S * Hq][kRowInfo] merge table
     int32_t pre_slices = 0, pre_nonempty = 0;
     int32_t n_items = 0;       // prefix items + n_seqs * Hkv suffix items
     int32_t slot_rows = 0;     // rows of the largest item
@@ -40,13 +37,20 @@ struct fka_plan {
     int32_t n_slots = 0;       // partial-result slots in the workspace
     size_t workspace_bytes = 0;
     int device = 0;
+    // half of the schedule cache the next launch reads; a decode flips it after launching the
+    // merge that builds the other half
+    mutable uint32_t cache_cur = 0;
     // device memory (one allocation, carved)
     void *mem = nullptr;
     fka::PrefixItem *d_pre = nullptr;
-    int32_t *d_row_info = nullptr;
     int32_t *d_seq_prefix_len = nullptr;
     int32_t *err = nullptr;
-    int32_t *sched = nullptr;
+    int32_t *d_tab[2][2] = {};     // [half][candidate] (see the schedule cache in internal.h)
+    int32_t *d_key[2][2] = {};
+    int32_t *d_rowrec[2][2] = {};
+    int32_t *d_rowrec_live = nullptr;
+    int32_t *d_sel = nullptr;
+    int32_t *d_lens = nullptr;
     float *part_o = nullptr;
     float *part_lse = nullptr;
 };
@@ -123,19 +127,13 @@ fka_status check_rounds(int32_t rounds)
 fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>> &units, int32_t rounds_req)
 {
     p->pre.clear();
-    p->seq_pre_item.assign(p->n_seqs, -1);
-    p->seq_pre_row.assign(p->n_seqs, 0);
     p->seq_prefix_len.assign(p->n_seqs, 0);
     int64_t c = 0;
     int32_t k = 0, max_nseq = 1;
     for (size_t u = 0; u < units.size(); ++u) {
         const int32_t seq0 = units[u][0], nseq = units[u][1], n_tok = units[u][2];
         max_nseq = std::max(max_nseq, nseq);
-        for (int32_t i = seq0; i < seq0 + nseq; ++i) {
-            p->seq_pre_item[i] = (int32_t)(u * p->Hkv);
-            p->seq_pre_row[i] = (i - seq0) * p->G;
-            p->seq_prefix_len[i] = n_tok;
-        }
+        for (int32_t i = seq0; i < seq0 + nseq; ++i) p->seq_prefix_len[i] = n_tok;
         for (int32_t g = 0; g < p->Hkv; ++g) {
             fka::PrefixItem it{};
             it.seq0 = seq0;
@@ -153,24 +151,6 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     if (c > (int64_t)1 << 30) return fail(FKA_ERR_UNSUPPORTED, "prefix of %lld slices is too long", (long long)c);
     p->pre_slices = (int32_t)c;
     p->pre_nonempty = k;
-    p->row_info.assign((size_t)p->n_seqs * p->Hq * fka::kRowInfo, 0);
-    for (int s = 0; s < p->n_seqs; ++s)
-        for (int h = 0; h < p->Hq; ++h) {
-            int32_t *ri = &p->row_info[((size_t)s * p->Hq + h) * fka::kRowInfo];
-            const int g = h / p->G;
-            const int ip0 = p->seq_pre_item[s];
-            ri[0] = ip0 >= 0 ? ip0 + g : -1;
-            ri[1] = p->seq_pre_row[s] + h % p->G;
-            if (ip0 >= 0) {
-                const fka::PrefixItem &it = p->pre[ip0 + g];
-                ri[2] = it.c0;
-                ri[3] = it.k0;
-                ri[4] = fka::slices_of(it.n_tok);
-            }
-            ri[5] = s;
-            ri[6] = g;
-            ri[7] = h % p->G;
-        }
     p->n_items = (int32_t)p->pre.size() + p->n_seqs * p->Hkv;
     p->slot_rows = max_nseq * p->G;
     p->row_tiles = ceil_div(p->slot_rows, 16);
@@ -192,20 +172,25 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     return FKA_OK;
 }
 
-// Allocate device memory for the schedule tables, error flag, snapshot and workspace,
-// and upload the tables.
+// Allocate device memory for the static tables, the error flag, the schedule cache and the
+// partial-result workspace, and upload the tables.
 fka_status finish_plan(fka_plan *p)
 {
     hipError_t e;
     auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    const size_t workers = (size_t)p->n_blocks * p->rounds * p->waves;
+    const size_t rows = (size_t)p->n_seqs * p->Hq;
     const size_t b_pre = up(std::max<size_t>(1, p->pre.size()) * sizeof(fka::PrefixItem));
     const size_t b_seq = up((size_t)p->n_seqs * sizeof(int32_t));
-    const size_t b_rows = up(p->row_info.size() * sizeof(int32_t));
     const size_t b_err = 256;
-    const size_t b_sched = up((size_t)fka::sched_words(p->n_seqs) * sizeof(int32_t));
+    const size_t b_tab = up(workers * fka::kTabWords * sizeof(int32_t));
+    const size_t b_rec = up(rows * fka::kRowRec * sizeof(int32_t));
     const size_t b_po = up((size_t)p->n_slots * p->slot_rows * p->d * sizeof(float));
     const size_t b_pl = up((size_t)p->n_slots * p->slot_rows * sizeof(float));
-    const size_t total = b_pre + b_rows + b_seq + b_err + b_sched + b_po + b_pl;
+    // err, then the cache (tables and records zeroed, keys all -1: no cached schedule yet)
+    const size_t b_zero = b_err + 4 * b_tab + 5 * b_rec + 2 * b_seq;
+    const size_t b_keys = 4 * b_seq;
+    const size_t total = b_pre + b_seq + b_zero + b_keys + b_po + b_pl;
     e = hipMalloc(&p->mem, total);
     if (e != hipSuccess) {
         p->mem = nullptr;
@@ -215,18 +200,35 @@ fka_status finish_plan(fka_plan *p)
     char *m = static_cast<char *>(p->mem);
     p->d_pre = reinterpret_cast<fka::PrefixItem *>(m);
     m += b_pre;
-    p->d_row_info = reinterpret_cast<int32_t *>(m);
-    m += b_rows;
     p->d_seq_prefix_len = reinterpret_cast<int32_t *>(m);
     m += b_seq;
+    char *zero = m;
     p->err = reinterpret_cast<int32_t *>(m);
     m += b_err;
-    p->sched = reinterpret_cast<int32_t *>(m);
-    m += b_sched;
+    for (int h = 0; h < 2; ++h)
+        for (int c = 0; c < 2; ++c) {
+            p->d_tab[h][c] = reinterpret_cast<int32_t *>(m);
+            m += b_tab;
+            p->d_rowrec[h][c] = reinterpret_cast<int32_t *>(m);
+            m += b_rec;
+        }
+    p->d_rowrec_live = reinterpret_cast<int32_t *>(m);
+    m += b_rec;
+    p->d_lens = reinterpret_cast<int32_t *>(m);
+    m += b_seq;
+    p->d_sel = reinterpret_cast<int32_t *>(m);
+    m += b_seq;
+    char *keys = m;
+    for (int h = 0; h < 2; ++h)
+        for (int c = 0; c < 2; ++c) {
+            p->d_key[h][c] = reinterpret_cast<int32_t *>(m);
+            m += b_seq;
+        }
     p->part_o = reinterpret_cast<float *>(m);
     m += b_po;
     p->part_lse = reinterpret_cast<float *>(m);
     p->workspace_bytes = total;
+    p->cache_cur = 0;
     auto put = [&](void *dst, const void *src, size_t bytes, const char *what) -> fka_status {
         if (bytes == 0) return FKA_OK;
         const hipError_t r = hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice);
@@ -234,23 +236,30 @@ fka_status finish_plan(fka_plan *p)
     };
     fka_status st;
     if ((st = put(p->d_pre, p->pre.data(), p->pre.size() * sizeof(fka::PrefixItem), "hipMemcpy(prefix items)")) != FKA_OK ||
-        (st = put(p->d_row_info, p->row_info.data(), p->row_info.size() * sizeof(int32_t), "hipMemcpy(row table)")) != FKA_OK ||
         (st = put(p->d_seq_prefix_len, p->seq_prefix_len.data(), p->seq_prefix_len.size() * sizeof(int32_t),
                   "hipMemcpy(sequence tables)")) != FKA_OK)
         return st;
-    if ((e = hipMemset(p->err, 0, b_err + b_sched)) != hipSuccess) return hip_fail(e, "hipMemset(flags)");
+    if ((e = hipMemset(zero, 0, b_zero)) != hipSuccess) return hip_fail(e, "hipMemset(flags and cache)");
+    if ((e = hipMemset(keys, 0xff, b_keys)) != hipSuccess) return hip_fail(e, "hipMemset(cache keys)");
     return FKA_OK;
 }
 
 fka::AttnArgs attn_args(const fka_plan *p)
 {
     fka::AttnArgs a{};
+    const uint32_t c = p->cache_cur;
     a.pre_items = p->d_pre;
     a.n_pre = (int32_t)p->pre.size();
     a.pre_slices = p->pre_slices;
     a.pre_nonempty = p->pre_nonempty;
     a.seq_prefix_len = p->d_seq_prefix_len;
-    a.sched = p->sched;
+    for (int k = 0; k < 2; ++k) {
+        a.tab[k] = p->d_tab[c][k];
+        a.key[k] = p->d_key[c][k];
+    }
+    a.rowrec_live = p->d_rowrec_live;
+    a.sel = p->d_sel;
+    a.lens = p->d_lens;
     a.max_suffix_len = p->max_suffix_len;
     a.n_seqs = p->n_seqs;
     a.n_q_heads = p->Hq;
@@ -273,6 +282,7 @@ fka::AttnArgs attn_args(const fka_plan *p)
 fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *out, float *out_lse)
 {
     fka::MergeArgs m{};
+    const uint32_t c = p->cache_cur;
     m.part_o = p->part_o;
     m.part_lse = p->part_lse;
     m.out = out;
@@ -280,13 +290,25 @@ fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *o
     m.rows = p->n_seqs * p->Hq;
     m.n_q_heads = p->Hq;
     m.n_parts = 0;
-    m.sched = p->sched;
-    m.row_info = p->d_row_info;
+    m.rowrec[0] = p->d_rowrec[c][0];
+    m.rowrec[1] = p->d_rowrec[c][1];
+    m.rowrec[2] = p->d_rowrec_live;
+    m.sel = p->d_sel;
+    m.lens = p->d_lens;
+    m.slot_rows = p->slot_rows;
+    m.n_slots = p->n_slots;
+    for (int k = 0; k < 2; ++k) {
+        m.tab_next[k] = p->d_tab[c ^ 1][k];
+        m.key_next[k] = p->d_key[c ^ 1][k];
+        m.rowrec_next[k] = p->d_rowrec[c ^ 1][k];
+    }
+    m.pre_items = p->d_pre;
     m.n_pre = (int32_t)p->pre.size();
     m.pre_slices = p->pre_slices;
     m.pre_nonempty = p->pre_nonempty;
+    m.n_seqs = p->n_seqs;
     m.waves = p->waves;
-    m.slot_rows = p->slot_rows;
+    m.n_workers = p->n_blocks * p->rounds * p->waves;
     m.suffix_len = const_cast<int32_t *>(suffix_len);  // only a fused step writes it
     m.max_suffix_len = p->max_suffix_len;
     m.err = p->err;
@@ -308,6 +330,7 @@ fka_status run_decode(const fka_plan *p, const fka::AttnArgs &a, const int32_t *
     if (e != hipSuccess) return hip_fail(e, "partials kernel launch");
     e = fka::launch_merge(step ? *step : merge_args(p, suffix_len, out, out_lse), p->d, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+    p->cache_cur ^= 1u;  // the merge builds the other buffer for the next launch
     return ok();
 }
 

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 namespace fka {
@@ -46,24 +47,44 @@ struct PrefixItem {  // eight int32 fields, read field by field on the device
     int32_t pad0, pad1;
 };
 
-// Per-launch schedule snapshot written by the partial kernel (block 0) for the merge.
-// int32 words: [0] T, [1] non-empty items, [2] NV, [3] unused, then for sequence s:
-// [4 + 3s] clamped suffix length, [5 + 3s] CS(s), [6 + 3s] NE(s), where CS(s) and NE(s)
-// count the slices and the non-empty items of the suffix items of sequences before s.
-constexpr int kSchedHeader = 4;
-
-// Static per-row table of the merge (row = s * Hq + h, g = h / G), int32 words:
-// [0] prefix item of the row (-1 if none), [1] the row's row within it, [2] its C, [3] its K,
-// [4] its slices, [5] s, [6] g, [7] h % G (the row within the suffix item (s, g)).
-constexpr int kRowInfo = 8;
-__host__ __device__ inline int sched_words(int n_seqs) { return kSchedHeader + 3 * n_seqs; }
+// Schedule cache.  The schedule depends only on the plan and on the clamped suffix lengths.  The
+// merge kernel of each launch builds, into the other half of a ping-pong pair, the schedule for
+// two candidates of the next launch's lengths: candidate 0 = this launch's lengths (the next
+// call of a multi-layer model, or a decode without append) and, after a fused step, candidate 1
+// = the lengths after the append (the same layer's next step).  Per candidate:
+//   table  [workers][kTabWords]: what the partial kernel's placement puts in LDS for each
+//          worker (its item, the item's rows and keys, and its group in the block), plus the
+//          group's first slice at [kTabWords - 1];
+//   key    [S]: the clamped suffix lengths the table is for (-1 at [0]: none);
+//   rowrec [S * Hq][kRowRec]: for merge row (s, h) the offset (slot * slot_rows + row within the
+//          slot) of its first prefix part and the count of prefix parts, then the same for its
+//          suffix item; parts of one item sit in consecutive slots.
+// A launch reads half `cur` (the host alternates it after each merge).  The partial kernel
+// takes the first candidate whose key equals the clamped lengths it reads; if none does, it
+// builds the schedule itself and writes its slot records to a separate live buffer.  Block 0
+// records the choice (sel: 0, 1, or 2 for the live records) and the clamped lengths (lens) for
+// the merge.  Only the merge writes a candidate, so a key always describes its table and records.
+constexpr int kTabWords = 10;
+constexpr int kRowRec = 4;
 
 __host__ __device__ inline int32_t slices_of(int32_t tokens) { return (tokens + kSlice - 1) / kSlice; }
 
-// Fixed-point ratio workers per slice, R = floor(A * 2^32 / T) (A < 2^31, T > 0).
+// Fixed-point ratio workers per slice, R = floor(A * 2^32 / T) (0 <= A < 2^31, 0 < T < 2^31).
+// Exact, without a 64-bit integer division (a long software sequence on the GPU): a double
+// quotient is within 2^10 + 1 of R, a second one on the remainder brings it within 1, and the
+// last remainder fixes it.  Products and remainders stay below 2^63.
 __host__ __device__ inline uint64_t sched_ratio(int64_t A, int64_t T)
 {
-    return ((uint64_t)A << 32) / (uint64_t)T;
+    const uint64_t num = (uint64_t)A << 32, t = (uint64_t)T;
+    uint64_t q = (uint64_t)((double)num / (double)T);
+    int64_t rem = (int64_t)(num - q * t);
+    q = (uint64_t)((int64_t)q + (int64_t)floor((double)rem / (double)T));
+    rem = (int64_t)(num - q * t);
+    if (rem < 0)
+        --q;
+    else if (rem >= T)
+        ++q;
+    return q;
 }
 
 // First worker of an item that starts at slice C (C <= T, so C * R < 2^63) with K
@@ -86,13 +107,45 @@ __host__ __device__ inline void worker_range(int32_t j, int32_t w, int32_t size,
     }
 }
 
+// The group of virtual block vb on an item with workers [ws0, ws1) and `size` slices: the
+// block's workers [lo, hi) of the item and the union [glo, ghi) of their slice ranges.
+__host__ __device__ inline void block_group(int32_t vb, int32_t nw, int32_t ws0, int32_t ws1, int32_t size,
+                                            int32_t &lo, int32_t &hi, int32_t &glo, int32_t &ghi)
+{
+    lo = ws0 > vb * nw ? ws0 : vb * nw;
+    hi = ws1 < (vb + 1) * nw ? ws1 : (vb + 1) * nw;
+    int32_t dummy;
+    worker_range(lo - ws0, ws1 - ws0, size, glo, dummy);
+    worker_range(hi - 1 - ws0, ws1 - ws0, size, dummy, ghi);
+}
+
+// Slot records (kRowRec) of the rows of item i, whose parts are `count` consecutive slots from
+// slot vb0 + i: a prefix item's rows are (s, g*G + r) for s in [seq0, seq0 + nseq), a suffix
+// item's (seq0, g*G + r); the record's row within the slot is (s - seq0) * G + r.
+__host__ __device__ inline void write_rowrecs(int32_t *rowrec, int32_t i, int32_t n_pre, int32_t seq0, int32_t nseq,
+                                              int32_t g, int32_t G, int32_t Hq, int32_t slot_rows, int32_t vb0,
+                                              int32_t count)
+{
+    const int32_t field = i < n_pre ? 0 : 2;
+    for (int32_t s = 0; s < nseq; ++s)
+        for (int32_t r = 0; r < G; ++r) {
+            int32_t *rr = rowrec + ((size_t)(seq0 + s) * Hq + g * G + r) * kRowRec + field;
+            rr[0] = (vb0 + i) * slot_rows + s * G + r;
+            rr[1] = count;
+        }
+}
+
 struct AttnArgs {
     const PrefixItem *pre_items;  // [n_pre]
     int32_t n_pre;
     int32_t pre_slices;   // sum of the prefix items' slices
     int32_t pre_nonempty; // non-empty prefix items
     const int32_t *seq_prefix_len;  // [S] prefix length of each sequence's unit (paged page offsets)
-    int32_t *sched;       // per-launch snapshot for the merge
+    const int32_t *tab[2];  // schedule cache of this launch: candidate tables and keys
+    const int32_t *key[2];
+    int32_t *rowrec_live;   // slot records written when no candidate is taken
+    int32_t *sel;           // block 0 writes the choice: candidate 0 / 1, or 2 (live records)
+    int32_t *lens;          // [S] clamped suffix lengths of this launch, for the merge
     const uint16_t *q;  // [S][Hq][d]
     // contiguous layout
     const uint16_t *prefix_k, *prefix_v;  // [Hkv][Lp][d]
@@ -126,17 +179,24 @@ struct MergeArgs {
     float *out_lse;         // [rows] or null
     int32_t rows;
     int32_t n_q_heads;       // rows of one sequence (plan mode)
-    // explicit mode (sched == null): every row merges parts 0..n_parts-1
+    // explicit mode (rowrec == null): every row merges parts 0..n_parts-1
     int32_t n_parts;
     // plan mode: row (s, h) merges the slots of its prefix item and of its suffix item
-    const int32_t *sched;         // snapshot written by the partial kernel
-    const int32_t *row_info;      // [rows][kRowInfo] static per-row table (see kRowInfo)
+    const int32_t *rowrec[3];  // slot records: candidates 0 and 1 of this launch, live (see kRowRec)
+    const int32_t *sel;        // which of them this launch's partial kernel used
+    const int32_t *lens;       // this launch's clamped suffix lengths
+    int32_t slot_rows;
+    int32_t n_slots;           // records pointing outside [0, n_slots * slot_rows) are not followed
+    int32_t *err;
+    // schedule cache for the next launch (tab_next[0] null: none is built)
+    int32_t *tab_next[2], *key_next[2], *rowrec_next[2];
+    const PrefixItem *pre_items;
     int32_t n_pre;
     int32_t pre_slices;
     int32_t pre_nonempty;
-    int32_t waves;          // NW: workers per virtual block
-    int32_t slot_rows;
-    int32_t *err;
+    int32_t n_seqs;
+    int32_t waves;      // NW: workers per virtual block
+    int32_t n_workers;  // NV
     // fused step: the token in k_new / v_new (not yet in the cache) joins each row as one
     // more part; block (s, head 0) then stores it and advances suffix_len[s]
     int32_t step_mode;
@@ -190,6 +250,7 @@ struct GatherArgs {
 constexpr int32_t kErrSuffixClamped = 1;
 constexpr int32_t kErrAppendNoRoom = 2;
 constexpr int32_t kErrBadPage = 4;
+constexpr int32_t kErrBadSchedule = 8;
 
 hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);
 // Resident blocks per compute unit of the partial kernel for this shape (0 on error).

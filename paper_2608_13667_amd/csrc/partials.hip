@@ -210,10 +210,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     __shared__ int32_t s_spl[PAGED ? kMaxSeqs : 1];  // prefix length of each sequence's unit
     // each wave's item: item, seq0, nseq, kv head, keys, and its group (the block's waves on the
     // same item): first wave, first slice, end slice, end wave
-    __shared__ int32_t s_wf[NW][9];
-    __shared__ int32_t s_ctr[NW];    // next slice of the group led by this wave
+    __shared__ int32_t s_wfc[2][NW][9];  // per candidate schedule (the built one goes to [0])
+    __shared__ int32_t s_ctrc[2][NW];    // next slice of the group led by this wave
     __shared__ int32_t s_grp[NW][4];  // the block's groups: first wave, end wave, rows, item
     __shared__ int32_t s_ngrp;
+    __shared__ int32_t s_stale[NW];   // bit c: a wave saw a suffix length that differs from key c
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -221,146 +222,179 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     const int l16 = lane & 15, q4 = lane >> 4;
     const int G = a.group, Hkv = a.n_kv_heads, N = a.n_seqs;
 
-    // ---- schedule inputs in one round trip: the suffix lengths (and, paged, the prefix
-    // lengths of the sequences' units) and the static prefix item of this thread's first item
+    // ---- the schedule.  One round trip brings the suffix lengths (and, paged, the prefix
+    // lengths of the sequences' units), the cached candidates' keys and this block's table rows
+    // and the static prefix item of this thread's first item.  The first candidate whose key
+    // equals the clamped lengths is taken; otherwise the block builds the schedule (internal.h).
+    const int vb = (int)blockIdx.x;
+    const int w_lo = vb * NW;
+    // the kernel arguments this needs, all read before the first branch: the compiler would
+    // otherwise fetch them one branch at a time, a scalar round trip each
+    const int32_t *tab0 = a.tab[0] + (size_t)w_lo * kTabWords, *tab1 = a.tab[1] + (size_t)w_lo * kTabWords;
+    const int32_t *key0 = a.key[0], *key1 = a.key[1], *sl = a.suffix_len, *spl = a.seq_prefix_len;
+    const int32_t *pre = reinterpret_cast<const int32_t *>(a.pre_items);
+    int32_t *lens = a.lens;
+    const int n_pre = a.n_pre, max_len = a.max_suffix_len;
+    asm volatile("" ::"s"(tab0), "s"(tab1), "s"(key0), "s"(key1), "s"(sl), "s"(spl), "s"(pre), "s"(lens),
+                 "s"(n_pre), "s"(max_len));
+    int32_t tab_v[2] = {0, 0};
+    if (tid < NW * kTabWords) {
+        tab_v[0] = tab0[tid];
+        tab_v[1] = tab1[tid];
+    }
     int32_t my_pre[6] = {0, 0, 0, 0, 0, 0};  // seq0, nseq, kv_head, n_tok, c0, k0
-    if (tid < a.n_pre) {
-        const int32_t *ip = reinterpret_cast<const int32_t *>(a.pre_items + tid);
+    if (tid < n_pre) {
 #pragma unroll
-        for (int f = 0; f < 6; ++f) my_pre[f] = ip[f];
+        for (int f = 0; f < 6; ++f) my_pre[f] = pre[tid * 8 + f];
     }
-    if (tid < NW) s_wf[tid][0] = -1;  // waves the placement below does not reach have no item
-    // per-sequence suffix tables: clamped length, CS(s), NE(s) (exclusive scans)
-    int carry_cs = 0, carry_ne = 0;
-    bool clamped = false;
-    for (int base = 0; base < N; base += NTH) {
-        const int s = base + tid;
-        int L = 0;
-        if (s < N) {
-            const int raw = a.suffix_len[s];
-            L = min(max(raw, 0), a.max_suffix_len);
-            clamped |= (L != raw);
-            if (PAGED) s_spl[s] = a.seq_prefix_len[s];
-        }
-        const int xs = slices_of(L) * Hkv, xe = (L > 0) ? Hkv : 0;
-        int x = xs, y = xe;
+    bool clamped = false, stale0 = false, stale1 = false;
+    for (int s = tid; s < N; s += NTH) {
+        const int raw = sl[s];
+        const int k0 = key0[s], k1 = key1[s];
+        const int L = min(max(raw, 0), max_len);
+        clamped |= (L != raw);
+        stale0 |= (k0 != L);
+        stale1 |= (k1 != L);
+        s_len[s] = L;
+        if (PAGED) s_spl[s] = spl[s];
+        if (vb == 0) lens[s] = L;  // what the merge appends at
+    }
+    if (vb == 0 && clamped) atomicOr(a.err, kErrSuffixClamped);
+    const int wave_stale = (__builtin_amdgcn_ballot_w64(stale0) != 0 ? 1 : 0) |
+                           (__builtin_amdgcn_ballot_w64(stale1) != 0 ? 2 : 0);
+    if (lane == 0) s_stale[wave] = wave_stale;
+    if (tid < NW * kTabWords) {  // both candidates' rows; the chosen one is used below
+        const int w = tid / kTabWords, f = tid % kTabWords;
 #pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const int ux = __shfl_up(x, off), uy = __shfl_up(y, off);
-            if (lane >= off) {
-                x += ux;
-                y += uy;
+        for (int c = 0; c < 2; ++c) {
+            if (f < kTabWords - 1)
+                s_wfc[c][w][f] = tab_v[c];
+            else
+                s_ctrc[c][w] = tab_v[c];
+        }
+    }
+    lds_barrier();
+    int any_stale = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) any_stale |= s_stale[w];
+    any_stale = __builtin_amdgcn_readfirstlane(any_stale);
+    const int choice = !(any_stale & 1) ? 0 : !(any_stale & 2) ? 1 : 2;
+    if (vb == 0 && tid == 0) *a.sel = choice;
+    int32_t(*s_wf)[9] = s_wfc[choice == 1 ? 1 : 0];
+    int32_t *s_ctr = s_ctrc[choice == 1 ? 1 : 0];
+    if (choice == 2) {
+        if (tid < NW) s_wf[tid][0] = -1;  // waves the placement below does not reach have no item
+        // per-sequence suffix tables: CS(s), NE(s) (exclusive scans)
+        int carry_cs = 0, carry_ne = 0;
+        for (int base = 0; base < N; base += NTH) {
+            const int s = base + tid;
+            const int L = s < N ? s_len[s] : 0;
+            const int xs = slices_of(L) * Hkv, xe = (L > 0) ? Hkv : 0;
+            int x = xs, y = xe;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int ux = __shfl_up(x, off), uy = __shfl_up(y, off);
+                if (lane >= off) {
+                    x += ux;
+                    y += uy;
+                }
+            }
+            if (lane == 63) {
+                s_wsum[0][wave] = x;
+                s_wsum[1][wave] = y;
+            }
+            lds_barrier();
+            int px = carry_cs, py = carry_ne;
+            for (int w = 0; w < NW; ++w) {
+                if (w < wave) {
+                    px += s_wsum[0][w];
+                    py += s_wsum[1][w];
+                }
+                carry_cs += s_wsum[0][w];
+                carry_ne += s_wsum[1][w];
+            }
+            if (s < N) {
+                s_cs[s] = px + x - xs;
+                s_ne[s] = py + y - xe;
+            }
+            lds_barrier();
+        }
+        const int T = __builtin_amdgcn_readfirstlane(a.pre_slices + carry_cs);      // total slices
+        const int NNE = __builtin_amdgcn_readfirstlane(a.pre_nonempty + carry_ne);  // non-empty items
+        const int NV = (int)gridDim.x * NW;  // workers: every block is one virtual block
+        const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
+        const int n_items = a.n_pre + N * Hkv;
+        // every thread places its items' workers of this block; the block holding an item's
+        // first worker writes the item's slot records for the merge (block 0 those of empty items)
+        for (int i = tid; i < n_items; i += NTH) {
+            int f[6];
+            int size, C, K;
+            if (i < a.n_pre) {
+                if (i == tid) {  // loaded at the start
+#pragma unroll
+                    for (int k = 0; k < 6; ++k) f[k] = my_pre[k];
+                } else {
+                    const int32_t *ip = reinterpret_cast<const int32_t *>(a.pre_items + i);
+#pragma unroll
+                    for (int k = 0; k < 6; ++k) f[k] = ip[k];
+                }
+                size = slices_of(f[3]);
+                C = f[4];
+                K = f[5];
+            } else {
+                const int j = i - a.n_pre, sq = j / Hkv, g = j % Hkv;
+                f[0] = sq;
+                f[1] = 1;
+                f[2] = g;
+                f[3] = s_len[sq];
+                size = slices_of(f[3]);
+                C = a.pre_slices + s_cs[sq] + g * size;
+                K = a.pre_nonempty + s_ne[sq] + (size > 0 ? g : 0);
+            }
+            if (size == 0 || T == 0) {
+                if (vb == 0) write_rowrecs(a.rowrec_live, i, a.n_pre, f[0], f[1], f[2], G, a.n_q_heads, a.slot_rows, 0, 0);
+                continue;
+            }
+            const int ws0 = worker_start(C, K, R), ws1 = worker_start(C + size, K + 1, R);
+            if (ws0 >= w_lo && ws0 < w_lo + NW)
+                write_rowrecs(a.rowrec_live, i, a.n_pre, f[0], f[1], f[2], G, a.n_q_heads, a.slot_rows, vb,
+                              (ws1 - 1) / NW - vb + 1);
+            if (ws1 <= w_lo || ws0 >= w_lo + NW) continue;
+            // the block's workers [lo, hi) of this item form one group over the union of
+            // their slice ranges; its waves take the slices one by one
+            int lo, hi, glo, ghi;
+            block_group(vb, NW, ws0, ws1, size, lo, hi, glo, ghi);
+            s_ctr[lo - w_lo] = glo;
+            for (int gw = lo; gw < hi; ++gw) {
+                int32_t *d = s_wf[gw - w_lo];
+                d[0] = i;
+                d[1] = f[0];
+                d[2] = f[1];
+                d[3] = f[2];
+                d[4] = f[3];
+                d[5] = lo - w_lo;
+                d[6] = glo;
+                d[7] = ghi;
+                d[8] = hi - w_lo;
             }
         }
-        if (lane == 63) {
-            s_wsum[0][wave] = x;
-            s_wsum[1][wave] = y;
-        }
         lds_barrier();
-        int px = carry_cs, py = carry_ne;
-        for (int w = 0; w < NW; ++w) {
-            if (w < wave) {
-                px += s_wsum[0][w];
-                py += s_wsum[1][w];
-            }
-            carry_cs += s_wsum[0][w];
-            carry_ne += s_wsum[1][w];
-        }
-        if (s < N) {
-            s_len[s] = L;
-            s_cs[s] = px + x - xs;
-            s_ne[s] = py + y - xe;
-        }
-        lds_barrier();
-    }
-    const int T = __builtin_amdgcn_readfirstlane(a.pre_slices + carry_cs);      // total slices of this launch
-    const int NNE = __builtin_amdgcn_readfirstlane(a.pre_nonempty + carry_ne);  // non-empty items
-    const int NV = (int)gridDim.x * NW;  // workers: every block is one virtual block
-    const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
-    const int n_items = a.n_pre + N * Hkv;
-
-    if (blockIdx.x == 0) {  // the snapshot the merge reads
-        for (int s = tid; s < N; s += NTH) {
-            a.sched[kSchedHeader + 3 * s] = s_len[s];
-            a.sched[kSchedHeader + 3 * s + 1] = s_cs[s];
-            a.sched[kSchedHeader + 3 * s + 2] = s_ne[s];
-        }
-        if (tid == 0) {
-            a.sched[0] = T;
-            a.sched[1] = NNE;
-            a.sched[2] = NV;
-            a.sched[3] = 0;
-        }
-        if (clamped) atomicOr(a.err, kErrSuffixClamped);
     }
 
     {
-        const int vb = (int)blockIdx.x;
-        const int w_lo = vb * NW;
-        // every thread places its items' workers of this block
-        if (T > 0) {
-            for (int i = tid; i < n_items; i += NTH) {
-                int f[6];
-                int size, C, K;
-                if (i < a.n_pre) {
-                    if (i == tid) {  // loaded at the start
-#pragma unroll
-                        for (int k = 0; k < 6; ++k) f[k] = my_pre[k];
-                    } else {
-                        const int32_t *ip = reinterpret_cast<const int32_t *>(a.pre_items + i);
-#pragma unroll
-                        for (int k = 0; k < 6; ++k) f[k] = ip[k];
-                    }
-                    size = slices_of(f[3]);
-                    C = f[4];
-                    K = f[5];
-                } else {
-                    const int j = i - a.n_pre, sq = j / Hkv, g = j % Hkv;
-                    f[0] = sq;
-                    f[1] = 1;
-                    f[2] = g;
-                    f[3] = s_len[sq];
-                    size = slices_of(f[3]);
-                    C = a.pre_slices + s_cs[sq] + g * size;
-                    K = a.pre_nonempty + s_ne[sq] + (size > 0 ? g : 0);
-                }
-                if (size == 0) continue;
-                const int ws0 = worker_start(C, K, R), ws1 = worker_start(C + size, K + 1, R);
-                const int lo = max(ws0, w_lo), hi = min(ws1, w_lo + NW);
-                if (lo >= hi) continue;
-                // the block's workers [lo, hi) of this item form one group over the union of
-                // their slice ranges; its waves take the slices one by one
-                int glo, ghi, dummy;
-                worker_range(lo - ws0, ws1 - ws0, size, glo, dummy);
-                worker_range(hi - 1 - ws0, ws1 - ws0, size, dummy, ghi);
-                s_ctr[lo - w_lo] = glo;
-                for (int gw = lo; gw < hi; ++gw) {
-                    int32_t *d = s_wf[gw - w_lo];
-                    d[0] = i;
-                    d[1] = f[0];
-                    d[2] = f[1];
-                    d[3] = f[2];
-                    d[4] = f[3];
-                    d[5] = lo - w_lo;
-                    d[6] = glo;
-                    d[7] = ghi;
-                    d[8] = hi - w_lo;
-                }
-            }
-        }
-        lds_barrier();
         const int item = __builtin_amdgcn_readfirstlane(s_wf[wave][0]);
-        if (tid == 0) {  // the block's groups, in wave order (read after the combine barrier)
-            int n = 0;
-            for (int w = 0; w < NW; ++w) {
-                if (s_wf[w][0] < 0 || s_wf[w][5] != w) continue;
+        if (wave == 0) {  // the block's groups, in wave order (read after the combine barrier)
+            const int w = lane < NW ? lane : 0;  // lane w looks at wave w
+            const bool lead = lane < NW && s_wf[w][0] >= 0 && s_wf[w][5] == w;
+            const uint64_t m = __builtin_amdgcn_ballot_w64(lead);
+            if (lead) {
+                const int n = __builtin_popcountll(m & ((uint64_t(1) << w) - 1));
                 s_grp[n][0] = w;
                 s_grp[n][1] = s_wf[w][8];
                 s_grp[n][2] = s_wf[w][2] * G;
                 s_grp[n][3] = s_wf[w][0];
-                ++n;
             }
-            s_ngrp = n;
+            if (lane == 0) s_ngrp = __builtin_popcountll(m);
         }
 
         // ---- this wave's item and group (all values uniform)

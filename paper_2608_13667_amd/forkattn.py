@@ -21,7 +21,7 @@ if not os.path.exists(LIB_PATH):
 _lib = C.CDLL(LIB_PATH)
 
 FKA_OK, FKA_ERR_INVALID_ARG, FKA_ERR_UNSUPPORTED, FKA_ERR_HIP, FKA_ERR_NOMEM = 0, -1, -2, -3, -4
-ERR_SUFFIX_CLAMPED, ERR_APPEND_NO_ROOM, ERR_BAD_PAGE = 1, 2, 4
+ERR_SUFFIX_CLAMPED, ERR_APPEND_NO_ROOM, ERR_BAD_PAGE, ERR_BAD_SCHEDULE = 1, 2, 4, 8
 
 
 class Heads(C.Structure):

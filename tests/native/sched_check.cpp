@@ -26,6 +26,22 @@ int main(int argc, char **argv)
 {
     const int cases = argc > 1 ? std::atoi(argv[1]) : 2000;
     std::mt19937_64 rng(12345);
+    // sched_ratio against the plain 64-bit division: edge values and random pairs over the range
+    {
+        const int64_t edge[] = {0, 1, 2, 3, 31, 32, 33, 1000, 65535, 65536, 1 << 20, (1 << 30) - 1, 1 << 30,
+                                (int64_t(1) << 31) - 2, (int64_t(1) << 31) - 1};
+        auto ref = [](int64_t A, int64_t T) { return ((uint64_t)A << 32) / (uint64_t)T; };
+        for (int64_t A : edge)
+            for (int64_t T : edge)
+                if (T > 0 && sched_ratio(A, T) != ref(A, T)) return fail("sched_ratio differs (edge)", (int)A);
+        for (int k = 0; k < 2000000; ++k) {
+            const int shift_a = (int)(rng() % 32), shift_t = (int)(rng() % 32);
+            const int64_t A = (int64_t)(rng() & ((uint64_t(1) << shift_a) - 1));
+            const int64_t T = 1 + (int64_t)(rng() & ((uint64_t(1) << shift_t) - 1));
+            if (A >= (int64_t(1) << 31) || T >= (int64_t(1) << 31)) continue;
+            if (sched_ratio(A, T) != ref(A, T)) return fail("sched_ratio differs", k);
+        }
+    }
     for (int c = 0; c < cases; ++c) {
         const int n_items = 1 + (int)(rng() % 300);
         const int NW = (rng() % 2) ? 8 : 4;

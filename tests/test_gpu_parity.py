@@ -227,6 +227,38 @@ def _check_slots(fa, w, plan, note):
             assert a1 == b0, key
 
 
+def test_schedule_cache_follows_length_changes(fa):
+    """Each decode builds the schedule of the next one for the lengths it expects, keyed by them.
+    Lengths set by the host between calls (new ones, empty suffixes, an earlier set again), a
+    partial stage launched in between, and repeated calls at the same lengths (which take the
+    cached schedule) all match the oracle."""
+    w = W.make("mid", steps=0, seed=83)
+    plan = contig_plan(fa, w)
+    dv = to_dev_contig(w)
+    N, Hq, d = w.q.shape
+    info = plan.info()
+    rng = np.random.default_rng(12)
+    # lengths up to the generated ones (positions past them hold NaN on purpose)
+    full = w.suffix_len.astype(np.int64)
+    sets = [w.suffix_len.copy(), rng.integers(0, full + 1).astype(np.int32), w.suffix_len.copy(),
+            np.zeros(N, np.int32), np.minimum(rng.integers(0, 40, N), full).astype(np.int32), w.suffix_len.copy()]
+    for i, ln in enumerate(sets):
+        print(f"[cache] set {i}: {ln.tolist()}", flush=True)
+        dv["suffix_len"].copy_(torch.from_numpy(ln))
+        ref, ref_lse = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, ln,
+                                            w.spec.softmax_scale)
+        for rep in range(3):
+            if rep == 1 and i in (1, 4):
+                po = torch.empty((info.n_slots, info.slot_rows, d), device="cuda")
+                pl = torch.empty((info.n_slots, info.slot_rows), device="cuda")
+                plan.partials(dv["q"], dv["prefix_k"], dv["prefix_v"], dv["suffix_k"], dv["suffix_v"],
+                              dv["suffix_len"], po, pl)
+            out, lse = run_contig(plan, dv, Hq)
+            gates.assert_gates(out, ref, what=f"set {i} call {rep}")
+            gates.assert_lse(lse, ref_lse, what=f"set {i} call {rep}")
+    assert plan.device_error() == 0
+
+
 @pytest.mark.parametrize("rounds", [0, 5])
 def test_partials_stage(fa, rounds):
     """Each first-stage partial equals the oracle's attention over that slot's key range."""
