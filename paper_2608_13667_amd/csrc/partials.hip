@@ -671,7 +671,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
         // Threads then own (row, chunk) units of each group: they weigh the group's waves by
         // exp(max_w - max) and sum.  All global stores of a pass follow its LDS work.
         static_assert(2 * 16 * HD * 4 <= kStages * SLICE_CHUNKS * 16, "two tiles fit in a wave's ring");
-        constexpr int CH4 = HD / 4;
+        constexpr int CH8 = HD / 8;
         auto stg = [&](int w) { return reinterpret_cast<float *>(&vring[w][0][0]); };
         auto stg_off = [&](int tt, int r, int c4) {  // float offset of chunk c4 (4 floats)
             return (tt * 16 + r) * HD + 16 * ((c4 >> 2) ^ (r & (NE - 1))) + 4 * (c4 & 3);
@@ -695,23 +695,25 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                 const int lw = s_grp[g][0], ge = s_grp[g][1], it = s_grp[g][3];
                 if (vb + it >= a.n_slots || it < 0) continue;  // never store outside the workspace
                 const int r0 = 32 * pass, r1 = min(s_grp[g][2], r0 + 32);
-                for (int u = tid_c; u < (r1 - r0) * CH4; u += NTH) {
-                    const int row = r0 + u / CH4, c = u % CH4;
+                // a unit is 8 floats of one row: the group's weights are computed once per unit
+                for (int u = tid_c; u < (r1 - r0) * CH8; u += NTH) {
+                    const int row = r0 + u / CH8, c8 = u % CH8;
                     const int t = row >> 4, tt = t - 2 * pass, r = row & 15;
                     float mw[NW], lw_[NW];
-                    f32x4 v[NW];
+                    f32x4 v0[NW], v1[NW];
 #pragma unroll
                     for (int w = 0; w < NW; ++w) {
                         mw[w] = red_m[w][t][r];
                         lw_[w] = red_l[w][t][r];
-                        v[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, c)]);
+                        v0[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, 2 * c8)]);
+                        v1[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, 2 * c8 + 1)]);
                     }
                     float M = -INFINITY;
 #pragma unroll
                     for (int w = 0; w < NW; ++w) M = (w >= lw && w < ge) ? fmaxf(M, mw[w]) : M;
                     const float Mu = (M == -INFINITY) ? 0.f : M;
                     float L = 0.f;
-                    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+                    f32x4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int w = 0; w < NW; ++w) {
                         // waves outside the group are selected out, not weighted by 0: their
@@ -720,13 +722,17 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                         const bool in = w >= lw && w < ge;
                         const float wt = (in && mw[w] != -INFINITY) ? fast_exp2(mw[w] - Mu) : 0.f;
                         L = in ? L + wt * lw_[w] : L;
-                        o = in ? o + wt * v[w] : o;
+                        o0 = in ? o0 + wt * v0[w] : o0;
+                        o1 = in ? o1 + wt * v1[w] : o1;
                     }
                     // L == 0 only when the group saw no keys; a NaN input keeps propagating
-                    const f32x4 res = (L == 0.f) ? f32x4{0.f, 0.f, 0.f, 0.f} : o / L;
+                    const float inv = __builtin_amdgcn_rcpf(L);
+                    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
                     const size_t so = (size_t)(vb + it) * a.slot_rows + row;
-                    *reinterpret_cast<f32x4 *>(a.part_o + so * HD + 4 * c) = res;
-                    if (c == 0) a.part_lse[so] = (L == 0.f) ? -INFINITY : (Mu + log2f(L)) * kLn2;
+                    float *dst = a.part_o + so * HD + 8 * c8;
+                    *reinterpret_cast<f32x4 *>(dst) = (L == 0.f) ? z : o0 * inv;
+                    *reinterpret_cast<f32x4 *>(dst + 4) = (L == 0.f) ? z : o1 * inv;
+                    if (c8 == 0) a.part_lse[so] = (L == 0.f) ? -INFINITY : (Mu + log2f(L)) * kLn2;
                 }
             }
         }
