@@ -203,8 +203,8 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
 
     // per wave: kStages V slices; chunk c of slice token T sits at T*CPR + (c ^ swz(T))
     __shared__ uint4 vring[NW][kStages][SLICE_CHUNKS];
-    __shared__ float red_m[NW][NT][16];
-    __shared__ float red_l[NW][NT][16];
+    __shared__ __attribute__((aligned(16))) float red_m[NT][16][NW];  // per row, the waves side by side
+    __shared__ __attribute__((aligned(16))) float red_l[NT][16][NW];
     __shared__ int32_t s_len[kMaxSeqs], s_cs[kMaxSeqs], s_ne[kMaxSeqs];
     __shared__ int32_t s_wsum[2][NW];
     __shared__ int32_t s_spl[PAGED ? kMaxSeqs : 1];  // prefix length of each sequence's unit
@@ -661,8 +661,8 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
         for (int t = 0; t < NT; ++t) {
             const float ls = sum_over_rows(l_run[t]);
             if (q4c == 0) {
-                red_m[wave][t][l16c] = m_ref[t];
-                red_l[wave][t][l16c] = ls;
+                red_m[t][l16c][wave] = m_ref[t];
+                red_l[t][l16c][wave] = ls;
             }
         }
         wait_vm<0>();  // this wave's ring is idle: it takes the wave's raw accumulators
@@ -703,8 +703,8 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                     f32x4 v0[NW], v1[NW];
 #pragma unroll
                     for (int w = 0; w < NW; ++w) {
-                        mw[w] = red_m[w][t][r];
-                        lw_[w] = red_l[w][t][r];
+                        mw[w] = red_m[t][r][w];
+                        lw_[w] = red_l[t][r][w];
                         v0[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, 2 * c8)]);
                         v1[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, 2 * c8 + 1)]);
                     }
