@@ -149,8 +149,8 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
         return;
     }
 
-    // Everything this block reads first is requested together: the row's static table and the
-    // schedule snapshot (plan mode) and, in a fused step, q and the appended key.
+    // Everything this block reads first is requested together: the row's slot records and the
+    // schedule choice (plan mode) and, in a fused step, q and the appended key and value.
     // Parts of this row, as offsets (part index * row stride + row) into part_o / part_lse:
     // parts [0, np) start at p_first with stride p_step; parts [np, n) at s_first.
     int np = 0, n = 0, L = 0, seq = 0, g = 0;
@@ -158,6 +158,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
     bool with_new = false;  // fused step: the appended token is one more part, read from k_new / v_new
     float dot = 0.f;
     uint4 app_k = {0, 0, 0, 0}, app_v = {0, 0, 0, 0};  // fused step, block (s, 0): the token to store
+    uint2 new_v = {0, 0};                              // fused step: this thread's 4 values of v_new
     constexpr int APP = HD / 8;                        // 16-byte chunks of one K/V row
     if (a.rowrec[0]) {
         seq = row / a.n_q_heads;
@@ -175,6 +176,8 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
             app_v = *reinterpret_cast<const uint4 *>(a.v_new + src);
         }
         with_new = a.step_mode && L < a.max_suffix_len;
+        if (a.step_mode && slice == 0)
+            new_v = *reinterpret_cast<const uint2 *>(a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk);
         if (with_new && wave == 0) {  // q . k_new, wave 0
             const uint16_t *qr = a.q + (size_t)row * HD;
             const uint16_t *kr = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
@@ -223,8 +226,8 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
         for (int u = 0; u < U; ++u) {
             if (l[u] == -INFINITY) continue;
             const float mn = fmaxf(m, l[u]);
-            const float sc = (m == -INFINITY) ? 0.f : exp2f((m - mn) * kLog2e);
-            const float e = exp2f((l[u] - mn) * kLog2e);
+            const float sc = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((m - mn) * kLog2e);
+            const float e = __builtin_amdgcn_exp2f((l[u] - mn) * kLog2e);
             w = w * sc + e;
             acc = acc * sc + e * o[u];
             m = mn;
@@ -251,19 +254,18 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
         if (M != -INFINITY) {
 #pragma unroll
             for (int k = 0; k < SL; ++k) {
-                const float sc = (s_m[k] == -INFINITY) ? 0.f : exp2f((s_m[k] - M) * kLog2e);
+                const float sc = (s_m[k] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((s_m[k] - M) * kLog2e);
                 t += sc * s_acc[k][chunk];
                 W += sc * s_w[k];
             }
             if (with_new) {
-                const uint16_t *vr = a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk;
-                const float e = exp2f((lse_new - M) * kLog2e);
+                const float e = __builtin_amdgcn_exp2f((lse_new - M) * kLog2e);
                 W += e;
-                t += e * f32x4{__uint_as_float((uint32_t)vr[0] << 16), __uint_as_float((uint32_t)vr[1] << 16),
-                               __uint_as_float((uint32_t)vr[2] << 16), __uint_as_float((uint32_t)vr[3] << 16)};
+                t += e * f32x4{__uint_as_float(new_v.x << 16), __uint_as_float(new_v.x & 0xffff0000u),
+                               __uint_as_float(new_v.y << 16), __uint_as_float(new_v.y & 0xffff0000u)};
             }
         }
-        const f32x4 r = (W == 0.f) ? f32x4{0.f, 0.f, 0.f, 0.f} : t / W;
+        const f32x4 r = (W == 0.f) ? f32x4{0.f, 0.f, 0.f, 0.f} : t * __builtin_amdgcn_rcpf(W);
         *reinterpret_cast<f32x4 *>(a.out + (size_t)row * HD + 4 * chunk) = r;
         if (a.out_lse && chunk == 0) a.out_lse[row] = (W == 0.f) ? -INFINITY : M + logf(W);
     }
