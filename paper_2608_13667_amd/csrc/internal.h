@@ -53,8 +53,7 @@ struct PrefixItem {  // eight int32 fields, read field by field on the device
 // call of a multi-layer model, or a decode without append) and, after a fused step, candidate 1
 // = the lengths after the append (the same layer's next step).  Per candidate:
 //   table  [workers][kTabWords]: what the partial kernel's placement puts in LDS for each
-//          worker (its item, the item's rows and keys, and its group in the block), plus the
-//          group's first slice at [kTabWords - 1];
+//          worker (its item, the item's rows and keys, and its group in the block);
 //   key    [S]: the clamped suffix lengths the table is for (-1 at [0]: none);
 //   rowrec [S * Hq][kRowRec]: for merge row (s, h) the offset (slot * slot_rows + row within the
 //          slot) of its first prefix part and the count of prefix parts, then the same for its
@@ -64,7 +63,7 @@ struct PrefixItem {  // eight int32 fields, read field by field on the device
 // builds the schedule itself and writes its slot records to a separate live buffer.  Block 0
 // records the choice (sel: 0, 1, or 2 for the live records) and the clamped lengths (lens) for
 // the merge.  Only the merge writes a candidate, so a key always describes its table and records.
-constexpr int kTabWords = 10;
+constexpr int kTabWords = 9;
 constexpr int kRowRec = 4;
 
 __host__ __device__ inline int32_t slices_of(int32_t tokens) { return (tokens + kSlice - 1) / kSlice; }

@@ -120,7 +120,6 @@ __device__ void build_next_schedule(const MergeArgs &a, int cand, int pb, int np
             t[6] = glo;
             t[7] = ghi;
             t[8] = hi - vb * NW;
-            t[9] = glo;
         }
     }
 }

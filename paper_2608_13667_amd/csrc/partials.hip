@@ -3,9 +3,9 @@
 //
 // Every launch first rebuilds the work schedule (internal.h) from the suffix lengths on
 // the device: the 32-token slices of the shared prefix items and of the suffix items are
-// spread evenly over all waves of the grid.  The waves of a block that share an item take
-// the slices of their joint range one at a time from an LDS counter, so the block streams
-// one contiguous region and its waves finish together.  An item holds every query row that reads its keys: for a
+// spread evenly over all waves of the grid.  The waves of a block that share an item deal
+// the slices of their joint range among themselves in turn, so the block streams one
+// contiguous region and its waves finish together.  An item holds every query row that reads its keys: for a
 // shared-prefix item, all sequences of the fork x the G query heads of the KV head, so
 // each prefix K/V byte is fetched from HBM once for all branches (paper, Sec. 3.3: the
 // prefix cache is reused by all decoding streams).  Within a wave:
@@ -211,7 +211,6 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     // each wave's item: item, seq0, nseq, kv head, keys, and its group (the block's waves on the
     // same item): first wave, first slice, end slice, end wave
     __shared__ int32_t s_wfc[2][NW][9];  // per candidate schedule (the built one goes to [0])
-    __shared__ int32_t s_ctrc[2][NW];    // next slice of the group led by this wave
     __shared__ int32_t s_grp[NW][4];  // the block's groups: first wave, end wave, rows, item
     __shared__ int32_t s_ngrp;
     __shared__ int32_t s_stale[NW];   // bit c: a wave saw a suffix length that differs from key c
@@ -265,13 +264,8 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     if (lane == 0) s_stale[wave] = wave_stale;
     if (tid < NW * kTabWords) {  // both candidates' rows; the chosen one is used below
         const int w = tid / kTabWords, f = tid % kTabWords;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            if (f < kTabWords - 1)
-                s_wfc[c][w][f] = tab_v[c];
-            else
-                s_ctrc[c][w] = tab_v[c];
-        }
+        s_wfc[0][w][f] = tab_v[0];
+        s_wfc[1][w][f] = tab_v[1];
     }
     lds_barrier();
     int any_stale = 0;
@@ -281,7 +275,6 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     const int choice = !(any_stale & 1) ? 0 : !(any_stale & 2) ? 1 : 2;
     if (vb == 0 && tid == 0) *a.sel = choice;
     int32_t(*s_wf)[9] = s_wfc[choice == 1 ? 1 : 0];
-    int32_t *s_ctr = s_ctrc[choice == 1 ? 1 : 0];
     if (choice == 2) {
         if (tid < NW) s_wf[tid][0] = -1;  // waves the placement below does not reach have no item
         // per-sequence suffix tables: CS(s), NE(s) (exclusive scans)
@@ -361,10 +354,9 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                               (ws1 - 1) / NW - vb + 1);
             if (ws1 <= w_lo || ws0 >= w_lo + NW) continue;
             // the block's workers [lo, hi) of this item form one group over the union of
-            // their slice ranges; its waves take the slices one by one
+            // their slice ranges; its waves deal the slices in turn
             int lo, hi, glo, ghi;
             block_group(vb, NW, ws0, ws1, size, lo, hi, glo, ghi);
-            s_ctr[lo - w_lo] = glo;
             for (int gw = lo; gw < hi; ++gw) {
                 int32_t *d = s_wf[gw - w_lo];
                 d[0] = i;
@@ -416,11 +408,15 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
         // keys of the group end at tok_lim: loads past it (the prefetch beyond the last slice)
         // move no data, and scores past it are masked
         const int tok_lim = min(tok_end, ghi * kSlice);
-        // next slice of the group (LDS counter shared by the group's waves; one lane adds)
+        // next slice of this wave: wave j of the group's g waves takes glo + j, glo + j + g, ...
+        // (a fixed assignment, so results repeat bit for bit; it also measured faster than
+        // taking slices from a shared LDS counter, whose round trip delayed each slice's loads)
+        const int g_waves = item >= 0 ? __builtin_amdgcn_readfirstlane(s_wf[wave][8]) - wa : 1;
+        int next_slice = (item >= 0 ? __builtin_amdgcn_readfirstlane(s_wf[wave][6]) : 0) + (wave - wa);
         auto grab = [&]() -> int {
-            int k = 0;
-            if (lane == 0) k = atomicAdd(&s_ctr[wa], 1);
-            return __builtin_amdgcn_readfirstlane(k);
+            const int k = next_slice;
+            next_slice += g_waves;
+            return k;
         };
 
         // key source of the item
