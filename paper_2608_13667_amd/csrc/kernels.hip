@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 
     // Fused step: block (s, head 0) stores the token sequence s appended (already attended
     // to from k_new / v_new) and advances suffix_len[s].  No block of this kernel reads the
-    // suffix cache or suffix_len (the lengths come from the snapshot), so nothing races.
+    // suffix cache or suffix_len (the lengths come from the partial kernel), so nothing races.
     if (!a.step_mode || row % a.n_q_heads != 0) return;
     bool ok = L < a.max_suffix_len;
     int page = 0;
