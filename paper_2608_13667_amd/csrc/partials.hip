@@ -63,12 +63,22 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const char *base, int bytes)
     return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), 0, n, 0x00020000);
 }
 
+// Cache policy of the K/V stream.  Contiguous K/V: non-temporal (each byte is read once;
+// measured 6% faster on the 32k-prefix workload and 13% on the 128k one).  Paged K/V (4 KiB
+// blocks in page order): the default policy (non-temporal measured 9% slower there).
+template <bool PAGED>
+constexpr int stream_policy()
+{
+    return PAGED ? 0 : 2;
+}
+
 // 16 bytes per lane from a buffer into LDS at dst + 16 * lane (LDS DMA).  Kept outside
 // the kernel template: used directly there, the builtin stops the host compiler from
 // emitting the kernel's launch stub.
+template <int POLICY>
 __device__ inline void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, lds_void *dst, uint32_t voff)
 {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, 0, 0, POLICY);
 }
 
 // Uniform (scalar-unit) load of a value that no kernel in flight writes.
@@ -487,7 +497,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                 const __amdgpu_buffer_rsrc_t r = group_rsrc(kbase, t0 + 16 * u);
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
-                    kr[u][c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, koff + 64 * c, 0, 0));
+                    kr[u][c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, koff + 64 * c, 0, stream_policy<PAGED>()));
             }
         };
 
@@ -508,7 +518,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
             const __amdgpu_buffer_rsrc_t r0 = group_rsrc(vbase, t0), r1 = group_rsrc(vbase, t0 + 16);
 #pragma unroll
             for (int i = 0; i < VDMA; ++i)
-                buffer_to_lds16(((64 * i) / CPR < 16) ? r0 : r1,
+                buffer_to_lds16<stream_policy<PAGED>()>(((64 * i) / CPR < 16) ? r0 : r1,
                                 (lds_void *)((__attribute__((address_space(3))) char *)dst + 1024 * i), voff[i]);
         };
 
