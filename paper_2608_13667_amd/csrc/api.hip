@@ -128,6 +128,12 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
 {
     p->pre.clear();
     p->seq_prefix_len.assign(p->n_seqs, 0);
+    // token counts stay far enough below 2^31 that ceil(tokens / kSlice) cannot overflow
+    constexpr int32_t kMaxTokens = 1 << 30;
+    if (p->max_suffix_len > kMaxTokens)
+        return fail(FKA_ERR_UNSUPPORTED, "max_suffix_len %d is too long (limit %d)", p->max_suffix_len, kMaxTokens);
+    for (const auto &u : units)
+        if (u[2] > kMaxTokens) return fail(FKA_ERR_UNSUPPORTED, "prefix of %d tokens is too long (limit %d)", u[2], kMaxTokens);
     int64_t c = 0;
     int32_t k = 0, max_nseq = 1;
     for (size_t u = 0; u < units.size(); ++u) {
@@ -148,7 +154,10 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
             k += sz > 0;
         }
     }
-    if (c > (int64_t)1 << 30) return fail(FKA_ERR_UNSUPPORTED, "prefix of %lld slices is too long", (long long)c);
+    // the schedule's total slices (prefix plus every suffix at its longest) stay in int32
+    const int64_t suffix_slices = (int64_t)p->n_seqs * p->Hkv * ((int64_t)p->max_suffix_len + fka::kSlice - 1) / fka::kSlice;
+    if (c + suffix_slices > (int64_t)1 << 30)
+        return fail(FKA_ERR_UNSUPPORTED, "prefix and suffixes of %lld slices are too long", (long long)(c + suffix_slices));
     p->pre_slices = (int32_t)c;
     p->pre_nonempty = k;
     p->n_items = (int32_t)p->pre.size() + p->n_seqs * p->Hkv;

@@ -210,11 +210,19 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     constexpr int KLOADS = 2 * NC;              // K loads per lane per slice
     static_assert(VDMA == KLOADS, "one wait count per slice");
     constexpr int ROWB = HD * 2;                // bytes per K/V row
+    static_assert(2 * 16 * HD * 4 <= kStages * SLICE_CHUNKS * 16, "two tiles fit in a wave's ring");
+    // 16-row tiles the combine stages per pass: all of them for d = 128 (one block per CU, so
+    // the LDS is there), else the two that fit in a wave's ring
+    constexpr int TPP = (HD == 128 && NT > 2) ? NT : 2;
+    constexpr int NPASS = (NT + TPP - 1) / TPP;
 
     // per wave: kStages V slices; chunk c of slice token T sits at T*CPR + (c ^ swz(T))
     __shared__ uint4 vring[NW][kStages][SLICE_CHUNKS];
     __shared__ __attribute__((aligned(16))) float red_m[NT][16][NW];  // per row, the waves side by side
     __shared__ __attribute__((aligned(16))) float red_l[NT][16][NW];
+    __shared__ __attribute__((aligned(16))) float wn[NT][16][NW];     // normalised weights of the combine
+    // staging of 16-row tiles past the first two when one pass holds them all
+    __shared__ __attribute__((aligned(16))) float stg_x[NW][TPP > 2 ? (TPP - 2) * 16 * HD : 4];
     __shared__ int32_t s_len[kMaxSeqs], s_cs[kMaxSeqs], s_ne[kMaxSeqs];
     __shared__ int32_t s_wsum[2][NW];
     __shared__ int32_t s_spl[PAGED ? kMaxSeqs : 1];  // prefix length of each sequence's unit
@@ -672,73 +680,106 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
             }
         }
         wait_vm<0>();  // this wave's ring is idle: it takes the wave's raw accumulators
-        // Staging, per pass two 16-row tiles: wave w's ring holds [tile][row][d] of its own
-        // accumulator (the 16-float blocks of a row XOR-permuted by the row, for the banks).
-        // Threads then own (row, chunk) units of each group: they weigh the group's waves by
-        // exp(max_w - max) and sum.  All global stores of a pass follow its LDS work.
-        static_assert(2 * 16 * HD * 4 <= kStages * SLICE_CHUNKS * 16, "two tiles fit in a wave's ring");
+        // Staging: wave w writes [tile][row][d] of its own accumulator (the 16-float blocks of a
+        // row XOR-permuted by the row, for the banks): tiles 0 and 1 into its ring, further tiles
+        // into stg_x when a pass holds them, else in later passes.  After one barrier, wave g
+        // turns group g's (max, sum) pairs into normalised weights, one lane per row, and stores
+        // the rows' lse; after a second, threads own (row, 8-float) units of each group and sum
+        // the group's staged accumulators with those weights.  All global stores of a pass
+        // follow its LDS work.
         constexpr int CH8 = HD / 8;
-        auto stg = [&](int w) { return reinterpret_cast<float *>(&vring[w][0][0]); };
-        auto stg_off = [&](int tt, int r, int c4) {  // float offset of chunk c4 (4 floats)
-            return (tt * 16 + r) * HD + 16 * ((c4 >> 2) ^ (r & (NE - 1))) + 4 * (c4 & 3);
+        auto stg = [&](int w, int tt) -> float * {
+            if (TPP <= 2 || tt < 2) return reinterpret_cast<float *>(&vring[w][0][0]) + tt * 16 * HD;
+            return &stg_x[w][(tt - 2) * 16 * HD];
+        };
+        auto stg_off = [&](int r, int c4) {  // float offset of chunk c4 (4 floats) of row r in a tile
+            return r * HD + 16 * ((c4 >> 2) ^ (r & (NE - 1))) + 4 * (c4 & 3);
         };
 #pragma unroll
-        for (int pass = 0; pass < (NT + 1) / 2; ++pass) {
+        for (int pass = 0; pass < NPASS; ++pass) {
             if (pass > 0) lds_barrier();  // the previous pass has read the staging
 #pragma unroll
-            for (int tt = 0; tt < 2; ++tt) {
-                const int t = 2 * pass + tt;
+            for (int tt = 0; tt < TPP; ++tt) {
+                const int t = TPP * pass + tt;
                 if (t >= NT) break;
                 if (item >= 0 && t < nt_act) {
 #pragma unroll
                     for (int e = 0; e < NE; ++e)
-                        *reinterpret_cast<f32x4 *>(&stg(wave)[stg_off(tt, l16c, 4 * e + q4c)]) = acc[t][e];
+                        *reinterpret_cast<f32x4 *>(&stg(wave, tt)[stg_off(l16c, 4 * e + q4c)]) = acc[t][e];
                 }
             }
-            lds_barrier();  // also orders the group table (written by thread 0 before streaming)
+            lds_barrier();  // also orders the group table (written by wave 0 before streaming)
             const int n_grp = min(s_ngrp, NW);
+            if (pass == 0) {
+                if (wave < n_grp) {
+                    const int lw = s_grp[wave][0], ge = s_grp[wave][1], it = s_grp[wave][3];
+                    const int row = lane_c;
+                    if (row < s_grp[wave][2] && vb + it < a.n_slots && it >= 0) {
+                        const int t = row >> 4, r = row & 15;
+                        float mw[NW], lw_[NW];
+#pragma unroll
+                        for (int w = 0; w < NW; ++w) {
+                            mw[w] = red_m[t][r][w];
+                            lw_[w] = red_l[t][r][w];
+                        }
+                        float M = -INFINITY;
+#pragma unroll
+                        for (int w = 0; w < NW; ++w) M = (w >= lw && w < ge) ? fmaxf(M, mw[w]) : M;
+                        const float Mu = (M == -INFINITY) ? 0.f : M;
+                        // a wave of the group that saw no keys has max -inf, weight 0 and a
+                        // zero accumulator; waves outside the group are never read
+                        float wt[NW], L = 0.f;
+#pragma unroll
+                        for (int w = 0; w < NW; ++w) {
+                            const bool in = w >= lw && w < ge;
+                            wt[w] = (in && mw[w] != -INFINITY) ? fast_exp2(mw[w] - Mu) : 0.f;
+                            L = in ? L + wt[w] * lw_[w] : L;
+                        }
+                        // L == 0 only when the group saw no keys: weights 0 give o = 0 from its
+                        // zero accumulators; a NaN input keeps propagating
+                        const float inv = (L == 0.f) ? 0.f : __builtin_amdgcn_rcpf(L);
+#pragma unroll
+                        for (int w = 0; w < NW; ++w)
+                            if (w >= lw && w < ge) wn[t][r][w] = wt[w] * inv;
+                        a.part_lse[(size_t)(vb + it) * a.slot_rows + row] =
+                            (L == 0.f) ? -INFINITY : (Mu + log2f(L)) * kLn2;
+                    }
+                }
+                lds_barrier();  // the weights
+            }
             for (int g = 0; g < n_grp; ++g) {
                 const int lw = s_grp[g][0], ge = s_grp[g][1], it = s_grp[g][3];
                 if (vb + it >= a.n_slots || it < 0) continue;  // never store outside the workspace
-                const int r0 = 32 * pass, r1 = min(s_grp[g][2], r0 + 32);
-                // a unit is 8 floats of one row: the group's weights are computed once per unit
+                const int r0 = 16 * TPP * pass, r1 = min(s_grp[g][2], r0 + 16 * TPP);
+                const bool whole = lw == 0 && ge == NW;  // the usual case: one group, all waves
                 for (int u = tid_c; u < (r1 - r0) * CH8; u += NTH) {
                     const int row = r0 + u / CH8, c8 = u % CH8;
-                    const int t = row >> 4, tt = t - 2 * pass, r = row & 15;
-                    float mw[NW], lw_[NW];
-                    f32x4 v0[NW], v1[NW];
-#pragma unroll
-                    for (int w = 0; w < NW; ++w) {
-                        mw[w] = red_m[t][r][w];
-                        lw_[w] = red_l[t][r][w];
-                        v0[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, 2 * c8)]);
-                        v1[w] = *reinterpret_cast<const f32x4 *>(&stg(w)[stg_off(tt, r, 2 * c8 + 1)]);
-                    }
-                    float M = -INFINITY;
-#pragma unroll
-                    for (int w = 0; w < NW; ++w) M = (w >= lw && w < ge) ? fmaxf(M, mw[w]) : M;
-                    const float Mu = (M == -INFINITY) ? 0.f : M;
-                    float L = 0.f;
+                    const int t = row >> 4, tt = t - TPP * pass, r = row & 15;
                     f32x4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = {0.f, 0.f, 0.f, 0.f};
+                    if (whole) {
+                        float wv[NW];
+                        f32x4 v0[NW], v1[NW];
 #pragma unroll
-                    for (int w = 0; w < NW; ++w) {
-                        // waves outside the group are selected out, not weighted by 0: their
-                        // staging may hold another item's NaN.  A wave of the group that saw no
-                        // keys has max -inf and weight 0 (its accumulator is 0).
-                        const bool in = w >= lw && w < ge;
-                        const float wt = (in && mw[w] != -INFINITY) ? fast_exp2(mw[w] - Mu) : 0.f;
-                        L = in ? L + wt * lw_[w] : L;
-                        o0 = in ? o0 + wt * v0[w] : o0;
-                        o1 = in ? o1 + wt * v1[w] : o1;
+                        for (int w = 0; w < NW; ++w) {
+                            wv[w] = wn[t][r][w];
+                            v0[w] = *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8)]);
+                            v1[w] = *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8 + 1)]);
+                        }
+#pragma unroll
+                        for (int w = 0; w < NW; ++w) {
+                            o0 += wv[w] * v0[w];
+                            o1 += wv[w] * v1[w];
+                        }
+                    } else {
+                        for (int w = lw; w < ge; ++w) {
+                            const float wv = wn[t][r][w];
+                            o0 += wv * *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8)]);
+                            o1 += wv * *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8 + 1)]);
+                        }
                     }
-                    // L == 0 only when the group saw no keys; a NaN input keeps propagating
-                    const float inv = __builtin_amdgcn_rcpf(L);
-                    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-                    const size_t so = (size_t)(vb + it) * a.slot_rows + row;
-                    float *dst = a.part_o + so * HD + 8 * c8;
-                    *reinterpret_cast<f32x4 *>(dst) = (L == 0.f) ? z : o0 * inv;
-                    *reinterpret_cast<f32x4 *>(dst + 4) = (L == 0.f) ? z : o1 * inv;
-                    if (c8 == 0) a.part_lse[so] = (L == 0.f) ? -INFINITY : (Mu + log2f(L)) * kLn2;
+                    float *dst = a.part_o + ((size_t)(vb + it) * a.slot_rows + row) * HD + 8 * c8;
+                    *reinterpret_cast<f32x4 *>(dst) = o0;
+                    *reinterpret_cast<f32x4 *>(dst + 4) = o1;
                 }
             }
         }

@@ -66,6 +66,10 @@ def _create(fa, heads, desc):
     ((8, 8, 64), (513, 512, 64, 64, 0, 0), -2, "sequences"),
     ((128, 2, 64), (2, 512, 64, 64, 1, 0), -2, "rows"),
     ((64, 8, 128), (9, 512, 64, 64, 1, 0), -2, "rows"),
+    # suffixes whose slices would overflow the schedule's 32-bit arithmetic
+    ((8, 2, 64), (512, 512, 2**31 - 1, 2**31 - 1, 0, 0), -2, "too long"),
+    ((8, 2, 64), (512, 512, 2**25, 2**25, 0, 0), -2, "too long"),
+    ((8, 2, 64), (5, 2**31 - 1, 64, 64, 1, 0), -2, "too long"),
 ])
 def test_plan_create_rejects(fa, heads, desc, status, needle):
     h = _heads(fa, *heads) if heads else None
