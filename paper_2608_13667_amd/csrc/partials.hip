@@ -220,7 +220,6 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
     __shared__ uint4 vring[NW][kStages][SLICE_CHUNKS];
     __shared__ __attribute__((aligned(16))) float red_m[NT][16][NW];  // per row, the waves side by side
     __shared__ __attribute__((aligned(16))) float red_l[NT][16][NW];
-    __shared__ __attribute__((aligned(16))) float wn[NT][16][NW];     // normalised weights of the combine
     // staging of 16-row tiles past the first two when one pass holds them all
     __shared__ __attribute__((aligned(16))) float stg_x[NW][TPP > 2 ? (TPP - 2) * 16 * HD : 4];
     __shared__ int32_t s_len[kMaxSeqs], s_cs[kMaxSeqs], s_ne[kMaxSeqs];
@@ -682,14 +681,14 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
         wait_vm<0>();  // this wave's ring is idle: it takes the wave's raw accumulators
         // Staging: wave w writes [tile][row][d] of its own accumulator (the 16-float blocks of a
         // row XOR-permuted by the row, for the banks): tiles 0 and 1 into its ring, further tiles
-        // into stg_x when a pass holds them, else in later passes.  After one barrier, wave g
-        // turns group g's (max, sum) pairs into normalised weights, one lane per row, and stores
-        // the rows' lse; after a second, threads own (row, 8-float) units of each group and sum
-        // the group's staged accumulators with those weights.  All global stores of a pass
-        // follow its LDS work.
+        // into stg_x when a pass holds them, else in later passes.  After one barrier, threads own
+        // (row, 8-float) units of each group: they weigh the group's waves by exp(max_w - max),
+        // sum, and normalise; the unit holding the row's first floats also stores its lse.  (A
+        // separate step computing the weights once per row cost more than it saved: one wave ran
+        // it alone behind a second barrier.)  All global stores of a pass follow its LDS work.
         constexpr int CH8 = HD / 8;
-        auto stg = [&](int w, int tt) -> float * {
-            if (TPP <= 2 || tt < 2) return reinterpret_cast<float *>(&vring[w][0][0]) + tt * 16 * HD;
+        auto stg = [&](int w, int tt) -> const float * {
+            if (TPP <= 2 || tt < 2) return reinterpret_cast<const float *>(&vring[w][0][0]) + tt * 16 * HD;
             return &stg_x[w][(tt - 2) * 16 * HD];
         };
         auto stg_off = [&](int r, int c4) {  // float offset of chunk c4 (4 floats) of row r in a tile
@@ -703,50 +702,14 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                 const int t = TPP * pass + tt;
                 if (t >= NT) break;
                 if (item >= 0 && t < nt_act) {
+                    float *dst = const_cast<float *>(stg(wave, tt));
 #pragma unroll
                     for (int e = 0; e < NE; ++e)
-                        *reinterpret_cast<f32x4 *>(&stg(wave, tt)[stg_off(l16c, 4 * e + q4c)]) = acc[t][e];
+                        *reinterpret_cast<f32x4 *>(&dst[stg_off(l16c, 4 * e + q4c)]) = acc[t][e];
                 }
             }
             lds_barrier();  // also orders the group table (written by wave 0 before streaming)
             const int n_grp = min(s_ngrp, NW);
-            if (pass == 0) {
-                if (wave < n_grp) {
-                    const int lw = s_grp[wave][0], ge = s_grp[wave][1], it = s_grp[wave][3];
-                    const int row = lane_c;
-                    if (row < s_grp[wave][2] && vb + it < a.n_slots && it >= 0) {
-                        const int t = row >> 4, r = row & 15;
-                        float mw[NW], lw_[NW];
-#pragma unroll
-                        for (int w = 0; w < NW; ++w) {
-                            mw[w] = red_m[t][r][w];
-                            lw_[w] = red_l[t][r][w];
-                        }
-                        float M = -INFINITY;
-#pragma unroll
-                        for (int w = 0; w < NW; ++w) M = (w >= lw && w < ge) ? fmaxf(M, mw[w]) : M;
-                        const float Mu = (M == -INFINITY) ? 0.f : M;
-                        // a wave of the group that saw no keys has max -inf, weight 0 and a
-                        // zero accumulator; waves outside the group are never read
-                        float wt[NW], L = 0.f;
-#pragma unroll
-                        for (int w = 0; w < NW; ++w) {
-                            const bool in = w >= lw && w < ge;
-                            wt[w] = (in && mw[w] != -INFINITY) ? fast_exp2(mw[w] - Mu) : 0.f;
-                            L = in ? L + wt[w] * lw_[w] : L;
-                        }
-                        // L == 0 only when the group saw no keys: weights 0 give o = 0 from its
-                        // zero accumulators; a NaN input keeps propagating
-                        const float inv = (L == 0.f) ? 0.f : __builtin_amdgcn_rcpf(L);
-#pragma unroll
-                        for (int w = 0; w < NW; ++w)
-                            if (w >= lw && w < ge) wn[t][r][w] = wt[w] * inv;
-                        a.part_lse[(size_t)(vb + it) * a.slot_rows + row] =
-                            (L == 0.f) ? -INFINITY : (Mu + log2f(L)) * kLn2;
-                    }
-                }
-                lds_barrier();  // the weights
-            }
             for (int g = 0; g < n_grp; ++g) {
                 const int lw = s_grp[g][0], ge = s_grp[g][1], it = s_grp[g][3];
                 if (vb + it >= a.n_slots || it < 0) continue;  // never store outside the workspace
@@ -755,31 +718,49 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_ker
                 for (int u = tid_c; u < (r1 - r0) * CH8; u += NTH) {
                     const int row = r0 + u / CH8, c8 = u % CH8;
                     const int t = row >> 4, tt = t - TPP * pass, r = row & 15;
+                    // a wave of the group that saw no keys has max -inf, weight 0 and a zero
+                    // accumulator; waves outside the group are never read (their staging may
+                    // hold another item's NaN)
+                    float M = -INFINITY, L = 0.f;
                     f32x4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = {0.f, 0.f, 0.f, 0.f};
                     if (whole) {
-                        float wv[NW];
+                        float mw[NW], lw_[NW];
                         f32x4 v0[NW], v1[NW];
 #pragma unroll
                         for (int w = 0; w < NW; ++w) {
-                            wv[w] = wn[t][r][w];
+                            mw[w] = red_m[t][r][w];
+                            lw_[w] = red_l[t][r][w];
                             v0[w] = *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8)]);
                             v1[w] = *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8 + 1)]);
                         }
 #pragma unroll
+                        for (int w = 0; w < NW; ++w) M = fmaxf(M, mw[w]);
+                        const float Mu = (M == -INFINITY) ? 0.f : M;
+#pragma unroll
                         for (int w = 0; w < NW; ++w) {
-                            o0 += wv[w] * v0[w];
-                            o1 += wv[w] * v1[w];
+                            const float wt = fast_exp2(mw[w] - Mu);  // 0 for max -inf
+                            L = __builtin_fmaf(wt, lw_[w], L);
+                            o0 += wt * v0[w];
+                            o1 += wt * v1[w];
                         }
                     } else {
+                        for (int w = lw; w < ge; ++w) M = fmaxf(M, red_m[t][r][w]);
+                        const float Mu = (M == -INFINITY) ? 0.f : M;
                         for (int w = lw; w < ge; ++w) {
-                            const float wv = wn[t][r][w];
-                            o0 += wv * *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8)]);
-                            o1 += wv * *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8 + 1)]);
+                            const float wt = fast_exp2(red_m[t][r][w] - Mu);
+                            L = __builtin_fmaf(wt, red_l[t][r][w], L);
+                            o0 += wt * *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8)]);
+                            o1 += wt * *reinterpret_cast<const f32x4 *>(&stg(w, tt)[stg_off(r, 2 * c8 + 1)]);
                         }
                     }
-                    float *dst = a.part_o + ((size_t)(vb + it) * a.slot_rows + row) * HD + 8 * c8;
-                    *reinterpret_cast<f32x4 *>(dst) = o0;
-                    *reinterpret_cast<f32x4 *>(dst + 4) = o1;
+                    // L == 0 only when the group saw no keys: its accumulators are zero and so is
+                    // o; a NaN input keeps propagating
+                    const float inv = (L == 0.f) ? 0.f : __builtin_amdgcn_rcpf(L);
+                    const size_t so = (size_t)(vb + it) * a.slot_rows + row;
+                    float *dst = a.part_o + so * HD + 8 * c8;
+                    *reinterpret_cast<f32x4 *>(dst) = o0 * inv;
+                    *reinterpret_cast<f32x4 *>(dst + 4) = o1 * inv;
+                    if (c8 == 0) a.part_lse[so] = (L == 0.f) ? -INFINITY : (((M == -INFINITY) ? 0.f : M) + log2f(L)) * kLn2;
                 }
             }
         }
