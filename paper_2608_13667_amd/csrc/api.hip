@@ -170,7 +170,7 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
         return hip_fail(e, "hipDeviceGetAttribute");
     const int per_cu = fka::partials_blocks_per_cu(p->d, p->row_tiles, p->paged);
-    p->waves = fka::partials_waves_per_block(p->d, p->row_tiles);
+    p->waves = fka::partials_waves_per_block(p->d, p->row_tiles, p->paged);
     if (per_cu <= 0 || p->waves <= 0) return fail(FKA_ERR_HIP, "occupancy query of the partial kernel failed");
     p->n_blocks = cus * per_cu;
     // at least two workers per item, so that A = workers - non-empty items stays >= half

@@ -255,7 +255,7 @@ hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int ro
 // Resident blocks per compute unit of the partial kernel for this shape (0 on error).
 int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged);
 // Waves per block of the partial kernel for this shape.
-int partials_waves_per_block(int head_dim, int row_tiles);
+int partials_waves_per_block(int head_dim, int row_tiles, bool paged);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);

@@ -186,21 +186,22 @@ __device__ inline bf16x8 join_tr16(vtr_t lo, vtr_t hi)
     return __builtin_bit_cast(bf16x8, v);
 }
 
-// Waves per SIMD the register budget is built for: two (<= 256 VGPRs each) unless the
-// accumulators of three or four 16-row tiles of d = 128 need the whole register file.
-// Waves per SIMD the register budget is built for: two (<= 256 VGPRs each) unless the
-// accumulators of three or four 16-row tiles of d = 128 need the whole register file.
-template <int HD, int NT>
+// Waves per SIMD (and so per block: four times as many, one block per compute unit).  d = 128:
+// one wave per SIMD with the whole register file (three or four 16-row tiles need it; with one
+// or two, contiguous K/V measured 1% faster on the 32k-prefix workload and 5% on the 8k one
+// than two waves of <= 256 VGPRs, whose older wave finishes well before the younger), except
+// paged K/V with one or two tiles, where two waves per SIMD measured 11% faster.  d = 64: two.
+template <int HD, int NT, bool PAGED>
 constexpr int waves_per_simd()
 {
-    return (HD <= 64 || NT <= 2) ? 2 : 1;
+    return (HD <= 64 || (PAGED && NT <= 2)) ? 2 : 1;
 }
 
 template <int HD, int NT, bool PAGED>
-__global__ __launch_bounds__((256 * waves_per_simd<HD, NT>()))
-__attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT>()))) void partials_kernel(AttnArgs a)
+__global__ __launch_bounds__((256 * waves_per_simd<HD, NT, PAGED>()))
+__attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void partials_kernel(AttnArgs a)
 {
-    constexpr int NW = 4 * waves_per_simd<HD, NT>();  // waves per block
+    constexpr int NW = 4 * waves_per_simd<HD, NT, PAGED>();  // waves per block
     constexpr int NTH = 64 * NW;
     constexpr int CPR = HD / 8;                 // 16-byte chunks per K/V row
     constexpr int NC = HD / 32;                 // MFMA k-steps of q.k
@@ -774,10 +775,10 @@ int blocks_per_cu_hd(int row_tiles)
     const void *f = nullptr;
     int threads = 0;
     switch (row_tiles) {
-    case 1: f = reinterpret_cast<const void *>(&partials_kernel<HD, 1, PAGED>); threads = 256 * waves_per_simd<HD, 1>(); break;
-    case 2: f = reinterpret_cast<const void *>(&partials_kernel<HD, 2, PAGED>); threads = 256 * waves_per_simd<HD, 2>(); break;
-    case 3: f = reinterpret_cast<const void *>(&partials_kernel<HD, 3, PAGED>); threads = 256 * waves_per_simd<HD, 3>(); break;
-    case 4: f = reinterpret_cast<const void *>(&partials_kernel<HD, 4, PAGED>); threads = 256 * waves_per_simd<HD, 4>(); break;
+    case 1: f = reinterpret_cast<const void *>(&partials_kernel<HD, 1, PAGED>); threads = 256 * waves_per_simd<HD, 1, PAGED>(); break;
+    case 2: f = reinterpret_cast<const void *>(&partials_kernel<HD, 2, PAGED>); threads = 256 * waves_per_simd<HD, 2, PAGED>(); break;
+    case 3: f = reinterpret_cast<const void *>(&partials_kernel<HD, 3, PAGED>); threads = 256 * waves_per_simd<HD, 3, PAGED>(); break;
+    case 4: f = reinterpret_cast<const void *>(&partials_kernel<HD, 4, PAGED>); threads = 256 * waves_per_simd<HD, 4, PAGED>(); break;
     default: return 0;
     }
     int n = 0;
@@ -790,10 +791,10 @@ hipError_t launch_hd(const AttnArgs &a, int n_blocks, int row_tiles, hipStream_t
 {
     const dim3 grid(n_blocks);
     switch (row_tiles) {
-    case 1: partials_kernel<HD, 1, PAGED><<<grid, 256 * waves_per_simd<HD, 1>(), 0, s>>>(a); break;
-    case 2: partials_kernel<HD, 2, PAGED><<<grid, 256 * waves_per_simd<HD, 2>(), 0, s>>>(a); break;
-    case 3: partials_kernel<HD, 3, PAGED><<<grid, 256 * waves_per_simd<HD, 3>(), 0, s>>>(a); break;
-    case 4: partials_kernel<HD, 4, PAGED><<<grid, 256 * waves_per_simd<HD, 4>(), 0, s>>>(a); break;
+    case 1: partials_kernel<HD, 1, PAGED><<<grid, 256 * waves_per_simd<HD, 1, PAGED>(), 0, s>>>(a); break;
+    case 2: partials_kernel<HD, 2, PAGED><<<grid, 256 * waves_per_simd<HD, 2, PAGED>(), 0, s>>>(a); break;
+    case 3: partials_kernel<HD, 3, PAGED><<<grid, 256 * waves_per_simd<HD, 3, PAGED>(), 0, s>>>(a); break;
+    case 4: partials_kernel<HD, 4, PAGED><<<grid, 256 * waves_per_simd<HD, 4, PAGED>(), 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -808,16 +809,22 @@ int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged)
     return 0;
 }
 
-int partials_waves_per_block(int head_dim, int row_tiles)
+template <bool PAGED>
+int waves_per_block_hd128(int row_tiles)
 {
-    if (head_dim == 64) return 4 * waves_per_simd<64, 1>();
     switch (row_tiles) {
-    case 1: return 4 * waves_per_simd<128, 1>();
-    case 2: return 4 * waves_per_simd<128, 2>();
-    case 3: return 4 * waves_per_simd<128, 3>();
-    case 4: return 4 * waves_per_simd<128, 4>();
+    case 1: return 4 * waves_per_simd<128, 1, PAGED>();
+    case 2: return 4 * waves_per_simd<128, 2, PAGED>();
+    case 3: return 4 * waves_per_simd<128, 3, PAGED>();
+    case 4: return 4 * waves_per_simd<128, 4, PAGED>();
     default: return 0;
     }
+}
+
+int partials_waves_per_block(int head_dim, int row_tiles, bool paged)
+{
+    if (head_dim == 64) return 4 * waves_per_simd<64, 1, false>();
+    return paged ? waves_per_block_hd128<true>(row_tiles) : waves_per_block_hd128<false>(row_tiles);
 }
 
 hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s)
