@@ -68,7 +68,9 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: 256 appends per replica)")
-    ap.add_argument("--warmup", type=int, default=20)
+    # 200 untimed steps: on the 128k-prefix workload the first ~20 ms of back-to-back launches run
+    # a transient (steps 5-10% slower, then settling); shorter workloads are unaffected
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="long", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--replicas", type=int, default=0, help="layer replicas (0: enough for >= 1 GiB)")
     ap.add_argument("--rounds", type=int, default=0, help="schedule rounds of the resident waves (0: automatic)")
