@@ -63,14 +63,19 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const char *base, int bytes)
     return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), 0, n, 0x00020000);
 }
 
-// Cache policy of the K/V stream.  Contiguous K/V: non-temporal (each byte is read once;
-// measured 6% faster on the 32k-prefix workload and 13% on the 128k one).  Paged K/V (4 KiB
-// blocks in page order): the default policy (non-temporal measured 9% slower there).
+// Cache policy of the K/V stream: non-temporal (each byte is read once; measured 6% faster on
+// the 32k-prefix workload and 13% on the 128k one), except paged K.  A K load instruction reads
+// 64 bytes of each of 16 rows (the MFMA operand layout), so with 4 KiB (page, head) blocks in
+// page-table order the halves of a 128-byte line come from different instructions; without
+// the line kept in the cache that measured 12% slower on the paged workload, the default policy
+// is kept there.  V arrives by LDS DMA, 1 KiB contiguous per instruction: non-temporal in both
+// layouts (5% faster on the paged workload than the default).
 template <bool PAGED>
-constexpr int stream_policy()
+constexpr int k_policy()
 {
     return PAGED ? 0 : 2;
 }
+constexpr int kVPolicy = 2;
 
 // 16 bytes per lane from a buffer into LDS at dst + 16 * lane (LDS DMA).  Kept outside
 // the kernel template: used directly there, the builtin stops the host compiler from
@@ -505,7 +510,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
                 const __amdgpu_buffer_rsrc_t r = group_rsrc(kbase, t0 + 16 * u);
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
-                    kr[u][c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, koff + 64 * c, 0, stream_policy<PAGED>()));
+                    kr[u][c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, koff + 64 * c, 0, k_policy<PAGED>()));
             }
         };
 
@@ -526,7 +531,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
             const __amdgpu_buffer_rsrc_t r0 = group_rsrc(vbase, t0), r1 = group_rsrc(vbase, t0 + 16);
 #pragma unroll
             for (int i = 0; i < VDMA; ++i)
-                buffer_to_lds16<stream_policy<PAGED>()>(((64 * i) / CPR < 16) ? r0 : r1,
+                buffer_to_lds16<kVPolicy>(((64 * i) / CPR < 16) ? r0 : r1,
                                 (lds_void *)((__attribute__((address_space(3))) char *)dst + 1024 * i), voff[i]);
         };
 
