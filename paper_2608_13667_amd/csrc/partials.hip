@@ -234,7 +234,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
     // each wave's item: item, seq0, nseq, kv head, keys, and its group (the block's waves on the
     // same item): first wave, first slice, end slice, end wave
     __shared__ int32_t s_wfc[2][NW][9];  // per candidate schedule (the built one goes to [0])
-    __shared__ int32_t s_grp[NW][4];  // the block's groups: first wave, end wave, rows, item
+    __shared__ __attribute__((aligned(16))) int32_t s_grp[NW][4];  // the block's groups: first wave, end wave, rows, item
     __shared__ int32_t s_ngrp;
     __shared__ int32_t s_stale[NW];   // bit c: a wave saw a suffix length that differs from key c
 
@@ -720,9 +720,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
             lds_barrier();  // also orders the group table (written by wave 0 before streaming)
             const int n_grp = min(s_ngrp, NW);
             for (int g = 0; g < n_grp; ++g) {
-                const int lw = s_grp[g][0], ge = s_grp[g][1], it = s_grp[g][3];
+                const int4 gi = *reinterpret_cast<const int4 *>(&s_grp[g][0]);
+                asm volatile("" ::"v"(gi.x), "v"(gi.y), "v"(gi.z), "v"(gi.w));  // one LDS read, not four
+                const int lw = gi.x, ge = gi.y, it = gi.w;
                 if (vb + it >= a.n_slots || it < 0) continue;  // never store outside the workspace
-                const int r0 = 16 * TPP * pass, r1 = min(s_grp[g][2], r0 + 16 * TPP);
+                const int r0 = 16 * TPP * pass, r1 = min(gi.z, r0 + 16 * TPP);
                 const bool whole = lw == 0 && ge == NW;  // the usual case: one group, all waves
                 for (int u = tid_c; u < (r1 - r0) * CHU; u += NTH) {
                     const int row = r0 + u / CHU, cu = u % CHU;
