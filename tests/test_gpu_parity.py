@@ -113,6 +113,37 @@ def test_edge_cases(fa, case):
     _check_contig(fa, W.make(spec))
 
 
+def _random_shapes(n, seed):
+    """Seeded random plan shapes within the plan limits: GQA group, branches, head_dim, prefix and
+    suffix lengths (ragged, some empty), rounds and sharing."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        d = int(rng.choice([64, 128]))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.integers(1, 17))
+        nb = int(rng.integers(1, 9))
+        while nb * g > 64:  # at most 64 query rows per KV head
+            nb -= 1
+        lo = int(rng.integers(0, 400))
+        out.append(dict(head_dim=d, n_kv_heads=hkv, n_q_heads=hkv * g, n_branches=nb,
+                        prefix_len=int(rng.integers(0, 4000)), suffix_range=(lo, lo + int(rng.integers(0, 400))),
+                        seed=int(rng.integers(1, 1 << 30)), share=bool(rng.integers(0, 4) > 0),
+                        rounds=int(rng.choice([0, 0, 0, 2, 7]))))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_shapes(16, 2026), ids=lambda c: "d{head_dim}-kv{n_kv_heads}-q{n_q_heads}-b{n_branches}-"
+                         "p{prefix_len}-s{suffix_range[0]}_{suffix_range[1]}-r{rounds}-{share}".format(**c))
+def test_random_shapes(fa, case):
+    """Parity on seeded random shapes (not tied to a named workload)."""
+    c = dict(case)
+    share, rounds = c.pop("share"), c.pop("rounds")
+    spec = W.CONFIGS["mid"].replace(**c)
+    print(f"[random] {case}", flush=True)
+    _check_contig(fa, W.make(spec), share_prefix=share, rounds=rounds)
+
+
 @pytest.mark.parametrize("rounds", [1, 3, 64])
 def test_explicit_rounds(fa, rounds):
     """More rounds: the keys spread over more, smaller partials (64 rounds: ~1 slice per wave)."""
