@@ -324,6 +324,40 @@ def _small_paged(headroom=0, seed=90):
                                              page_headroom=headroom, seed=seed))
 
 
+def _random_paged(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        d = int(rng.choice([64, 128]))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.integers(1, 9))
+        nb = int(rng.integers(1, 7))
+        while nb * g > 64:
+            nb -= 1
+        p0 = int(rng.integers(0, 2000))
+        s0 = int(rng.integers(0, 300))
+        out.append(dict(head_dim=d, n_kv_heads=hkv, n_q_heads=hkv * g, n_branches=nb,
+                        n_tasks=int(rng.integers(1, 7)), prefix_range=(p0, p0 + int(rng.integers(0, 3000))),
+                        suffix_range=(s0, s0 + int(rng.integers(0, 400))), page_headroom=int(rng.integers(0, 3)),
+                        seed=int(rng.integers(1, 1 << 30)), share=bool(rng.integers(0, 4) > 0)))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_paged(8, 4242), ids=lambda c: "d{head_dim}-kv{n_kv_heads}-q{n_q_heads}-b{n_branches}-"
+                         "t{n_tasks}-p{prefix_range[0]}_{prefix_range[1]}-{share}".format(**c))
+def test_random_paged_shapes(fa, case):
+    """Paged parity on seeded random shapes: tasks, branches, GQA group, head_dim, prefix and
+    suffix lengths (pages scattered by a random permutation of the pool)."""
+    c = dict(case)
+    share = c.pop("share")
+    w = W.make(W.CONFIGS["paged"].replace(**c))
+    print(f"[random paged] {case}", flush=True)
+    ref, ref_lse = oracle.decode_workload(w)
+    out, lse = run_paged(paged_plan(fa, w, share_prefix=share), to_dev_paged(w))
+    gates.assert_gates(out, ref, what="random paged")
+    gates.assert_lse(lse, ref_lse, what="random paged")
+
+
 def test_paged_small_parity_and_naive(fa):
     w = _small_paged()
     ref, ref_lse = oracle.decode_workload(w)
