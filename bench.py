@@ -55,6 +55,8 @@ DESCRIPTIONS = {
     "mid": "mid context: 8192-token shared prefix, 5 sequences, 32 q / 8 kv heads, head_dim 128, "
            "suffixes 256..1024 tokens",
     "tiny": "tiny: 512-token shared prefix, 5 sequences, 8 q / 2 kv heads, head_dim 64, suffixes 0..64 tokens",
+    "onset": "fork at turn onset: 32768-token shared prefix, 5 sequences, 40 q / 8 kv heads, head_dim 128, "
+             "main suffix 4096..8192 tokens (the Thought), branch suffixes 0..512",
     "paged": "concurrent agents, paged: 16 tasks x 5 sequences, 32 q / 8 kv heads, head_dim 128, prefixes "
              "4096..65536, suffixes 0..2048, 16-token pages from a permuted pool",
 }

@@ -97,6 +97,7 @@ class Spec:
     prefix_len: int = 0                       # contiguous: shared prefix length
     prefix_range: tuple = (0, 0)              # paged: per-task prefix length range (inclusive)
     suffix_range: tuple = (0, 0)              # per-branch suffix length range (inclusive)
+    main_suffix_range: Optional[tuple] = None  # contiguous: sequence 0's own range, drawn after the others
     value_scale: float = 1.0                  # N(0,1) draws are multiplied by this
     k_channel_scale: bool = False             # per-(kv head, channel) LogNormal(0, 0.5) factor on K
     steps: int = 0                            # decode steps with one appended token per branch
@@ -128,6 +129,10 @@ CONFIGS = {
                  k_channel_scale=True, steps=256),
     "very-long": Spec("very-long", 64, 8, 128, seed=1004, prefix_len=131072, suffix_range=(1024, 4096),
                       k_channel_scale=True),
+    # Fork at turn onset (Sec. 4.4, fork-conditioning comparison): the branches fork before the
+    # Thought, so the main sequence's suffix is the whole Thought while the branches' stay short.
+    "onset": Spec("onset", 40, 8, 128, seed=1006, prefix_len=32768, suffix_range=(0, 512),
+                  main_suffix_range=(4096, 8192), k_channel_scale=True),
     "paged": Spec("paged", 32, 8, 128, seed=1005, paged=True, n_tasks=16, prefix_range=(4096, 65536),
                   suffix_range=(0, 2048), k_channel_scale=True),
 }
@@ -237,6 +242,10 @@ def make_contig(spec: Spec) -> ContigWorkload:
     lens_rng = np.random.Generator(np.random.PCG64(streams[_S_LEN]))
     lo, hi = spec.suffix_range
     suffix_len = lens_rng.integers(lo, hi, size=N, endpoint=True).astype(np.int32)
+    if spec.main_suffix_range is not None:
+        mlo, mhi = spec.main_suffix_range
+        suffix_len[0] = lens_rng.integers(mlo, mhi, endpoint=True)
+        hi = max(hi, mhi)
     cap = max(1, hi + spec.steps)
     kscale = _draw_kscale(streams[_S_KSCALE], spec)
 

@@ -35,7 +35,7 @@ def _check_contig(fa, w, **plan_kw):
     return m
 
 
-@pytest.mark.parametrize("name", ["tiny", "tiny-unscaled", "mid", "long", "very-long"])
+@pytest.mark.parametrize("name", ["tiny", "tiny-unscaled", "mid", "long", "very-long", "onset"])
 def test_config_parity(fa, name):
     spec = W.CONFIGS[name].replace(steps=0)
     print(f"[parity] {name}", flush=True)

@@ -343,3 +343,21 @@ def test_mutation_missing_scale_fails(ref_case):
     w, out, _ = ref_case
     bad, _ = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, w.suffix_len, 1.0)
     assert not gates.passes(bad, out)
+
+
+@pytest.mark.parametrize("name", ["tiny", "mid", "long", "very-long", "onset"])
+def test_workload_lengths(name):
+    """Suffix lengths are integers drawn inclusively from the stated ranges; the fork-onset
+    workload's main sequence draws from its own (long) range after the branches, so the branch
+    draws match those of the same spec without it."""
+    spec = W.CONFIGS[name]
+    w = W.make(spec.replace(steps=0))
+    lo, hi = spec.suffix_range
+    first = 0 if spec.main_suffix_range is None else 1
+    assert all(lo <= int(L) <= hi for L in w.suffix_len[first:])
+    if spec.main_suffix_range is not None:
+        mlo, mhi = spec.main_suffix_range
+        assert mlo <= int(w.suffix_len[0]) <= mhi
+        base = W.make(spec.replace(main_suffix_range=None, steps=0, prefix_len=16))
+        assert np.array_equal(base.suffix_len[1:], w.suffix_len[1:])
+    assert w.suffix_k.shape[2] >= int(w.suffix_len.max())
