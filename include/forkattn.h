@@ -206,6 +206,80 @@ fka_status fka_fork_step_paged(const fka_plan *plan, const void *q, const void *
 fka_status fka_gather_paged(const fka_plan *plan, int32_t seq, const void *k_pool, const void *v_pool,
                             const int32_t *page_table, int32_t out_len, void *k_out, void *v_out, void *stream);
 
+/* ------------------------------------------------ page pool: the K/V lifecycle of a fork */
+
+/*
+ * Host-side bookkeeping of the page ids [0, n_pages) of a paged K/V pool, one reference count per
+ * page, following the lifecycle of a fork (Sec. 3.2 Overview; Sec. 3.3 Forking via Trajectory
+ * Continuation; Sec. 3.5 Thought Harvesting):
+ *   fork       every sequence of the group reads the snapshot's pages: one reference per page
+ *              table row (fka_pool_fork);
+ *   decode     a sequence takes a fresh page when its suffix reaches a page boundary; suffix
+ *              position j of a sequence whose group prefix is Lp tokens is at page-table index
+ *              ceil(Lp / 16) + j / 16, slot j % 16 (fka_pool_reserve, ahead of the appends);
+ *   merge      the branches are terminated and their pages released (fka_pool_drop); what is
+ *              harvested returns as text, so no branch K/V outlives the turn;
+ *   next turn  the main sequence's context becomes the next snapshot, laid out densely
+ *              (position p at index p / 16, slot p % 16): fka_pool_promote assigns the pages and
+ *              fka_scatter_pages moves the K/V on the device.
+ * Page tables here are host int32 arrays [rows][max_pages], -1 = no page; the caller copies the
+ * rows it changed to the device table the kernels read.  A pool is not thread-safe.  Errors:
+ * FKA_ERR_INVALID_ARG (a bad argument, or a page id that is not live), FKA_ERR_NOMEM (too few
+ * free pages).  A call that fails changes nothing.
+ */
+typedef struct fka_pool fka_pool;
+
+fka_status fka_pool_create(int32_t n_pages, fka_pool **out);
+void fka_pool_destroy(fka_pool *pool);  /* NULL is ignored */
+
+/* Free pages; -1 for a NULL pool. */
+int32_t fka_pool_free_pages(const fka_pool *pool);
+
+/* Reference count of `page` (0 = free); -1 for a NULL pool or an id outside [0, n_pages). */
+int32_t fka_pool_refcount(const fka_pool *pool, int32_t page);
+
+/* Take n free pages (count 1 each), lowest ids first, into ids[n]. */
+fka_status fka_pool_alloc(fka_pool *pool, int32_t n, int32_t *ids);
+
+/* One more / one less reference to each of ids[n]; every id must be live (an id may repeat as
+ * often as it has references to drop).  A page whose count reaches 0 is free. */
+fka_status fka_pool_retain(fka_pool *pool, int32_t n, const int32_t *ids);
+fka_status fka_pool_release(fka_pool *pool, int32_t n, const int32_t *ids);
+
+/* Fork: rows [first, first + n) of page_table, which must hold no pages, receive the snapshot's
+ * page ids prefix_pages[n_prefix_pages] at indices [0, n_prefix_pages), one reference per row. */
+fka_status fka_pool_fork(fka_pool *pool, const int32_t *prefix_pages, int32_t n_prefix_pages,
+                         int32_t *page_table, int32_t max_pages, int32_t first, int32_t n);
+
+/* Row `seq` (group prefix prefix_len tokens, whose ceil(prefix_len / 16) pages it holds) gets
+ * pages for suffix positions [0, suffix_len): the missing ones are taken (count 1) and written at
+ * indices ceil(prefix_len / 16) + j / 16.  *n_new (nullable) receives how many were taken. */
+fka_status fka_pool_reserve(fka_pool *pool, int32_t *page_table, int32_t max_pages, int32_t seq,
+                            int32_t prefix_len, int32_t suffix_len, int32_t *n_new);
+
+/* Cancel or harvest row `seq`: one reference to each of its pages is released; the row becomes -1. */
+fka_status fka_pool_drop(fka_pool *pool, int32_t *page_table, int32_t max_pages, int32_t seq);
+
+/* Next snapshot from row `seq`, a context of prefix_len + suffix_len tokens in the fork layout.
+ * dense[ceil((prefix_len + suffix_len) / 16)] receives page ids for the same context laid out
+ * densely; the row's references move there and the row becomes -1.  Pages are reused where the
+ * row holds the only reference: the full prefix pages keep their ids and positions; the last,
+ * partly filled prefix page (unless shared) and the suffix pages are refilled in order; pages
+ * left over are released and missing ones taken.  *from receives 16 * floor(prefix_len / 16):
+ * positions [from, prefix_len + suffix_len) must be rewritten by fka_scatter_pages from a copy
+ * gathered (fka_gather_paged) with the row's old device table before the scatter runs. */
+fka_status fka_pool_promote(fka_pool *pool, int32_t *page_table, int32_t max_pages, int32_t seq,
+                            int32_t prefix_len, int32_t suffix_len, int32_t *dense, int32_t *from);
+
+/* Device copy of positions [from, len) of k_src / v_src bf16 [n_kv_heads][len][head_dim]
+ * (contiguous) into the pool bf16 [n_pool_pages][n_kv_heads][16][head_dim] at the dense layout
+ * of page_row (device int32 [ceil(len / 16)]): position p goes to page page_row[p / 16], slot
+ * p % 16.  Bit copies.  A page id outside [0, n_pool_pages) is skipped and bit 4 is or-ed into
+ * *err (device int32; nullable).  Enqueued on `stream`. */
+fka_status fka_scatter_pages(const void *k_src, const void *v_src, int32_t len, int32_t from,
+                             const int32_t *page_row, int32_t n_kv_heads, int32_t head_dim, int32_t n_pool_pages,
+                             void *k_pool, void *v_pool, int32_t *err, void *stream);
+
 /* -------------------------------------------------------------- stage entry points */
 
 /* Schedule geometry of a plan.  The keys are cut into items: one per (prefix unit,

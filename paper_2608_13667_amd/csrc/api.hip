@@ -6,7 +6,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <new>
+#include <set>
 #include <vector>
 
 #include "forkattn.h"
@@ -53,6 +55,12 @@ struct fka_plan {
     int32_t *d_lens = nullptr;
     float *part_o = nullptr;
     float *part_lse = nullptr;
+};
+
+// Page pool: reference count per page id; free ids kept ordered so allocation takes the lowest.
+struct fka_pool {
+    std::vector<int32_t> ref;
+    std::set<int32_t> free_ids;
 };
 
 namespace {
@@ -814,6 +822,246 @@ void fka_plan_destroy(fka_plan *p)
     if (!p) return;
     if (p->mem) (void)hipFree(p->mem);
     delete p;
+}
+
+/* ------------------------------------------------------------------ page pool */
+
+fka_status fka_pool_create(int32_t n_pages, fka_pool **out)
+{
+    REQUIRE(out != nullptr, "out is null");
+    *out = nullptr;
+    REQUIRE(n_pages >= 0, "n_pages must be >= 0");
+    fka_pool *pool = new (std::nothrow) fka_pool;
+    if (!pool) return fail(FKA_ERR_NOMEM, "pool: host allocation failed");
+    try {
+        pool->ref.assign(n_pages, 0);
+        for (int32_t i = 0; i < n_pages; ++i) pool->free_ids.insert(pool->free_ids.end(), i);
+    } catch (...) {
+        delete pool;
+        return fail(FKA_ERR_NOMEM, "pool: host allocation failed");
+    }
+    *out = pool;
+    return ok();
+}
+
+void fka_pool_destroy(fka_pool *pool) { delete pool; }
+
+int32_t fka_pool_free_pages(const fka_pool *pool) { return pool ? (int32_t)pool->free_ids.size() : -1; }
+
+int32_t fka_pool_refcount(const fka_pool *pool, int32_t page)
+{
+    if (!pool || page < 0 || page >= (int32_t)pool->ref.size()) return -1;
+    return pool->ref[page];
+}
+
+}  // extern "C"
+
+namespace {
+
+// References to drop per page, checked against the counts before anything changes.
+fka_status check_drops(const fka_pool *pool, const std::map<int32_t, int32_t> &drops)
+{
+    for (const auto &kv : drops) {
+        REQUIRE(kv.first >= 0 && kv.first < (int32_t)pool->ref.size(), "page id %d outside the pool", kv.first);
+        REQUIRE(pool->ref[kv.first] >= kv.second, "page %d has %d reference(s), %d to drop", kv.first,
+                pool->ref[kv.first], kv.second);
+    }
+    return FKA_OK;
+}
+
+void apply_drops(fka_pool *pool, const std::map<int32_t, int32_t> &drops)
+{
+    for (const auto &kv : drops)
+        if ((pool->ref[kv.first] -= kv.second) == 0) pool->free_ids.insert(kv.first);
+}
+
+void take_pages(fka_pool *pool, int32_t n, int32_t *ids)  // n <= free pages
+{
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t id = *pool->free_ids.begin();
+        pool->free_ids.erase(pool->free_ids.begin());
+        pool->ref[id] = 1;
+        ids[i] = id;
+    }
+}
+
+bool live(const fka_pool *pool, int32_t id) { return id >= 0 && id < (int32_t)pool->ref.size() && pool->ref[id] > 0; }
+
+int32_t pages_for(int64_t tokens) { return (int32_t)((tokens + fka::kPageSize - 1) / fka::kPageSize); }
+
+}  // namespace
+
+extern "C" {
+
+fka_status fka_pool_alloc(fka_pool *pool, int32_t n, int32_t *ids)
+{
+    REQUIRE(pool != nullptr, "pool is null");
+    REQUIRE(n >= 0, "n must be >= 0");
+    REQUIRE(n == 0 || ids != nullptr, "ids is null");
+    if (n > (int32_t)pool->free_ids.size())
+        return fail(FKA_ERR_NOMEM, "%d pages asked, %d free", n, (int32_t)pool->free_ids.size());
+    take_pages(pool, n, ids);
+    return ok();
+}
+
+fka_status fka_pool_retain(fka_pool *pool, int32_t n, const int32_t *ids)
+{
+    REQUIRE(pool != nullptr, "pool is null");
+    REQUIRE(n >= 0, "n must be >= 0");
+    REQUIRE(n == 0 || ids != nullptr, "ids is null");
+    for (int32_t i = 0; i < n; ++i) REQUIRE(live(pool, ids[i]), "page id %d is not live", ids[i]);
+    for (int32_t i = 0; i < n; ++i) ++pool->ref[ids[i]];
+    return ok();
+}
+
+fka_status fka_pool_release(fka_pool *pool, int32_t n, const int32_t *ids)
+{
+    REQUIRE(pool != nullptr, "pool is null");
+    REQUIRE(n >= 0, "n must be >= 0");
+    REQUIRE(n == 0 || ids != nullptr, "ids is null");
+    std::map<int32_t, int32_t> drops;
+    for (int32_t i = 0; i < n; ++i) ++drops[ids[i]];
+    fka_status st = check_drops(pool, drops);
+    if (st != FKA_OK) return st;
+    apply_drops(pool, drops);
+    return ok();
+}
+
+fka_status fka_pool_fork(fka_pool *pool, const int32_t *prefix_pages, int32_t n_prefix_pages, int32_t *page_table,
+                         int32_t max_pages, int32_t first, int32_t n)
+{
+    REQUIRE(pool != nullptr && page_table != nullptr, "null argument");
+    REQUIRE(max_pages > 0 && n_prefix_pages >= 0 && n_prefix_pages <= max_pages,
+            "n_prefix_pages %d outside [0, max_pages %d]", n_prefix_pages, max_pages);
+    REQUIRE(n_prefix_pages == 0 || prefix_pages != nullptr, "prefix_pages is null");
+    REQUIRE(first >= 0 && n >= 0, "first and n must be >= 0");
+    for (int32_t i = 0; i < n_prefix_pages; ++i)
+        REQUIRE(live(pool, prefix_pages[i]), "snapshot page id %d is not live", prefix_pages[i]);
+    for (int64_t r = first; r < (int64_t)first + n; ++r)
+        for (int32_t i = 0; i < max_pages; ++i)
+            REQUIRE(page_table[r * max_pages + i] == -1, "row %lld holds pages", (long long)r);
+    for (int64_t r = first; r < (int64_t)first + n; ++r)
+        for (int32_t i = 0; i < n_prefix_pages; ++i) {
+            page_table[r * max_pages + i] = prefix_pages[i];
+            ++pool->ref[prefix_pages[i]];
+        }
+    return ok();
+}
+
+fka_status fka_pool_reserve(fka_pool *pool, int32_t *page_table, int32_t max_pages, int32_t seq,
+                            int32_t prefix_len, int32_t suffix_len, int32_t *n_new)
+{
+    REQUIRE(pool != nullptr && page_table != nullptr, "null argument");
+    REQUIRE(max_pages > 0 && seq >= 0 && prefix_len >= 0 && suffix_len >= 0, "negative size or index");
+    const int32_t a = pages_for(prefix_len), ns = pages_for(suffix_len);
+    REQUIRE((int64_t)a + ns <= max_pages, "%d prefix and %d suffix pages exceed max_pages %d", a, ns, max_pages);
+    int32_t *row = page_table + (int64_t)seq * max_pages;
+    int32_t missing = 0;
+    for (int32_t i = 0; i < a + ns; ++i) {
+        if (row[i] == -1 && i >= a) {
+            ++missing;
+            continue;
+        }
+        REQUIRE(live(pool, row[i]), "row %d index %d: page id %d is not live", seq, i, row[i]);
+    }
+    if (missing > (int32_t)pool->free_ids.size())
+        return fail(FKA_ERR_NOMEM, "%d pages needed, %d free", missing, (int32_t)pool->free_ids.size());
+    for (int32_t i = a; i < a + ns; ++i)
+        if (row[i] == -1) take_pages(pool, 1, &row[i]);
+    if (n_new) *n_new = missing;
+    return ok();
+}
+
+fka_status fka_pool_drop(fka_pool *pool, int32_t *page_table, int32_t max_pages, int32_t seq)
+{
+    REQUIRE(pool != nullptr && page_table != nullptr, "null argument");
+    REQUIRE(max_pages > 0 && seq >= 0, "bad max_pages or seq");
+    int32_t *row = page_table + (int64_t)seq * max_pages;
+    std::map<int32_t, int32_t> drops;
+    for (int32_t i = 0; i < max_pages; ++i)
+        if (row[i] != -1) ++drops[row[i]];
+    fka_status st = check_drops(pool, drops);
+    if (st != FKA_OK) return st;
+    apply_drops(pool, drops);
+    for (int32_t i = 0; i < max_pages; ++i) row[i] = -1;
+    return ok();
+}
+
+fka_status fka_pool_promote(fka_pool *pool, int32_t *page_table, int32_t max_pages, int32_t seq, int32_t prefix_len,
+                            int32_t suffix_len, int32_t *dense, int32_t *from)
+{
+    REQUIRE(pool != nullptr && page_table != nullptr && dense != nullptr && from != nullptr, "null argument");
+    REQUIRE(max_pages > 0 && seq >= 0 && prefix_len >= 0 && suffix_len >= 0, "negative size or index");
+    const int32_t k0 = prefix_len / fka::kPageSize, a = pages_for(prefix_len), ns = pages_for(suffix_len);
+    REQUIRE((int64_t)a + ns <= max_pages, "%d prefix and %d suffix pages exceed max_pages %d", a, ns, max_pages);
+    const int32_t n_dense = pages_for((int64_t)prefix_len + suffix_len);
+    int32_t *row = page_table + (int64_t)seq * max_pages;
+    for (int32_t i = 0; i < a + ns; ++i)
+        REQUIRE(live(pool, row[i]), "row %d index %d: page id %d is not live", seq, i, row[i]);
+    std::map<int32_t, int32_t> held;  // the row's references
+    for (int32_t i = 0; i < max_pages; ++i)
+        if (row[i] != -1) ++held[row[i]];
+    fka_status st = check_drops(pool, held);
+    if (st != FKA_OK) return st;
+    // pages the row may refill: the partial prefix page, then the suffix pages (and any reserved
+    // beyond them), each only where the row holds the page's one reference
+    std::vector<int32_t> reuse, drop;
+    for (int32_t i = k0; i < max_pages; ++i) {
+        if (row[i] == -1) continue;
+        if (pool->ref[row[i]] == 1 && held[row[i]] == 1)
+            reuse.push_back(row[i]);
+        else
+            drop.push_back(row[i]);
+    }
+    const int32_t need = n_dense - k0;
+    const int32_t take = std::max(0, need - (int32_t)reuse.size());
+    if (take > (int32_t)pool->free_ids.size())
+        return fail(FKA_ERR_NOMEM, "%d pages needed, %d free", take, (int32_t)pool->free_ids.size());
+    for (int32_t i = 0; i < k0; ++i) dense[i] = row[i];
+    std::map<int32_t, int32_t> drops;
+    for (int32_t id : drop) ++drops[id];
+    for (int32_t j = 0; j < (int32_t)reuse.size(); ++j) {
+        if (j < need)
+            dense[k0 + j] = reuse[j];
+        else
+            ++drops[reuse[j]];
+    }
+    apply_drops(pool, drops);
+    if (take > 0) take_pages(pool, take, dense + k0 + (int32_t)reuse.size());
+    for (int32_t i = 0; i < max_pages; ++i) row[i] = -1;
+    *from = k0 * fka::kPageSize;
+    return ok();
+}
+
+fka_status fka_scatter_pages(const void *k_src, const void *v_src, int32_t len, int32_t from, const int32_t *page_row,
+                             int32_t n_kv_heads, int32_t head_dim, int32_t n_pool_pages, void *k_pool, void *v_pool,
+                             int32_t *err, void *stream)
+{
+    REQUIRE(len >= 0 && from >= 0 && from <= len, "need 0 <= from <= len (from %d, len %d)", from, len);
+    REQUIRE(head_dim == 64 || head_dim == 128, "head_dim %d: 64 or 128", head_dim);
+    REQUIRE(n_kv_heads >= 1 && n_kv_heads <= 65535, "n_kv_heads %d outside [1, 65535]", n_kv_heads);
+    REQUIRE(n_pool_pages >= 0, "n_pool_pages must be >= 0");
+    if (len == from) return ok();
+    REQUIRE_PTR16(k_src);
+    REQUIRE_PTR16(v_src);
+    REQUIRE_PTR16(k_pool);
+    REQUIRE_PTR16(v_pool);
+    REQUIRE(page_row != nullptr, "page_row is null");
+    fka::ScatterArgs s{};
+    s.k_src = static_cast<const uint16_t *>(k_src);
+    s.v_src = static_cast<const uint16_t *>(v_src);
+    s.page_row = page_row;
+    s.k_pool = static_cast<uint16_t *>(k_pool);
+    s.v_pool = static_cast<uint16_t *>(v_pool);
+    s.len = len;
+    s.from = from;
+    s.n_pool_pages = n_pool_pages;
+    s.n_kv_heads = n_kv_heads;
+    s.head_dim = head_dim;
+    s.err = err;
+    hipError_t e = fka::launch_scatter(s, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "scatter kernel launch");
+    return ok();
 }
 
 }  // extern "C"

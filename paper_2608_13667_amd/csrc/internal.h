@@ -245,6 +245,18 @@ struct GatherArgs {
     int32_t *err;
 };
 
+struct ScatterArgs {
+    const uint16_t *k_src, *v_src;  // [Hkv][len][d]
+    const int32_t *page_row;        // dense layout: position p at page_row[p / 16], slot p % 16
+    uint16_t *k_pool, *v_pool;
+    int32_t len;
+    int32_t from;
+    int32_t n_pool_pages;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t *err;                   // nullable
+};
+
 // error-flag bits (device)
 constexpr int32_t kErrSuffixClamped = 1;
 constexpr int32_t kErrAppendNoRoom = 2;
@@ -259,5 +271,6 @@ int partials_waves_per_block(int head_dim, int row_tiles, bool paged);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
+hipError_t launch_scatter(const ScatterArgs &a, hipStream_t s);
 
 }  // namespace fka

@@ -374,7 +374,37 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a)
     }
 }
 
+// grid (pages covering [from, len), Hkv): block copies the positions of one page of one KV head
+// from the contiguous source into the pool's dense layout.
+__global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a)
+{
+    const int g = blockIdx.y;
+    const int pidx = a.from / kPageSize + blockIdx.x;
+    const int page = a.page_row[pidx];
+    if (page < 0 || page >= a.n_pool_pages) {
+        if (threadIdx.x == 0 && a.err) atomicOr(a.err, kErrBadPage);
+        return;
+    }
+    const int cpr = a.head_dim / 8;
+    for (int i = threadIdx.x; i < kPageSize * cpr; i += blockDim.x) {
+        const int slot = i / cpr, c = i % cpr, pos = pidx * kPageSize + slot;
+        if (pos < a.from || pos >= a.len) continue;
+        const size_t src = ((size_t)g * a.len + pos) * a.head_dim + 8 * c;
+        const size_t dst = (((size_t)page * a.n_kv_heads + g) * kPageSize + slot) * a.head_dim + 8 * c;
+        *reinterpret_cast<uint4 *>(a.k_pool + dst) = *reinterpret_cast<const uint4 *>(a.k_src + src);
+        *reinterpret_cast<uint4 *>(a.v_pool + dst) = *reinterpret_cast<const uint4 *>(a.v_src + src);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_scatter(const ScatterArgs &a, hipStream_t s)
+{
+    if (a.len <= a.from) return hipSuccess;
+    const int blocks = (a.len + kPageSize - 1) / kPageSize - a.from / kPageSize;
+    scatter_kernel<<<dim3(blocks, a.n_kv_heads), dim3(256), 0, s>>>(a);
+    return hipGetLastError();
+}
 
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s)
 {

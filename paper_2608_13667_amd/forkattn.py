@@ -10,6 +10,7 @@ import ctypes as C
 import os
 from typing import Optional
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -71,6 +72,20 @@ _sig = {
     "fka_lse_merge": ([C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp], C.c_int),
     "fka_plan_device_error": ([_vp, C.POINTER(C.c_int32)], C.c_int),
     "fka_plan_destroy": ([_vp], None),
+    "fka_pool_create": ([C.c_int32, C.POINTER(_vp)], C.c_int),
+    "fka_pool_destroy": ([_vp], None),
+    "fka_pool_free_pages": ([_vp], C.c_int32),
+    "fka_pool_refcount": ([_vp, C.c_int32], C.c_int32),
+    "fka_pool_alloc": ([_vp, C.c_int32, _vp], C.c_int),
+    "fka_pool_retain": ([_vp, C.c_int32, _vp], C.c_int),
+    "fka_pool_release": ([_vp, C.c_int32, _vp], C.c_int),
+    "fka_pool_fork": ([_vp, _vp, C.c_int32, _vp, C.c_int32, C.c_int32, C.c_int32], C.c_int),
+    "fka_pool_reserve": ([_vp, _vp, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_int32)], C.c_int),
+    "fka_pool_drop": ([_vp, _vp, C.c_int32, C.c_int32], C.c_int),
+    "fka_pool_promote": ([_vp, _vp, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _vp, C.POINTER(C.c_int32)],
+                         C.c_int),
+    "fka_scatter_pages": ([_vp, _vp, C.c_int32, C.c_int32, _vp, C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp],
+                          C.c_int),
 }
 for _name, (_args, _res) in _sig.items():
     _f = getattr(_lib, _name)
@@ -135,7 +150,6 @@ class Plan:
     def paged_plan(cls, n_q_heads, n_kv_heads, head_dim, group_start, group_prefix_len, max_pages_per_seq,
                    n_pool_pages, max_suffix_len, share_prefix=True, rounds=0, softmax_scale=0.0,
                    page_size=16) -> "Plan":
-        import numpy as np
         gs = np.ascontiguousarray(group_start, np.int32)
         gl = np.ascontiguousarray(group_prefix_len, np.int32)
         h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
@@ -217,6 +231,82 @@ class Plan:
     def gather_paged(self, seq, k_pool, v_pool, page_table, out_len, k_out, v_out, stream=None):
         _check(_lib.fka_gather_paged(self._h, int(seq), _p(k_pool), _p(v_pool), _p(page_table), int(out_len),
                                      _p(k_out), _p(v_out), _stream(stream)))
+
+
+def _host_i32(a: np.ndarray) -> _vp:
+    if a.dtype != np.int32 or not a.flags["C_CONTIGUOUS"] or not a.flags["WRITEABLE"]:
+        raise ValueError("host page ids must be a writeable C-contiguous int32 array")
+    return _vp(a.ctypes.data)
+
+
+class Pool:
+    """Page pool of a paged K/V store (host bookkeeping; see fka_pool_* in forkattn.h).  Page
+    tables are host numpy int32 arrays [rows][max_pages] with -1 for no page."""
+
+    def __init__(self, n_pages: int):
+        h = _vp()
+        _check(_lib.fka_pool_create(int(n_pages), C.byref(h)))
+        self._h = h
+
+    def close(self):
+        if self._h:
+            _lib.fka_pool_destroy(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def free_pages(self) -> int:
+        return _lib.fka_pool_free_pages(self._h)
+
+    def refcount(self, page: int) -> int:
+        return _lib.fka_pool_refcount(self._h, int(page))
+
+    def alloc(self, n: int) -> np.ndarray:
+        ids = np.empty(int(n), np.int32)
+        _check(_lib.fka_pool_alloc(self._h, int(n), _host_i32(ids)))
+        return ids
+
+    def retain(self, ids: np.ndarray):
+        ids = np.ascontiguousarray(ids, np.int32)
+        _check(_lib.fka_pool_retain(self._h, ids.size, _host_i32(ids)))
+
+    def release(self, ids: np.ndarray):
+        ids = np.ascontiguousarray(ids, np.int32)
+        _check(_lib.fka_pool_release(self._h, ids.size, _host_i32(ids)))
+
+    def fork(self, prefix_pages: np.ndarray, table: np.ndarray, first: int, n: int):
+        prefix_pages = np.ascontiguousarray(prefix_pages, np.int32)
+        _check(_lib.fka_pool_fork(self._h, _host_i32(prefix_pages), prefix_pages.size, _host_i32(table),
+                                  table.shape[1], int(first), int(n)))
+
+    def reserve(self, table: np.ndarray, seq: int, prefix_len: int, suffix_len: int) -> int:
+        n_new = C.c_int32(0)
+        _check(_lib.fka_pool_reserve(self._h, _host_i32(table), table.shape[1], int(seq), int(prefix_len),
+                                     int(suffix_len), C.byref(n_new)))
+        return n_new.value
+
+    def drop(self, table: np.ndarray, seq: int):
+        _check(_lib.fka_pool_drop(self._h, _host_i32(table), table.shape[1], int(seq)))
+
+    def promote(self, table: np.ndarray, seq: int, prefix_len: int, suffix_len: int):
+        """Returns (dense page ids, first position to rewrite)."""
+        n = (int(prefix_len) + int(suffix_len) + 15) // 16
+        dense = np.full(max(n, 1), -1, np.int32)
+        frm = C.c_int32(0)
+        _check(_lib.fka_pool_promote(self._h, _host_i32(table), table.shape[1], int(seq), int(prefix_len),
+                                     int(suffix_len), _host_i32(dense), C.byref(frm)))
+        return dense[:n], frm.value
+
+
+def scatter_pages(k_src, v_src, frm, page_row, n_pool_pages, k_pool, v_pool, err=None, stream=None):
+    """k_src / v_src bf16 (int16 storage) [Hkv][len][d] -> pool pages of page_row (device int32)."""
+    Hkv, L, d = k_src.shape
+    _check(_lib.fka_scatter_pages(_p(k_src), _p(v_src), L, int(frm), _p(page_row), Hkv, d, int(n_pool_pages),
+                                  _p(k_pool), _p(v_pool), _p(err), _stream(stream)))
 
 
 def lse_merge(part_o, part_lse, out, out_lse=None, stream=None):

@@ -1,0 +1,109 @@
+"""The K/V lifecycle of a fork on the device, through the C ABI: the snapshot scattered into pool
+pages, five sequences forked off it (fka_pool_fork), decode steps with appends into pages the pool
+reserves ahead, harvest (the four branches dropped), the main sequence promoted to the next
+snapshot (gather, fka_pool_promote, fka_scatter_pages) and a second turn forked off that.  Outputs
+are checked against the oracle over the materialised contexts; the gathers bit-exactly."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13667_amd import workloads as W
+from tests import gates
+from tests.gpu_util import dev_bf16, dev_i32
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fa():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_13667_amd import forkattn
+    return forkattn
+
+
+def _bf16(rng, shape):
+    return W.bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+
+
+def test_fork_lifecycle_on_device(fa):
+    Hq, Hkv, d, N = 16, 4, 128, 5
+    Lp, S1, S2 = 1000, 37, 21  # 1000 = 62 pages + 8 tokens: the last prefix page is shared, partly filled
+    n_pages, max_pages = 160, 72
+    scale = 1.0 / math.sqrt(d)
+    rng = np.random.default_rng(2608)
+    prefix_k, prefix_v = _bf16(rng, (Hkv, Lp, d)), _bf16(rng, (Hkv, Lp, d))
+    pool = fa.Pool(n_pages)
+    k_pool = dev_bf16(np.full((n_pages, Hkv, 16, d), W.BF16_NAN, np.uint16))
+    v_pool = dev_bf16(np.full((n_pages, Hkv, 16, d), W.BF16_NAN, np.uint16))
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def turn(plan, table, lp, ctx_k, ctx_v, steps, what):
+        """steps fused append + decode steps on all N sequences, pages reserved one token ahead."""
+        suf_k = np.full((N, Hkv, steps, d), W.BF16_NAN, np.uint16)
+        suf_v = np.full((N, Hkv, steps, d), W.BF16_NAN, np.uint16)
+        lens = dev_i32(np.zeros(N, np.int32))
+        out = torch.empty((N, Hq, d), device="cuda")
+        lse = torch.empty((N, Hq), device="cuda")
+        for t in range(steps):
+            for b in range(N):
+                pool.reserve(table, b, lp, t + 1)
+            q, kn, vn = _bf16(rng, (N, Hq, d)), _bf16(rng, (N, Hkv, d)), _bf16(rng, (N, Hkv, d))
+            suf_k[:, :, t], suf_v[:, :, t] = kn, vn
+            plan.step_paged(dev_bf16(q), dev_bf16(kn), dev_bf16(vn), k_pool, v_pool, dev_i32(table), lens, out, lse)
+            if t in (0, steps - 1):
+                torch.cuda.synchronize()
+                ref, ref_lse = oracle.decode_contig(q, ctx_k, ctx_v, suf_k, suf_v, np.full(N, t + 1, np.int32), scale)
+                print(f"[pool] {what} step {t}", flush=True)
+                gates.assert_gates(out.cpu().numpy(), ref, what=f"{what} step {t}")
+                gates.assert_lse(lse.cpu().numpy(), ref_lse, what=f"{what} step {t}")
+        assert lens.cpu().tolist() == [steps] * N
+        return suf_k, suf_v
+
+    # turn 1: the snapshot into pages, five sequences forked off it
+    snap = pool.alloc(-(-Lp // 16))
+    fa.scatter_pages(dev_bf16(prefix_k), dev_bf16(prefix_v), 0, dev_i32(snap), n_pages, k_pool, v_pool, err)
+    table = np.full((N, max_pages), -1, np.int32)
+    pool.fork(snap, table, 0, N)
+    pool.release(snap)
+    assert pool.refcount(int(snap[-1])) == N
+    plan1 = fa.Plan.paged_plan(Hq, Hkv, d, [0, N], [Lp], max_pages, n_pages, S1)
+    suf_k, suf_v = turn(plan1, table, Lp, prefix_k, prefix_v, S1, "turn 1")
+
+    # harvest: the branches end; the main sequence's context becomes the next snapshot
+    for b in range(1, N):
+        pool.drop(table, b)
+    assert pool.refcount(int(snap[-1])) == 1
+    L0 = Lp + S1
+    ctx_k = np.concatenate([prefix_k, suf_k[0]], axis=1)
+    ctx_v = np.concatenate([prefix_v, suf_v[0]], axis=1)
+    tmp_k = torch.empty((Hkv, L0, d), dtype=torch.bfloat16, device="cuda")
+    tmp_v = torch.empty_like(tmp_k)
+    plan1.gather_paged(0, k_pool, v_pool, dev_i32(table), L0, tmp_k, tmp_v)
+    dense, frm = pool.promote(table, 0, Lp, S1)
+    assert frm == (Lp // 16) * 16 and len(dense) == -(-L0 // 16)
+    fa.scatter_pages(tmp_k, tmp_v, frm, dev_i32(dense), n_pages, k_pool, v_pool, err)
+    torch.cuda.synchronize()
+    assert np.array_equal(tmp_k.cpu().view(torch.int16).numpy().view(np.uint16), ctx_k)
+    assert np.array_equal(tmp_v.cpu().view(torch.int16).numpy().view(np.uint16), ctx_v)
+
+    # turn 2: five sequences forked off the promoted context
+    table2 = np.full((N, max_pages), -1, np.int32)
+    pool.fork(dense, table2, 0, N)
+    pool.release(dense)
+    plan2 = fa.Plan.paged_plan(Hq, Hkv, d, [0, N], [L0], max_pages, n_pages, S2)
+    g_k, g_v = torch.empty_like(tmp_k), torch.empty_like(tmp_v)
+    plan2.gather_paged(3, k_pool, v_pool, dev_i32(table2), L0, g_k, g_v)
+    torch.cuda.synchronize()
+    assert np.array_equal(g_k.cpu().view(torch.int16).numpy().view(np.uint16), ctx_k)
+    assert np.array_equal(g_v.cpu().view(torch.int16).numpy().view(np.uint16), ctx_v)
+    turn(plan2, table2, L0, ctx_k, ctx_v, S2, "turn 2")
+
+    for b in range(N):
+        pool.drop(table2, b)
+    assert pool.free_pages() == n_pages
+    assert int(err.item()) == 0
+    assert plan1.device_error() == 0 and plan2.device_error() == 0
