@@ -79,7 +79,86 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-naive", action="store_true", help="skip the naive per-branch GPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--lifecycle", action="store_true",
+                    help="also time the fork lifecycle on the page pool (contiguous workloads' shapes)")
     return ap.parse_args()
+
+
+def lifecycle_timing(fa, torch, w):
+    """One turn transition of the fork lifecycle at the workload's shape, with a page pool: fork
+    the snapshot to all sequences, reserve their suffix pages, drop the branches, promote the main
+    sequence (host bookkeeping), and the promote's device work (a gather of the main context's tail,
+    from the first page the dense layout rewrites, and its scatter into the dense pages).  Host calls are timed with perf_counter over many cycles,
+    the device work with HIP events on the launch stream."""
+    spec = w.spec
+    N, Hkv, d = w.n_branches, spec.n_kv_heads, spec.head_dim
+    Lp, lens = w.prefix_len, [int(x) for x in w.suffix_len]
+    a = -(-Lp // 16)
+    max_pages = a + -(-max(lens) // 16) + 1
+    n_pages = a + sum(-(-L // 16) for L in lens) + -(-(Lp + max(lens)) // 16) + 8
+    pool = fa.Pool(n_pages)
+    pages = torch.zeros((n_pages, Hkv, 16, d), dtype=torch.bfloat16, device="cuda")
+    v_pages = torch.zeros_like(pages)
+    host = {"fork": [], "reserve": [], "drop": [], "promote": []}
+    cycles = 50
+    for _ in range(cycles):
+        snap = pool.alloc(a)
+        table = np.full((N, max_pages), -1, np.int32)
+        t0 = time.perf_counter()
+        pool.fork(snap, table, 0, N)
+        t1 = time.perf_counter()
+        for b in range(N):
+            pool.reserve(table, b, Lp, lens[b])
+        t2 = time.perf_counter()
+        for b in range(1, N):
+            pool.drop(table, b)
+        t3 = time.perf_counter()
+        dense, frm = pool.promote(table, 0, Lp, lens[0])
+        t4 = time.perf_counter()
+        host["fork"].append(t1 - t0)
+        host["reserve"].append((t2 - t1) / N)
+        host["drop"].append((t3 - t2) / (N - 1))
+        host["promote"].append(t4 - t3)
+        pool.release(snap)
+        pool.release(dense)
+    assert pool.free_pages() == n_pages
+    # device work of one promote, on a table from a fresh fork
+    snap = pool.alloc(a)
+    table = np.full((N, max_pages), -1, np.int32)
+    pool.fork(snap, table, 0, N)
+    pool.reserve(table, 0, Lp, lens[0])
+    L0 = Lp + lens[0]
+    plan = fa.Plan.paged_plan(spec.n_q_heads, Hkv, d, [0, N], [Lp], max_pages, n_pages, max(lens))
+    old_row = torch.from_numpy(table).cuda()
+    for b in range(1, N):
+        pool.drop(table, b)
+    dense, frm = pool.promote(table, 0, Lp, lens[0])
+    dense_dev = torch.from_numpy(dense).cuda()
+    tmp_k = torch.empty((Hkv, L0 - frm, d), dtype=torch.bfloat16, device="cuda")
+    tmp_v = torch.empty_like(tmp_k)
+    stream = torch.cuda.current_stream()
+
+    def promote_device():
+        plan.gather_paged_range(0, frm, L0, pages, v_pages, old_row, tmp_k, tmp_v, stream)
+        fa.scatter_pages(tmp_k, tmp_v, frm, dense_dev, n_pages, pages, v_pages, None, stream)
+
+    for _ in range(5):
+        promote_device()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    e0.record(stream)
+    for _ in range(reps):
+        promote_device()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    dev_s = e0.elapsed_time(e1) / 1e3 / reps
+    per_tok = Hkv * d * 2 * 2
+    moved = 4 * per_tok * (L0 - frm)  # the gather and the scatter each read and write L0 - frm tokens
+    plan.close()
+    pool.close()
+    ms = lambda v: float(np.median(v) * 1e6)
+    return {"tokens_promoted": L0, "host_us": {k: ms(v) for k, v in host.items()},
+            "promote_device_us": dev_s * 1e6, "promote_device_gbps": moved / dev_s / 1e9}
 
 
 def main():
@@ -304,6 +383,9 @@ def main():
         "cpu_baseline": cpu,
     }
     res.update(result_extra)
+    if args.lifecycle and not paged:
+        res["lifecycle"] = lifecycle_timing(fa, torch, w)
+        log(f"[bench] lifecycle: {res['lifecycle']}")
     plan.close()
     print(json.dumps(res), flush=True)
 

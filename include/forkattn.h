@@ -206,6 +206,12 @@ fka_status fka_fork_step_paged(const fka_plan *plan, const void *q, const void *
 fka_status fka_gather_paged(const fka_plan *plan, int32_t seq, const void *k_pool, const void *v_pool,
                             const int32_t *page_table, int32_t out_len, void *k_out, void *v_out, void *stream);
 
+/* As fka_gather_paged for logical positions [begin, out_len) only: k_out / v_out bf16
+ * [Hkv][out_len - begin][d].  0 <= begin <= out_len. */
+fka_status fka_gather_paged_range(const fka_plan *plan, int32_t seq, int32_t begin, int32_t out_len,
+                                  const void *k_pool, const void *v_pool, const int32_t *page_table, void *k_out,
+                                  void *v_out, void *stream);
+
 /* ------------------------------------------------ page pool: the K/V lifecycle of a fork */
 
 /*
@@ -267,12 +273,12 @@ fka_status fka_pool_drop(fka_pool *pool, int32_t *page_table, int32_t max_pages,
  * partly filled prefix page (unless shared) and the suffix pages are refilled in order; pages
  * left over are released and missing ones taken.  *from receives 16 * floor(prefix_len / 16):
  * positions [from, prefix_len + suffix_len) must be rewritten by fka_scatter_pages from a copy
- * gathered (fka_gather_paged) with the row's old device table before the scatter runs. */
+ * gathered (fka_gather_paged_range) with the row's old device table before the scatter runs. */
 fka_status fka_pool_promote(fka_pool *pool, int32_t *page_table, int32_t max_pages, int32_t seq,
                             int32_t prefix_len, int32_t suffix_len, int32_t *dense, int32_t *from);
 
-/* Device copy of positions [from, len) of k_src / v_src bf16 [n_kv_heads][len][head_dim]
- * (contiguous) into the pool bf16 [n_pool_pages][n_kv_heads][16][head_dim] at the dense layout
+/* Device copy of positions [from, len), held in k_src / v_src bf16 [n_kv_heads][len - from][head_dim]
+ * (contiguous), into the pool bf16 [n_pool_pages][n_kv_heads][16][head_dim] at the dense layout
  * of page_row (device int32 [ceil(len / 16)]): position p goes to page page_row[p / 16], slot
  * p % 16.  Bit copies.  A page id outside [0, n_pool_pages) is skipped and bit 4 is or-ed into
  * *err (device int32; nullable).  Enqueued on `stream`. */

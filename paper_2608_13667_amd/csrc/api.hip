@@ -6,7 +6,6 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
-#include <map>
 #include <new>
 #include <set>
 #include <vector>
@@ -61,6 +60,8 @@ struct fka_plan {
 struct fka_pool {
     std::vector<int32_t> ref;
     std::set<int32_t> free_ids;
+    std::vector<int32_t> pending;  // references a call is about to drop, per page (zero between calls)
+    std::vector<int32_t> touched;  // pages with a pending count
 };
 
 namespace {
@@ -748,6 +749,13 @@ fka_status fka_append_kv_paged(const fka_plan *p, const void *k_new, const void 
 fka_status fka_gather_paged(const fka_plan *p, int32_t seq, const void *k_pool, const void *v_pool,
                             const int32_t *page_table, int32_t out_len, void *k_out, void *v_out, void *stream)
 {
+    return fka_gather_paged_range(p, seq, 0, out_len, k_pool, v_pool, page_table, k_out, v_out, stream);
+}
+
+fka_status fka_gather_paged_range(const fka_plan *p, int32_t seq, int32_t begin, int32_t out_len, const void *k_pool,
+                                  const void *v_pool, const int32_t *page_table, void *k_out, void *v_out,
+                                  void *stream)
+{
     REQUIRE(p != nullptr, "plan is null");
     REQUIRE(p->paged, "plan is contiguous");
     REQUIRE(seq >= 0 && seq < p->n_seqs, "seq %d out of range [0, %d)", seq, p->n_seqs);
@@ -759,7 +767,8 @@ fka_status fka_gather_paged(const fka_plan *p, int32_t seq, const void *k_pool, 
     int t = 0;
     while (t + 1 < p->n_groups && p->group_start[t + 1] <= seq) ++t;
     const int lp = p->group_prefix_len[t];
-    REQUIRE(out_len >= 0, "out_len must be >= 0");
+    REQUIRE(out_len >= 0 && begin >= 0 && begin <= out_len, "need 0 <= begin <= out_len (begin %d, out_len %d)",
+            begin, out_len);
     const int64_t pages = ceil_div(lp, fka::kPageSize) + (out_len > lp ? ceil_div(out_len - lp, fka::kPageSize) : 0);
     REQUIRE(pages <= p->max_pages, "out_len %d needs %lld pages, the table has %d", out_len, (long long)pages,
             p->max_pages);
@@ -771,6 +780,7 @@ fka_status fka_gather_paged(const fka_plan *p, int32_t seq, const void *k_pool, 
     a.v_out = static_cast<uint16_t *>(v_out);
     a.seq = seq;
     a.prefix_len = lp;
+    a.begin = begin;
     a.out_len = out_len;
     a.max_pages = p->max_pages;
     a.n_pool_pages = p->n_pool_pages;
@@ -835,6 +845,7 @@ fka_status fka_pool_create(int32_t n_pages, fka_pool **out)
     if (!pool) return fail(FKA_ERR_NOMEM, "pool: host allocation failed");
     try {
         pool->ref.assign(n_pages, 0);
+        pool->pending.assign(n_pages, 0);
         for (int32_t i = 0; i < n_pages; ++i) pool->free_ids.insert(pool->free_ids.end(), i);
     } catch (...) {
         delete pool;
@@ -858,21 +869,41 @@ int32_t fka_pool_refcount(const fka_pool *pool, int32_t page)
 
 namespace {
 
-// References to drop per page, checked against the counts before anything changes.
-fka_status check_drops(const fka_pool *pool, const std::map<int32_t, int32_t> &drops)
+void clear_drops(fka_pool *pool)
 {
-    for (const auto &kv : drops) {
-        REQUIRE(kv.first >= 0 && kv.first < (int32_t)pool->ref.size(), "page id %d outside the pool", kv.first);
-        REQUIRE(pool->ref[kv.first] >= kv.second, "page %d has %d reference(s), %d to drop", kv.first,
-                pool->ref[kv.first], kv.second);
+    for (int32_t id : pool->touched) pool->pending[id] = 0;
+    pool->touched.clear();
+}
+
+// Counts the references to drop per page (ids[n], entries equal to -1 skipped) and checks them
+// against the counts; nothing changes until apply_drops.
+fka_status count_drops(fka_pool *pool, const int32_t *ids, int64_t n)
+{
+    clear_drops(pool);
+    for (int64_t i = 0; i < n; ++i) {
+        const int32_t id = ids[i];
+        if (id == -1) continue;
+        if (id < 0 || id >= (int32_t)pool->ref.size()) {
+            clear_drops(pool);
+            return fail(FKA_ERR_INVALID_ARG, "page id %d outside the pool", id);
+        }
+        if (pool->pending[id]++ == 0) pool->touched.push_back(id);
+        if (pool->pending[id] > pool->ref[id]) {
+            const int32_t r = pool->ref[id];
+            clear_drops(pool);
+            return fail(FKA_ERR_INVALID_ARG, "page %d has %d reference(s), more to drop", id, r);
+        }
     }
     return FKA_OK;
 }
 
-void apply_drops(fka_pool *pool, const std::map<int32_t, int32_t> &drops)
+void apply_drops(fka_pool *pool)
 {
-    for (const auto &kv : drops)
-        if ((pool->ref[kv.first] -= kv.second) == 0) pool->free_ids.insert(kv.first);
+    for (int32_t id : pool->touched) {
+        if ((pool->ref[id] -= pool->pending[id]) == 0) pool->free_ids.insert(id);
+        pool->pending[id] = 0;
+    }
+    pool->touched.clear();
 }
 
 void take_pages(fka_pool *pool, int32_t n, int32_t *ids)  // n <= free pages
@@ -919,11 +950,10 @@ fka_status fka_pool_release(fka_pool *pool, int32_t n, const int32_t *ids)
     REQUIRE(pool != nullptr, "pool is null");
     REQUIRE(n >= 0, "n must be >= 0");
     REQUIRE(n == 0 || ids != nullptr, "ids is null");
-    std::map<int32_t, int32_t> drops;
-    for (int32_t i = 0; i < n; ++i) ++drops[ids[i]];
-    fka_status st = check_drops(pool, drops);
+    for (int32_t i = 0; i < n; ++i) REQUIRE(ids[i] != -1, "page id -1");
+    fka_status st = count_drops(pool, ids, n);
     if (st != FKA_OK) return st;
-    apply_drops(pool, drops);
+    apply_drops(pool);
     return ok();
 }
 
@@ -977,12 +1007,9 @@ fka_status fka_pool_drop(fka_pool *pool, int32_t *page_table, int32_t max_pages,
     REQUIRE(pool != nullptr && page_table != nullptr, "null argument");
     REQUIRE(max_pages > 0 && seq >= 0, "bad max_pages or seq");
     int32_t *row = page_table + (int64_t)seq * max_pages;
-    std::map<int32_t, int32_t> drops;
-    for (int32_t i = 0; i < max_pages; ++i)
-        if (row[i] != -1) ++drops[row[i]];
-    fka_status st = check_drops(pool, drops);
+    fka_status st = count_drops(pool, row, max_pages);
     if (st != FKA_OK) return st;
-    apply_drops(pool, drops);
+    apply_drops(pool);
     for (int32_t i = 0; i < max_pages; ++i) row[i] = -1;
     return ok();
 }
@@ -998,35 +1025,31 @@ fka_status fka_pool_promote(fka_pool *pool, int32_t *page_table, int32_t max_pag
     int32_t *row = page_table + (int64_t)seq * max_pages;
     for (int32_t i = 0; i < a + ns; ++i)
         REQUIRE(live(pool, row[i]), "row %d index %d: page id %d is not live", seq, i, row[i]);
-    std::map<int32_t, int32_t> held;  // the row's references
-    for (int32_t i = 0; i < max_pages; ++i)
-        if (row[i] != -1) ++held[row[i]];
-    fka_status st = check_drops(pool, held);
+    fka_status st = count_drops(pool, row, max_pages);  // the row's references, checked
     if (st != FKA_OK) return st;
     // pages the row may refill: the partial prefix page, then the suffix pages (and any reserved
     // beyond them), each only where the row holds the page's one reference
     std::vector<int32_t> reuse, drop;
     for (int32_t i = k0; i < max_pages; ++i) {
         if (row[i] == -1) continue;
-        if (pool->ref[row[i]] == 1 && held[row[i]] == 1)
+        if (pool->ref[row[i]] == 1 && pool->pending[row[i]] == 1)
             reuse.push_back(row[i]);
         else
             drop.push_back(row[i]);
     }
+    clear_drops(pool);
     const int32_t need = n_dense - k0;
     const int32_t take = std::max(0, need - (int32_t)reuse.size());
     if (take > (int32_t)pool->free_ids.size())
         return fail(FKA_ERR_NOMEM, "%d pages needed, %d free", take, (int32_t)pool->free_ids.size());
     for (int32_t i = 0; i < k0; ++i) dense[i] = row[i];
-    std::map<int32_t, int32_t> drops;
-    for (int32_t id : drop) ++drops[id];
     for (int32_t j = 0; j < (int32_t)reuse.size(); ++j) {
         if (j < need)
             dense[k0 + j] = reuse[j];
         else
-            ++drops[reuse[j]];
+            drop.push_back(reuse[j]);
     }
-    apply_drops(pool, drops);
+    if (count_drops(pool, drop.data(), (int64_t)drop.size()) == FKA_OK) apply_drops(pool);  // held: cannot fail
     if (take > 0) take_pages(pool, take, dense + k0 + (int32_t)reuse.size());
     for (int32_t i = 0; i < max_pages; ++i) row[i] = -1;
     *from = k0 * fka::kPageSize;

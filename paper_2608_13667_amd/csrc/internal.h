@@ -234,10 +234,11 @@ struct AppendArgs {
 struct GatherArgs {
     const uint16_t *k_pool, *v_pool;
     const int32_t *page_table;
-    uint16_t *k_out, *v_out;  // [Hkv][out_len][d]
+    uint16_t *k_out, *v_out;  // [Hkv][out_len - begin][d]
     int32_t seq;
     int32_t prefix_len;
-    int32_t out_len;
+    int32_t begin;            // first logical position copied
+    int32_t out_len;          // one past the last
     int32_t max_pages;
     int32_t n_pool_pages;
     int32_t n_kv_heads;
@@ -246,7 +247,7 @@ struct GatherArgs {
 };
 
 struct ScatterArgs {
-    const uint16_t *k_src, *v_src;  // [Hkv][len][d]
+    const uint16_t *k_src, *v_src;  // positions [from, len): [Hkv][len - from][d]
     const int32_t *page_row;        // dense layout: position p at page_row[p / 16], slot p % 16
     uint16_t *k_pool, *v_pool;
     int32_t len;

@@ -342,13 +342,13 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a)
     if (threadIdx.x == 0) a.suffix_len[seq] = row + 1;
 }
 
-// grid (ceil(out_len / 16), Hkv): block copies 16 logical positions of one KV head.
+// grid (ceil((out_len - begin) / 16), Hkv): block copies 16 logical positions of one KV head.
 __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a)
 {
     const int g = blockIdx.y;
     const int cpr = a.head_dim / 8;
     for (int i = threadIdx.x; i < kPageSize * cpr; i += blockDim.x) {
-        const int pos = blockIdx.x * kPageSize + i / cpr, c = i % cpr;
+        const int pos = a.begin + blockIdx.x * kPageSize + i / cpr, c = i % cpr;
         if (pos >= a.out_len) continue;
         int pidx, slot;
         if (pos < a.prefix_len) {
@@ -360,7 +360,7 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a)
             slot = u % kPageSize;
         }
         const int page = a.page_table[(size_t)a.seq * a.max_pages + pidx];
-        const size_t dst = ((size_t)g * a.out_len + pos) * a.head_dim + 8 * c;
+        const size_t dst = ((size_t)g * (a.out_len - a.begin) + (pos - a.begin)) * a.head_dim + 8 * c;
         uint4 kv = uint4{0, 0, 0, 0}, vv = uint4{0, 0, 0, 0};
         if (page >= 0 && page < a.n_pool_pages) {
             const size_t src = (((size_t)page * a.n_kv_heads + g) * kPageSize + slot) * a.head_dim + 8 * c;
@@ -389,7 +389,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a)
     for (int i = threadIdx.x; i < kPageSize * cpr; i += blockDim.x) {
         const int slot = i / cpr, c = i % cpr, pos = pidx * kPageSize + slot;
         if (pos < a.from || pos >= a.len) continue;
-        const size_t src = ((size_t)g * a.len + pos) * a.head_dim + 8 * c;
+        const size_t src = ((size_t)g * (a.len - a.from) + (pos - a.from)) * a.head_dim + 8 * c;
         const size_t dst = (((size_t)page * a.n_kv_heads + g) * kPageSize + slot) * a.head_dim + 8 * c;
         *reinterpret_cast<uint4 *>(a.k_pool + dst) = *reinterpret_cast<const uint4 *>(a.k_src + src);
         *reinterpret_cast<uint4 *>(a.v_pool + dst) = *reinterpret_cast<const uint4 *>(a.v_src + src);
@@ -430,8 +430,8 @@ hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s)
 
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s)
 {
-    if (a.out_len <= 0) return hipSuccess;
-    gather_kernel<<<dim3((a.out_len + kPageSize - 1) / kPageSize, a.n_kv_heads), dim3(256), 0, s>>>(a);
+    if (a.out_len <= a.begin) return hipSuccess;
+    gather_kernel<<<dim3((a.out_len - a.begin + kPageSize - 1) / kPageSize, a.n_kv_heads), dim3(256), 0, s>>>(a);
     return hipGetLastError();
 }
 

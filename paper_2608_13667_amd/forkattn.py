@@ -66,6 +66,7 @@ _sig = {
     "fka_fork_step_paged": ([_vp] * 11, C.c_int),
     "fka_append_kv_paged": ([_vp] * 8, C.c_int),
     "fka_gather_paged": ([_vp, C.c_int32, _vp, _vp, _vp, C.c_int32, _vp, _vp, _vp], C.c_int),
+    "fka_gather_paged_range": ([_vp, C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp], C.c_int),
     "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
     "fka_plan_slots": ([_vp, _vp, _vp, C.c_int32, C.POINTER(C.c_int32)], C.c_int),
     "fka_partials": ([_vp] * 10, C.c_int),
@@ -228,6 +229,10 @@ class Plan:
         _check(_lib.fka_append_kv_paged(self._h, _p(k_new), _p(v_new), _p(k_pool), _p(v_pool), _p(page_table),
                                         _p(suffix_len), _stream(stream)))
 
+    def gather_paged_range(self, seq, begin, out_len, k_pool, v_pool, page_table, k_out, v_out, stream=None):
+        _check(_lib.fka_gather_paged_range(self._h, int(seq), int(begin), int(out_len), _p(k_pool), _p(v_pool),
+                                           _p(page_table), _p(k_out), _p(v_out), _stream(stream)))
+
     def gather_paged(self, seq, k_pool, v_pool, page_table, out_len, k_out, v_out, stream=None):
         _check(_lib.fka_gather_paged(self._h, int(seq), _p(k_pool), _p(v_pool), _p(page_table), int(out_len),
                                      _p(k_out), _p(v_out), _stream(stream)))
@@ -303,9 +308,9 @@ class Pool:
 
 
 def scatter_pages(k_src, v_src, frm, page_row, n_pool_pages, k_pool, v_pool, err=None, stream=None):
-    """k_src / v_src bf16 (int16 storage) [Hkv][len][d] -> pool pages of page_row (device int32)."""
-    Hkv, L, d = k_src.shape
-    _check(_lib.fka_scatter_pages(_p(k_src), _p(v_src), L, int(frm), _p(page_row), Hkv, d, int(n_pool_pages),
+    """Positions [frm, frm + n) held in k_src / v_src bf16 [Hkv][n][d] -> pool pages of page_row (device int32)."""
+    Hkv, n, d = k_src.shape
+    _check(_lib.fka_scatter_pages(_p(k_src), _p(v_src), int(frm) + n, int(frm), _p(page_row), Hkv, d, int(n_pool_pages),
                                   _p(k_pool), _p(v_pool), _p(err), _stream(stream)))
 
 

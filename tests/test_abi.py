@@ -110,6 +110,8 @@ def test_calls_with_null_plan_are_rejected(fa):
     assert fa.raw_call("fka_fork_decode_paged", n, n, n, n, n, n, n, n, n) == -1
     assert fa.raw_call("fka_append_kv", n, n, n, n, n, n, n) == -1
     assert fa.raw_call("fka_gather_paged", n, 0, n, n, n, 0, n, n, n) == -1
+    assert fa.raw_call("fka_gather_paged_range", n, 0, 0, 0, n, n, n, n, n, n) == -1
+    assert fa.raw_call("fka_scatter_pages", n, n, 4, 5, n, 1, 128, 1, n, n, n, n) == -1  # from > len
     assert fa.raw_call("fka_plan_get_info", n, n) == -1
     assert fa.raw_call("fka_plan_slots", n, n, n, 0, n) == -1
     fa.raw_call("fka_plan_destroy", n)   # NULL is ignored

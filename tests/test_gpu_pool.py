@@ -1,7 +1,7 @@
 """The K/V lifecycle of a fork on the device, through the C ABI: the snapshot scattered into pool
 pages, five sequences forked off it (fka_pool_fork), decode steps with appends into pages the pool
 reserves ahead, harvest (the four branches dropped), the main sequence promoted to the next
-snapshot (gather, fka_pool_promote, fka_scatter_pages) and a second turn forked off that.  Outputs
+snapshot (fka_pool_promote, a gather of the tail, fka_scatter_pages) and a second turn forked off that.  Outputs
 are checked against the oracle over the materialised contexts; the gathers bit-exactly."""
 import math
 
@@ -80,22 +80,24 @@ def test_fork_lifecycle_on_device(fa):
     L0 = Lp + S1
     ctx_k = np.concatenate([prefix_k, suf_k[0]], axis=1)
     ctx_v = np.concatenate([prefix_v, suf_v[0]], axis=1)
-    tmp_k = torch.empty((Hkv, L0, d), dtype=torch.bfloat16, device="cuda")
-    tmp_v = torch.empty_like(tmp_k)
-    plan1.gather_paged(0, k_pool, v_pool, dev_i32(table), L0, tmp_k, tmp_v)
+    old_table = dev_i32(table)
     dense, frm = pool.promote(table, 0, Lp, S1)
     assert frm == (Lp // 16) * 16 and len(dense) == -(-L0 // 16)
+    tmp_k = torch.empty((Hkv, L0 - frm, d), dtype=torch.bfloat16, device="cuda")
+    tmp_v = torch.empty_like(tmp_k)
+    plan1.gather_paged_range(0, frm, L0, k_pool, v_pool, old_table, tmp_k, tmp_v)  # before the scatter
     fa.scatter_pages(tmp_k, tmp_v, frm, dev_i32(dense), n_pages, k_pool, v_pool, err)
     torch.cuda.synchronize()
-    assert np.array_equal(tmp_k.cpu().view(torch.int16).numpy().view(np.uint16), ctx_k)
-    assert np.array_equal(tmp_v.cpu().view(torch.int16).numpy().view(np.uint16), ctx_v)
+    assert np.array_equal(tmp_k.cpu().view(torch.int16).numpy().view(np.uint16), ctx_k[:, frm:])
+    assert np.array_equal(tmp_v.cpu().view(torch.int16).numpy().view(np.uint16), ctx_v[:, frm:])
 
     # turn 2: five sequences forked off the promoted context
     table2 = np.full((N, max_pages), -1, np.int32)
     pool.fork(dense, table2, 0, N)
     pool.release(dense)
     plan2 = fa.Plan.paged_plan(Hq, Hkv, d, [0, N], [L0], max_pages, n_pages, S2)
-    g_k, g_v = torch.empty_like(tmp_k), torch.empty_like(tmp_v)
+    g_k = torch.empty((Hkv, L0, d), dtype=torch.bfloat16, device="cuda")
+    g_v = torch.empty_like(g_k)
     plan2.gather_paged(3, k_pool, v_pool, dev_i32(table2), L0, g_k, g_v)
     torch.cuda.synchronize()
     assert np.array_equal(g_k.cpu().view(torch.int16).numpy().view(np.uint16), ctx_k)
