@@ -155,10 +155,39 @@ def lifecycle_timing(fa, torch, w):
     per_tok = Hkv * d * 2 * 2
     moved = 4 * per_tok * (L0 - frm)  # the gather and the scatter each read and write L0 - frm tokens
     plan.close()
+    pool.release(dense)
+    pool.release(snap)
+    # branch-instruction prefill, one chunk: n tokens per branch as N * n virtual sequences in one
+    # group (token t of branch b reads b's pages with suffix length L_b + t + 1), as many as the
+    # 64 query rows per KV head allow; the prefix is read once per chunk
+    G = spec.n_q_heads // Hkv
+    n = max(1, 64 // (N * G))
+    table = np.full((N, max_pages), -1, np.int32)
+    snap2 = pool.alloc(a)
+    pool.fork(snap2, table, 0, N)
+    for b in range(N):
+        pool.reserve(table, b, Lp, min(lens[b] + n, max(lens)))
+    vt = torch.from_numpy(np.repeat(table, n, axis=0)).cuda()
+    vlen_np = np.array([min(lens[b] + t + 1, max(lens)) for b in range(N) for t in range(n)], np.int32)
+    vlen = torch.from_numpy(vlen_np).cuda()
+    pplan = fa.Plan.paged_plan(spec.n_q_heads, Hkv, d, [0, N * n], [Lp], max_pages, n_pages, max(lens))
+    q = torch.zeros((N * n, spec.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
+    o = torch.empty((N * n, spec.n_q_heads, d), device="cuda")
+    for _ in range(20):
+        pplan.decode_paged(q, pages, v_pages, vt, vlen, o, None, stream)
+    e0.record(stream)
+    for _ in range(reps * 5):
+        pplan.decode_paged(q, pages, v_pages, vt, vlen, o, None, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    pf_s = e0.elapsed_time(e1) / 1e3 / (reps * 5)
+    pf_bytes = per_tok * (Lp + sum(int(x) for x in vlen_np))  # the prefix once, each token's suffix
+    pplan.close()
     pool.close()
     ms = lambda v: float(np.median(v) * 1e6)
     return {"tokens_promoted": L0, "host_us": {k: ms(v) for k, v in host.items()},
-            "promote_device_us": dev_s * 1e6, "promote_device_gbps": moved / dev_s / 1e9}
+            "promote_device_us": dev_s * 1e6, "promote_device_gbps": moved / dev_s / 1e9,
+            "prefill_chunk": {"tokens_per_branch": n, "us": pf_s * 1e6, "kv_gbps": pf_bytes / pf_s / 1e9}}
 
 
 def main():

@@ -109,3 +109,53 @@ def test_fork_lifecycle_on_device(fa):
     assert pool.free_pages() == n_pages
     assert int(err.item()) == 0
     assert plan1.device_error() == 0 and plan2.device_error() == 0
+
+
+def test_branch_instruction_prefill(fa):
+    """Each branch appends a short instruction (n tokens, causal among themselves) over the shared
+    prefix (Sec. 3.3: the snapshot followed by a branch-specific instruction).  It runs as one paged
+    decode over N*n virtual sequences in one group -- token t of branch b is a sequence whose page
+    row is b's and whose suffix length is L_b + t + 1 -- so the prefix is read once for all N*n*G
+    query rows.  Checked against the oracle's causal definition: query (b, t) attends to the
+    prefix and to b's suffix positions [0, L_b + t]."""
+    Hq, Hkv, d, N, n = 16, 4, 128, 5, 3  # 5 * 3 virtual sequences x 4 q heads = 60 rows per KV head
+    Lp, n_pages, max_pages = 1000, 120, 70
+    scale = 1.0 / math.sqrt(d)
+    rng = np.random.default_rng(4242)
+    Lb = rng.integers(0, 41, size=N)
+    prefix_k, prefix_v = _bf16(rng, (Hkv, Lp, d)), _bf16(rng, (Hkv, Lp, d))
+    cap = int(Lb.max()) + n
+    suf_k = np.full((N, Hkv, cap, d), W.BF16_NAN, np.uint16)
+    suf_v = np.full((N, Hkv, cap, d), W.BF16_NAN, np.uint16)
+    for b in range(N):
+        suf_k[b, :, :Lb[b] + n] = _bf16(rng, (Hkv, Lb[b] + n, d))
+        suf_v[b, :, :Lb[b] + n] = _bf16(rng, (Hkv, Lb[b] + n, d))
+    pool = fa.Pool(n_pages)
+    k_pool = dev_bf16(np.full((n_pages, Hkv, 16, d), W.BF16_NAN, np.uint16))
+    v_pool = dev_bf16(np.full((n_pages, Hkv, 16, d), W.BF16_NAN, np.uint16))
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    snap = pool.alloc(-(-Lp // 16))
+    fa.scatter_pages(dev_bf16(prefix_k), dev_bf16(prefix_v), 0, dev_i32(snap), n_pages, k_pool, v_pool, err)
+    table = np.full((N, max_pages), -1, np.int32)
+    pool.fork(snap, table, 0, N)
+    pool.release(snap)
+    a = -(-Lp // 16)
+    for b in range(N):  # the branch's suffix so far and its instruction, through the suffix layout
+        pool.reserve(table, b, Lp, int(Lb[b]) + n)
+        fa.scatter_pages(dev_bf16(suf_k[b, :, :Lb[b] + n]), dev_bf16(suf_v[b, :, :Lb[b] + n]), 0,
+                         dev_i32(table[b, a:]), n_pages, k_pool, v_pool, err)
+    vt = np.repeat(table, n, axis=0)                                      # row b*n + t is branch b's
+    vlen = np.array([Lb[b] + t + 1 for b in range(N) for t in range(n)], np.int32)
+    q = _bf16(rng, (N * n, Hq, d))
+    plan = fa.Plan.paged_plan(Hq, Hkv, d, [0, N * n], [Lp], max_pages, n_pages, int(vlen.max()))
+    out = torch.empty((N * n, Hq, d), device="cuda")
+    lse = torch.empty((N * n, Hq), device="cuda")
+    plan.decode_paged(dev_bf16(q), k_pool, v_pool, dev_i32(vt), dev_i32(vlen), out, lse)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.decode_contig(q, prefix_k, prefix_v, np.repeat(suf_k, n, axis=0),
+                                        np.repeat(suf_v, n, axis=0), vlen, scale)
+    gates.assert_gates(out.cpu().numpy(), ref, what="instruction prefill")
+    gates.assert_lse(lse.cpu().numpy(), ref_lse, what="instruction prefill")
+    assert int(err.item()) == 0 and plan.device_error() == 0
+    info = plan.info()
+    assert info.n_items == Hkv + N * n * Hkv  # one prefix item per KV head: the prefix is read once
