@@ -159,3 +159,49 @@ def test_branch_instruction_prefill(fa):
     assert int(err.item()) == 0 and plan.device_error() == 0
     info = plan.info()
     assert info.n_items == Hkv + N * n * Hkv  # one prefix item per KV head: the prefix is read once
+
+
+def test_ranged_gather_bit_exact(fa):
+    """fka_gather_paged_range copies exactly logical positions [begin, end) of a sequence, across
+    the prefix / suffix boundary, the partly filled prefix page and empty ranges."""
+    w = W.make(W.CONFIGS["paged"].replace(n_tasks=3, prefix_range=(1, 400), suffix_range=(0, 90), n_kv_heads=2,
+                                          n_q_heads=8, seed=94))
+    from tests.gpu_util import paged_plan, to_dev_paged
+    plan = paged_plan(fa, w)
+    dv = to_dev_paged(w)
+    rng = np.random.default_rng(95)
+    for i in range(w.n_seqs):
+        t = i // w.spec.n_branches
+        Lp, Ls = int(w.prefix_len[t]), int(w.suffix_len[i])
+        rk, rv = oracle.gather_paged(w.k_pool, w.v_pool, w.page_table, i, Lp, Ls)
+        for begin, end in ((0, Lp + Ls), (Lp, Lp + Ls), (max(Lp - 5, 0), min(Lp + 7, Lp + Ls)),
+                           tuple(sorted(rng.integers(0, Lp + Ls + 1, size=2))), (Lp + Ls, Lp + Ls)):
+            begin, end = int(begin), int(end)
+            ko = torch.full((w.spec.n_kv_heads, max(end - begin, 1), w.spec.head_dim), 7.0, dtype=torch.bfloat16,
+                            device="cuda")
+            vo = torch.full_like(ko, 7.0)
+            plan.gather_paged_range(i, begin, end, dv["k_pool"], dv["v_pool"], dv["page_table"], ko, vo)
+            torch.cuda.synchronize()
+            n = end - begin
+            assert np.array_equal(ko.view(torch.int16).cpu().numpy().view(np.uint16)[:, :n], rk[:, begin:end])
+            assert np.array_equal(vo.view(torch.int16).cpu().numpy().view(np.uint16)[:, :n], rv[:, begin:end])
+    assert plan.device_error() == 0
+
+
+def test_scatter_skips_and_flags_bad_page_ids(fa):
+    """A page id outside the pool is not written: its positions are skipped, bit 4 is raised in the
+    error word, and the valid pages still receive their positions."""
+    Hkv, d, n_pages = 2, 64, 6
+    rng = np.random.default_rng(96)
+    src_k, src_v = _bf16(rng, (Hkv, 40, d)), _bf16(rng, (Hkv, 40, d))
+    k_pool = dev_bf16(np.full((n_pages, Hkv, 16, d), W.BF16_NAN, np.uint16))
+    v_pool = dev_bf16(np.full((n_pages, Hkv, 16, d), W.BF16_NAN, np.uint16))
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    row = np.array([4, n_pages + 3, 1], np.int32)  # positions 16..31 have no valid page
+    fa.scatter_pages(dev_bf16(src_k), dev_bf16(src_v), 0, dev_i32(row), n_pages, k_pool, v_pool, err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 4
+    kp = k_pool.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(kp[4], src_k[:, 0:16])
+    assert np.array_equal(kp[1, :, :8], src_k[:, 32:40])
+    assert np.all(kp[1, :, 8:] == W.BF16_NAN) and np.all(kp[[0, 2, 3, 5]] == W.BF16_NAN)
