@@ -30,13 +30,8 @@
  *     fka_plan_device_error (reads the device error word).
  *   - A plan owns a workspace for partial results, so it may be used by one
  *     stream at a time.  Plans are independent of each other.
- *   - A plan also caches the work schedule: each decode or step builds, on the
- *     device, the schedule of the next launch for the suffix lengths it expects
- *     that launch to see, keyed by those lengths.  A launch whose lengths match
- *     the key skips building its schedule; any other lengths are equally valid
- *     (the schedule is then built in the launch).  Calls on one plan must be
- *     ordered on one stream (as above), so each launch sees the previous one's
- *     cache.
+ *   - Every launch builds its work schedule on the device from the suffix lengths
+ *     it finds there, so the lengths may change freely between calls.
  *   - Arguments are validated on the host before anything is launched; on an
  *     error nothing is enqueued, the call returns a negative fka_status and
  *     fka_last_error() describes it.  Values that live on the device (suffix
@@ -79,9 +74,9 @@ typedef struct {
     float softmax_scale; /* scores are scale * q.k; 0 selects 1 / sqrt(head_dim) */
 } fka_heads;
 
-/* Opaque plan: the static part of the work schedule (prefix items), the grid, and
- * the workspace for partial (o, lse) results.  Built once per fork (the prefix
- * length is fixed at the fork instant), reused for every decode step. */
+/* Opaque plan: the static part of the work schedule (the prefix-sharing units), the
+ * grid, and the workspace for partial (o, lse) results.  Built once per fork (the
+ * prefix length is fixed at the fork instant), reused for every decode step. */
 typedef struct fka_plan fka_plan;
 
 /* ---------------------------------------------------------------- contiguous KV */
@@ -97,13 +92,16 @@ typedef struct {
                                0: naive baseline, every branch re-reads the prefix on its own */
     int32_t rounds;         /* 0 = automatic; k in [1, 64] = spread the keys over at least k
                                rounds of the resident waves (more, smaller partial results) */
+    int32_t blocks;         /* 0 = automatic (enough blocks for the keys at max_suffix_len, at most
+                               those resident at once); k >= 1 = k blocks per round (capped at
+                               the resident ones) */
 } fka_contig_desc;
 
 /* Build a plan for the contiguous layout.  Allocates device memory (schedule
  * tables, workspace, error flag) on the current device.  *out receives the plan,
  * owned by the caller until fka_plan_destroy.  Errors: FKA_ERR_INVALID_ARG (null
  * pointer, non-positive sizes, Hq % Hkv != 0, max_suffix_len > suffix_cap, rounds
- * outside [0, 64]), FKA_ERR_UNSUPPORTED (head_dim not 64/128, more than 64 rows N*G
+ * outside [0, 64], blocks < 0), FKA_ERR_UNSUPPORTED (head_dim not 64/128, more than 64 rows N*G
  * per KV head, more than 512 sequences), FKA_ERR_NOMEM, FKA_ERR_HIP. */
 fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc *desc, fka_plan **out);
 
@@ -157,6 +155,7 @@ typedef struct {
     int32_t max_suffix_len;    /* upper bound on suffix_len[i] over the plan's lifetime */
     int32_t share_prefix;      /* 1 fork-aware, 0 naive baseline (as in fka_contig_desc) */
     int32_t rounds;            /* as in fka_contig_desc */
+    int32_t blocks;            /* as in fka_contig_desc */
 } fka_paged_desc;
 
 /*
@@ -288,40 +287,48 @@ fka_status fka_scatter_pages(const void *k_src, const void *v_src, int32_t len, 
 
 /* -------------------------------------------------------------- stage entry points */
 
-/* Schedule geometry of a plan.  The keys are cut into items: one per (prefix unit,
- * KV head) -- a unit is a sequence group sharing its prefix, or one sequence in the
- * naive baseline -- and one per (sequence, KV head) for the suffixes.  Every decode
- * spreads the slices (32 keys) of all items evenly over n_blocks * rounds *
- * waves_per_block waves, using the suffix lengths it finds on the device; the waves of
- * one block that work on the same item share their slices and write one partial result
- * to a slot. */
+/* The first stage (Sec. 3.3: the prefix is read once for all branches) runs as one kernel
+ * over work items: one per (prefix unit, KV head) -- a unit is a sequence group sharing its
+ * prefix, or one sequence in the naive baseline.  An item's keys are the unit's prefix
+ * (scored against all the unit's query rows) followed by each of its sequences' suffixes
+ * (scored against that sequence's rows only), so the prefix and the suffix partial
+ * attentions are one launch and one hook, fka_partials.  Every decode spreads the slices
+ * (32 keys) of the items over n_blocks * rounds * waves_per_block waves: statically when
+ * the plan has one unit (each item the same share), else in proportion to each item's
+ * slices at the suffix lengths it finds on the device.  The waves of one block that work on
+ * the same item share their slices and write one partial result per row to a slot;
+ * fka_lse_merge is the second stage.  workspace_bytes is the plan's device memory. */
 typedef struct {
-    int32_t n_items;           /* prefix items + n_seqs * n_kv_heads suffix items */
-    int32_t n_prefix_items;
+    int32_t n_items;           /* units * n_kv_heads */
+    int32_t n_units;           /* prefix-sharing units */
     int32_t waves_per_block;   /* waves of one block of the partial kernel */
-    int32_t n_blocks;          /* blocks of the partial kernel resident at once */
+    int32_t n_blocks;          /* blocks of the partial kernel per round */
     int32_t rounds;            /* the kernel runs n_blocks * rounds blocks */
     int32_t n_slots;           /* partial-result slots in the workspace */
     int32_t slot_rows;         /* rows per slot: the largest item's query rows */
+    int32_t static_split;      /* 1: one unit, items split statically */
     size_t workspace_bytes;    /* device bytes held by the plan */
 } fka_plan_info;
 
 fka_status fka_plan_get_info(const fka_plan *plan, fka_plan_info *info);
 
 /* One partial result written by the first stage: rows of sequences [seq0, seq0 + nseq)
- * x the G query heads of kv_head (row r = (s - seq0) * G + h % G), attended over key
- * positions [tok_begin, tok_end) of the item's keys (prefix positions for kind 0,
- * positions in sequence seq0's suffix for kind 1).  n_tok is the item's key count. */
+ * x the G query heads of kv_head (row r = (s - seq0) * G + h % G).  Row r of sequence
+ * s attends over prefix positions [prefix_begin, prefix_end) and over the slices
+ * [suffix_begin, suffix_end) of the unit's suffix list that belong to s: the list holds,
+ * for each sequence of the unit in order, its ceil(suffix_len / 32) slices of 32 suffix
+ * positions (the last one partial).  prefix_len is the unit's prefix length. */
 typedef struct {
     int32_t slot;
-    int32_t kind;
     int32_t seq0;
     int32_t nseq;
     int32_t kv_head;
     int32_t rows;
-    int32_t tok_begin;
-    int32_t tok_end;
-    int32_t n_tok;
+    int32_t prefix_begin;
+    int32_t prefix_end;
+    int32_t suffix_begin;
+    int32_t suffix_end;
+    int32_t prefix_len;
 } fka_slot;
 
 /* The slots a decode writes when the device holds the suffix lengths
@@ -334,15 +341,20 @@ fka_status fka_plan_slots(const fka_plan *plan, const int32_t *host_suffix_len, 
 /*
  * Partial results of the first stage (test hook; the decode calls write the same
  * values to the plan's workspace).  For every slot listed by fka_plan_slots, rows
- * [0, rows) of slot `slot` hold the attention of those rows over the slot's key
- * range: o normalised, lse the natural-log log-sum-exp of the scaled scores, (0, -inf)
- * for a range without keys.  Other slots and rows are left unwritten.
+ * [0, rows) of slot `slot` hold the attention of those rows over the slot's keys:
+ * o normalised, lse the natural-log log-sum-exp of the scaled scores, (0, -inf)
+ * for a row without keys there.  Other slots and rows are left unwritten.
  *   part_o   fp32 [n_slots][slot_rows][d]
  *   part_lse fp32 [n_slots][slot_rows]
  */
 fka_status fka_partials(const fka_plan *plan, const void *q, const void *prefix_k, const void *prefix_v,
                         const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *part_o,
                         float *part_lse, void *stream);
+
+/* As fka_partials for a paged plan (arguments as in fka_fork_decode_paged). */
+fka_status fka_partials_paged(const fka_plan *plan, const void *q, const void *k_pool, const void *v_pool,
+                              const int32_t *page_table, const int32_t *suffix_len, float *part_o,
+                              float *part_lse, void *stream);
 
 /*
  * Log-sum-exp merge of partial softmax results (combine attention over disjoint
@@ -358,9 +370,9 @@ fka_status fka_lse_merge(int32_t rows, int32_t n_parts, int32_t head_dim, const 
 /* Read and clear the plan's device error flag (synchronises with the device):
  * *flags receives a bit mask: 1 = a suffix length above max_suffix_len was
  * clamped, 2 = an append found no room (length at max_suffix_len or no page),
- * 4 = a page id outside the page table bounds was met, 8 = a schedule record
- * in the plan's workspace pointed outside it (only if that memory was written
- * from outside the library; the record was not followed). */
+ * 4 = a page id outside the page table bounds was met, 8 = a merge record in
+ * the plan's workspace pointed outside it (only if that memory was written from
+ * outside the library; the record was not followed). */
 fka_status fka_plan_device_error(const fka_plan *plan, int32_t *flags);
 
 /* Release a plan and its device memory.  NULL is ignored. */

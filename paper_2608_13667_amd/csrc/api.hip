@@ -26,31 +26,25 @@ struct fka_plan {
     int32_t n_groups = 0, page_size = 0, max_pages = 0, n_pool_pages = 0;
     std::vector<int32_t> group_start, group_prefix_len;
     // schedule (see the work schedule in internal.h)
-    std::vector<fka::PrefixItem> pre;      // static prefix items, unit-major, KV head minor
+    std::vector<fka::UnitRec> units;       // prefix-sharing units in sequence order
     std::vector<int32_t> seq_prefix_len;   // prefix length of s's unit
-    int32_t pre_slices = 0, pre_nonempty = 0;
-    int32_t n_items = 0;       // prefix items + n_seqs * Hkv suffix items
+    int32_t ps_total = 0;      // prefix slices of all units
+    bool static_split = false; // one unit: items split statically
+    int32_t n_items = 0;       // units * Hkv
     int32_t slot_rows = 0;     // rows of the largest item
     int32_t row_tiles = 1;
     int32_t waves = 0;         // waves per block of the partial kernel
-    int32_t n_blocks = 0;      // blocks resident at once on the device
+    int32_t n_blocks = 0;      // blocks launched per round (at most those resident at once)
     int32_t rounds = 1;        // launches n_blocks * rounds blocks
     int32_t n_slots = 0;       // partial-result slots in the workspace
     size_t workspace_bytes = 0;
     int device = 0;
-    // half of the schedule cache the next launch reads; a decode flips it after launching the
-    // merge that builds the other half
-    mutable uint32_t cache_cur = 0;
     // device memory (one allocation, carved)
     void *mem = nullptr;
-    fka::PrefixItem *d_pre = nullptr;
+    fka::UnitRec *d_units = nullptr;
     int32_t *d_seq_prefix_len = nullptr;
     int32_t *err = nullptr;
-    int32_t *d_tab[2][2] = {};     // [half][candidate] (see the schedule cache in internal.h)
-    int32_t *d_key[2][2] = {};
-    int32_t *d_rowrec[2][2] = {};
-    int32_t *d_rowrec_live = nullptr;
-    int32_t *d_sel = nullptr;
+    int32_t *d_rowrec = nullptr;
     int32_t *d_lens = nullptr;
     float *part_o = nullptr;
     float *part_lse = nullptr;
@@ -124,18 +118,25 @@ void init_heads(fka_plan *p, const fka_heads *h)
     p->scale = h->softmax_scale > 0.f ? h->softmax_scale : 1.0f / std::sqrt((float)h->head_dim);
 }
 
-fka_status check_rounds(int32_t rounds)
+fka_status check_grid(int32_t rounds, int32_t blocks)
 {
     REQUIRE(rounds >= 0 && rounds <= 64, "rounds (%d) must be in [0, 64]", rounds);
+    REQUIRE(blocks >= 0, "blocks (%d) must be >= 0", blocks);
     return FKA_OK;
 }
 
+// Slices of work a wave takes at the least before the automatic grid uses another block:
+// a small fork then runs on a few blocks (fewer partials for the merge) instead of the whole
+// device.
+constexpr int32_t kMinSlicesPerWave = 2;
+
 // Prefix units in order: unit u covers sequences [seq0, seq0 + nseq) that share a prefix of
-// n_tok tokens.  Builds the static prefix items (one per unit and KV head), the
-// per-sequence tables, the slot geometry, the grid and the round count.
-fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>> &units, int32_t rounds_req)
+// n_tok tokens.  Builds the unit table, the per-sequence prefix lengths, the slot geometry,
+// the grid and the round count.
+fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>> &units, int32_t rounds_req,
+                          int32_t blocks_req)
 {
-    p->pre.clear();
+    p->units.clear();
     p->seq_prefix_len.assign(p->n_seqs, 0);
     // token counts stay far enough below 2^31 that ceil(tokens / kSlice) cannot overflow
     constexpr int32_t kMaxTokens = 1 << 30;
@@ -144,32 +145,27 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     for (const auto &u : units)
         if (u[2] > kMaxTokens) return fail(FKA_ERR_UNSUPPORTED, "prefix of %d tokens is too long (limit %d)", u[2], kMaxTokens);
     int64_t c = 0;
-    int32_t k = 0, max_nseq = 1;
+    int32_t max_nseq = 1;
+    int64_t est = 0;  // slices per KV head with every suffix at max_suffix_len
     for (size_t u = 0; u < units.size(); ++u) {
         const int32_t seq0 = units[u][0], nseq = units[u][1], n_tok = units[u][2];
         max_nseq = std::max(max_nseq, nseq);
         for (int32_t i = seq0; i < seq0 + nseq; ++i) p->seq_prefix_len[i] = n_tok;
-        for (int32_t g = 0; g < p->Hkv; ++g) {
-            fka::PrefixItem it{};
-            it.seq0 = seq0;
-            it.nseq = nseq;
-            it.kv_head = g;
-            it.n_tok = n_tok;
-            it.c0 = (int32_t)c;
-            it.k0 = k;
-            p->pre.push_back(it);
-            const int32_t sz = fka::slices_of(n_tok);
-            c += sz;
-            k += sz > 0;
-        }
+        fka::UnitRec r{};
+        r.seq0 = seq0;
+        r.nseq = nseq;
+        r.plen = n_tok;
+        r.ps_before = (int32_t)c;
+        p->units.push_back(r);
+        c += fka::slices_of(n_tok);
+        est += fka::slices_of(n_tok) + (int64_t)nseq * fka::slices_of(p->max_suffix_len);
     }
-    // the schedule's total slices (prefix plus every suffix at its longest) stay in int32
-    const int64_t suffix_slices = (int64_t)p->n_seqs * p->Hkv * ((int64_t)p->max_suffix_len + fka::kSlice - 1) / fka::kSlice;
-    if (c + suffix_slices > (int64_t)1 << 30)
-        return fail(FKA_ERR_UNSUPPORTED, "prefix and suffixes of %lld slices are too long", (long long)(c + suffix_slices));
-    p->pre_slices = (int32_t)c;
-    p->pre_nonempty = k;
-    p->n_items = (int32_t)p->pre.size() + p->n_seqs * p->Hkv;
+    // the schedule's total slices (every item at its longest, over all KV heads) stay in int32
+    if (est * p->Hkv > (int64_t)1 << 30)
+        return fail(FKA_ERR_UNSUPPORTED, "prefix and suffixes of %lld slices are too long", (long long)(est * p->Hkv));
+    p->ps_total = (int32_t)c;
+    p->static_split = units.size() == 1;
+    p->n_items = (int32_t)units.size() * p->Hkv;
     p->slot_rows = max_nseq * p->G;
     p->row_tiles = ceil_div(p->slot_rows, 16);
 
@@ -181,7 +177,16 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     const int per_cu = fka::partials_blocks_per_cu(p->d, p->row_tiles, p->paged);
     p->waves = fka::partials_waves_per_block(p->d, p->row_tiles, p->paged);
     if (per_cu <= 0 || p->waves <= 0) return fail(FKA_ERR_HIP, "occupancy query of the partial kernel failed");
-    p->n_blocks = cus * per_cu;
+    const int32_t resident = cus * per_cu;
+    if (blocks_req > 0) {
+        p->n_blocks = std::min(blocks_req, resident);
+    } else {
+        // enough blocks that every wave has kMinSlicesPerWave slices at the longest suffixes,
+        // a multiple of Hkv (so that items start on block boundaries), at most the resident ones
+        int64_t b = (est * p->Hkv + (int64_t)p->waves * kMinSlicesPerWave - 1) / ((int64_t)p->waves * kMinSlicesPerWave);
+        b = (b + p->Hkv - 1) / p->Hkv * p->Hkv;
+        p->n_blocks = (int32_t)std::max<int64_t>(1, std::min<int64_t>(b, resident));
+    }
     // at least two workers per item, so that A = workers - non-empty items stays >= half
     const int32_t per_round = p->n_blocks * p->waves;
     const int32_t need = ceil_div(2 * (int64_t)p->n_items, per_round);
@@ -190,25 +195,21 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     return FKA_OK;
 }
 
-// Allocate device memory for the static tables, the error flag, the schedule cache and the
-// partial-result workspace, and upload the tables.
+// Allocate device memory for the unit table, the error flag, the merge records, the lengths
+// and the partial-result workspace, and upload the tables.
 fka_status finish_plan(fka_plan *p)
 {
     hipError_t e;
     auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-    const size_t workers = (size_t)p->n_blocks * p->rounds * p->waves;
     const size_t rows = (size_t)p->n_seqs * p->Hq;
-    const size_t b_pre = up(std::max<size_t>(1, p->pre.size()) * sizeof(fka::PrefixItem));
+    const size_t b_units = up(std::max<size_t>(1, p->units.size()) * sizeof(fka::UnitRec));
     const size_t b_seq = up((size_t)p->n_seqs * sizeof(int32_t));
     const size_t b_err = 256;
-    const size_t b_tab = up(workers * fka::kTabWords * sizeof(int32_t));
     const size_t b_rec = up(rows * fka::kRowRec * sizeof(int32_t));
     const size_t b_po = up((size_t)p->n_slots * p->slot_rows * p->d * sizeof(float));
     const size_t b_pl = up((size_t)p->n_slots * p->slot_rows * sizeof(float));
-    // err, then the cache (tables and records zeroed, keys all -1: no cached schedule yet)
-    const size_t b_zero = b_err + 4 * b_tab + 5 * b_rec + 2 * b_seq;
-    const size_t b_keys = 4 * b_seq;
-    const size_t total = b_pre + b_seq + b_zero + b_keys + b_po + b_pl;
+    const size_t b_zero = b_err + b_rec + b_seq;  // err, records, lengths: zeroed
+    const size_t total = b_units + b_seq + b_zero + b_po + b_pl;
     e = hipMalloc(&p->mem, total);
     if (e != hipSuccess) {
         p->mem = nullptr;
@@ -216,67 +217,44 @@ fka_status finish_plan(fka_plan *p)
         return fail(FKA_ERR_NOMEM, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
     }
     char *m = static_cast<char *>(p->mem);
-    p->d_pre = reinterpret_cast<fka::PrefixItem *>(m);
-    m += b_pre;
+    p->d_units = reinterpret_cast<fka::UnitRec *>(m);
+    m += b_units;
     p->d_seq_prefix_len = reinterpret_cast<int32_t *>(m);
     m += b_seq;
     char *zero = m;
     p->err = reinterpret_cast<int32_t *>(m);
     m += b_err;
-    for (int h = 0; h < 2; ++h)
-        for (int c = 0; c < 2; ++c) {
-            p->d_tab[h][c] = reinterpret_cast<int32_t *>(m);
-            m += b_tab;
-            p->d_rowrec[h][c] = reinterpret_cast<int32_t *>(m);
-            m += b_rec;
-        }
-    p->d_rowrec_live = reinterpret_cast<int32_t *>(m);
+    p->d_rowrec = reinterpret_cast<int32_t *>(m);
     m += b_rec;
     p->d_lens = reinterpret_cast<int32_t *>(m);
     m += b_seq;
-    p->d_sel = reinterpret_cast<int32_t *>(m);
-    m += b_seq;
-    char *keys = m;
-    for (int h = 0; h < 2; ++h)
-        for (int c = 0; c < 2; ++c) {
-            p->d_key[h][c] = reinterpret_cast<int32_t *>(m);
-            m += b_seq;
-        }
     p->part_o = reinterpret_cast<float *>(m);
     m += b_po;
     p->part_lse = reinterpret_cast<float *>(m);
     p->workspace_bytes = total;
-    p->cache_cur = 0;
     auto put = [&](void *dst, const void *src, size_t bytes, const char *what) -> fka_status {
         if (bytes == 0) return FKA_OK;
         const hipError_t r = hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice);
         return r == hipSuccess ? FKA_OK : hip_fail(r, what);
     };
     fka_status st;
-    if ((st = put(p->d_pre, p->pre.data(), p->pre.size() * sizeof(fka::PrefixItem), "hipMemcpy(prefix items)")) != FKA_OK ||
+    if ((st = put(p->d_units, p->units.data(), p->units.size() * sizeof(fka::UnitRec), "hipMemcpy(units)")) != FKA_OK ||
         (st = put(p->d_seq_prefix_len, p->seq_prefix_len.data(), p->seq_prefix_len.size() * sizeof(int32_t),
                   "hipMemcpy(sequence tables)")) != FKA_OK)
         return st;
-    if ((e = hipMemset(zero, 0, b_zero)) != hipSuccess) return hip_fail(e, "hipMemset(flags and cache)");
-    if ((e = hipMemset(keys, 0xff, b_keys)) != hipSuccess) return hip_fail(e, "hipMemset(cache keys)");
+    if ((e = hipMemset(zero, 0, b_zero)) != hipSuccess) return hip_fail(e, "hipMemset(flags and records)");
     return FKA_OK;
 }
 
 fka::AttnArgs attn_args(const fka_plan *p)
 {
     fka::AttnArgs a{};
-    const uint32_t c = p->cache_cur;
-    a.pre_items = p->d_pre;
-    a.n_pre = (int32_t)p->pre.size();
-    a.pre_slices = p->pre_slices;
-    a.pre_nonempty = p->pre_nonempty;
+    a.units = p->d_units;
+    a.n_units = (int32_t)p->units.size();
+    a.static_split = p->static_split ? 1 : 0;
+    a.ps_total = p->ps_total;
     a.seq_prefix_len = p->d_seq_prefix_len;
-    for (int k = 0; k < 2; ++k) {
-        a.tab[k] = p->d_tab[c][k];
-        a.key[k] = p->d_key[c][k];
-    }
-    a.rowrec_live = p->d_rowrec_live;
-    a.sel = p->d_sel;
+    a.rowrec = p->d_rowrec;
     a.lens = p->d_lens;
     a.max_suffix_len = p->max_suffix_len;
     a.n_seqs = p->n_seqs;
@@ -289,7 +267,9 @@ fka::AttnArgs attn_args(const fka_plan *p)
     a.slot_rows = p->slot_rows;
     a.n_slots = p->n_slots;
     a.err = p->err;
-    a.prefix_len = p->prefix_len;
+    // contiguous: the prefix buffer's length; a static split also takes its one unit's prefix
+    // length from here (paged with one group)
+    a.prefix_len = p->paged ? p->units[0].plen : p->prefix_len;
     a.suffix_cap = p->suffix_cap;
     a.max_pages = p->max_pages;
     a.n_pool_pages = p->n_pool_pages;
@@ -300,7 +280,6 @@ fka::AttnArgs attn_args(const fka_plan *p)
 fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *out, float *out_lse)
 {
     fka::MergeArgs m{};
-    const uint32_t c = p->cache_cur;
     m.part_o = p->part_o;
     m.part_lse = p->part_lse;
     m.out = out;
@@ -308,23 +287,12 @@ fka::MergeArgs merge_args(const fka_plan *p, const int32_t *suffix_len, float *o
     m.rows = p->n_seqs * p->Hq;
     m.n_q_heads = p->Hq;
     m.n_parts = 0;
-    m.rowrec[0] = p->d_rowrec[c][0];
-    m.rowrec[1] = p->d_rowrec[c][1];
-    m.rowrec[2] = p->d_rowrec_live;
-    m.sel = p->d_sel;
+    m.plan = 1;
+    m.static_split = p->static_split ? 1 : 0;
+    m.rowrec = p->d_rowrec;
     m.lens = p->d_lens;
     m.slot_rows = p->slot_rows;
     m.n_slots = p->n_slots;
-    for (int k = 0; k < 2; ++k) {
-        m.tab_next[k] = p->d_tab[c ^ 1][k];
-        m.key_next[k] = p->d_key[c ^ 1][k];
-        m.rowrec_next[k] = p->d_rowrec[c ^ 1][k];
-    }
-    m.pre_items = p->d_pre;
-    m.n_pre = (int32_t)p->pre.size();
-    m.pre_slices = p->pre_slices;
-    m.pre_nonempty = p->pre_nonempty;
-    m.n_seqs = p->n_seqs;
     m.waves = p->waves;
     m.n_workers = p->n_blocks * p->rounds * p->waves;
     m.suffix_len = const_cast<int32_t *>(suffix_len);  // only a fused step writes it
@@ -348,7 +316,6 @@ fka_status run_decode(const fka_plan *p, const fka::AttnArgs &a, const int32_t *
     if (e != hipSuccess) return hip_fail(e, "partials kernel launch");
     e = fka::launch_merge(step ? *step : merge_args(p, suffix_len, out, out_lse), p->d, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
-    p->cache_cur ^= 1u;  // the merge builds the other buffer for the next launch
     return ok();
 }
 
@@ -373,7 +340,7 @@ fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc 
     REQUIRE(desc->max_suffix_len >= 0 && desc->max_suffix_len <= desc->suffix_cap,
             "max_suffix_len (%d) must be in [0, suffix_cap=%d]", desc->max_suffix_len, desc->suffix_cap);
     REQUIRE(desc->share_prefix == 0 || desc->share_prefix == 1, "share_prefix must be 0 or 1");
-    if ((st = check_rounds(desc->rounds)) != FKA_OK) return st;
+    if ((st = check_grid(desc->rounds, desc->blocks)) != FKA_OK) return st;
     if (desc->n_branches > fka::kMaxSeqs)
         return fail(FKA_ERR_UNSUPPORTED, "%d sequences exceed the limit of %d", desc->n_branches, fka::kMaxSeqs);
     const int G = heads->n_q_heads / heads->n_kv_heads;
@@ -394,7 +361,7 @@ fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc 
         units.push_back({0, desc->n_branches, desc->prefix_len});
     else
         for (int b = 0; b < desc->n_branches; ++b) units.push_back({b, 1, desc->prefix_len});
-    if ((st = build_schedule(p, units, desc->rounds)) != FKA_OK || (st = finish_plan(p)) != FKA_OK) {
+    if ((st = build_schedule(p, units, desc->rounds, desc->blocks)) != FKA_OK || (st = finish_plan(p)) != FKA_OK) {
         fka_plan_destroy(p);
         return st;
     }
@@ -417,7 +384,7 @@ fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *d
     REQUIRE(desc->n_pool_pages >= 1, "n_pool_pages must be >= 1");
     REQUIRE(desc->max_suffix_len >= 0, "max_suffix_len must be >= 0");
     REQUIRE(desc->share_prefix == 0 || desc->share_prefix == 1, "share_prefix must be 0 or 1");
-    if ((st = check_rounds(desc->rounds)) != FKA_OK) return st;
+    if ((st = check_grid(desc->rounds, desc->blocks)) != FKA_OK) return st;
     REQUIRE(host_group_start[0] == 0 && host_group_start[desc->n_groups] == desc->n_seqs,
             "group_start must begin at 0 and end at n_seqs");
     const int G = heads->n_q_heads / heads->n_kv_heads;
@@ -459,7 +426,7 @@ fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *d
         else
             for (int i = s0; i < s1; ++i) units.push_back({i, 1, lp});
     }
-    if ((st = build_schedule(p, units, desc->rounds)) != FKA_OK || (st = finish_plan(p)) != FKA_OK) {
+    if ((st = build_schedule(p, units, desc->rounds, desc->blocks)) != FKA_OK || (st = finish_plan(p)) != FKA_OK) {
         fka_plan_destroy(p);
         return st;
     }
@@ -471,12 +438,13 @@ fka_status fka_plan_get_info(const fka_plan *p, fka_plan_info *info)
 {
     REQUIRE(p != nullptr && info != nullptr, "null argument");
     info->n_items = p->n_items;
-    info->n_prefix_items = (int32_t)p->pre.size();
+    info->n_units = (int32_t)p->units.size();
     info->waves_per_block = p->waves;
     info->n_blocks = p->n_blocks;
     info->rounds = p->rounds;
     info->n_slots = p->n_slots;
     info->slot_rows = p->slot_rows;
+    info->static_split = p->static_split ? 1 : 0;
     info->workspace_bytes = p->workspace_bytes;
     return ok();
 }
@@ -486,58 +454,54 @@ fka_status fka_plan_slots(const fka_plan *p, const int32_t *host_suffix_len, fka
 {
     REQUIRE(p != nullptr && host_suffix_len != nullptr && n_slots != nullptr, "null argument");
     REQUIRE(capacity >= 0 && (capacity == 0 || slots != nullptr), "slots is null");
-    const int N = p->n_seqs, Hkv = p->Hkv;
-    std::vector<int32_t> len(N), cs(N), ne(N);
-    int64_t c = 0, k = 0;
+    const int N = p->n_seqs, Hkv = p->Hkv, NW = p->waves;
+    const int32_t NV = p->n_blocks * p->rounds * NW;
+    // per sequence: clamped length; exclusive scan of slice counts (as the kernel's tables)
+    std::vector<int32_t> cs(N + 1, 0);
     for (int s = 0; s < N; ++s) {
-        len[s] = std::min(std::max(host_suffix_len[s], 0), p->max_suffix_len);
-        cs[s] = (int32_t)c;
-        ne[s] = (int32_t)k;
-        c += (int64_t)fka::slices_of(len[s]) * Hkv;
-        k += len[s] > 0 ? Hkv : 0;
+        const int32_t len = std::min(std::max(host_suffix_len[s], 0), p->max_suffix_len);
+        cs[s + 1] = cs[s] + fka::slices_of(len);
     }
-    const int64_t T = p->pre_slices + c, NNE = p->pre_nonempty + k;
-    const int64_t NV = (int64_t)p->n_blocks * p->rounds * p->waves;
+    const int n_units = (int)p->units.size();
+    std::vector<int32_t> ne(n_units + 1, 0);
+    for (int u = 0; u < n_units; ++u) {
+        const fka::UnitRec &r = p->units[u];
+        ne[u + 1] = ne[u] + ((fka::slices_of(r.plen) + cs[r.seq0 + r.nseq] - cs[r.seq0]) > 0 ? 1 : 0);
+    }
+    const int64_t T = (int64_t)Hkv * (p->ps_total + cs[N]), NNE = (int64_t)Hkv * ne[n_units];
     const uint64_t R = T > 0 ? fka::sched_ratio(NV - NNE, T) : 0;
     int32_t count = 0;
-    const int n_pre = (int)p->pre.size();
-    for (int i = 0; T > 0 && i < p->n_items; ++i) {
-        fka_slot base{};
-        int32_t C, K, size;
-        if (i < n_pre) {
-            const fka::PrefixItem &it = p->pre[i];
-            size = fka::slices_of(it.n_tok);
-            C = it.c0;
-            K = it.k0;
-            base.kind = 0;
-            base.seq0 = it.seq0;
-            base.nseq = it.nseq;
-            base.kv_head = it.kv_head;
-            base.n_tok = it.n_tok;
+    for (int i = 0; i < p->n_items; ++i) {
+        const int u = i / Hkv, g = i % Hkv;
+        const fka::UnitRec &r = p->units[u];
+        const int32_t P = fka::slices_of(r.plen), S = cs[r.seq0 + r.nseq] - cs[r.seq0];
+        int32_t ws0, ws1;
+        if (p->static_split) {
+            ws0 = fka::static_start(g, NV, Hkv);
+            ws1 = fka::static_start(g + 1, NV, Hkv);
         } else {
-            const int j = i - n_pre, s = j / Hkv, g = j % Hkv;
-            size = fka::slices_of(len[s]);
-            C = p->pre_slices + cs[s] + g * size;
-            K = p->pre_nonempty + ne[s] + (size > 0 ? g : 0);
-            base.kind = 1;
-            base.seq0 = s;
-            base.nseq = 1;
-            base.kv_head = g;
-            base.n_tok = len[s];
+            if (P + S == 0 || T == 0) continue;
+            const int64_t C = (int64_t)Hkv * (r.ps_before + cs[r.seq0]) + (int64_t)g * (P + S);
+            const int64_t K = (int64_t)Hkv * ne[u] + g;
+            ws0 = fka::worker_start(C, K, R);
+            ws1 = fka::worker_start(C + P + S, K + 1, R);
         }
-        if (size == 0) continue;
-        const int32_t ws0 = fka::worker_start(C, K, R), ws1 = fka::worker_start(C + size, K + 1, R);
-        for (int32_t vb = ws0 / p->waves; vb <= (ws1 - 1) / p->waves; ++vb) {
-            const int32_t lo = std::max(ws0, vb * p->waves), hi = std::min(ws1, (vb + 1) * p->waves);
-            int32_t a0, a1, b0, b1;
-            fka::worker_range(lo - ws0, ws1 - ws0, size, a0, a1);
-            fka::worker_range(hi - 1 - ws0, ws1 - ws0, size, b0, b1);
+        if (ws1 <= ws0) continue;
+        const int32_t W = ws1 - ws0;
+        for (int32_t vb = ws0 / NW; vb <= (ws1 - 1) / NW; ++vb) {
+            const int32_t lo = std::max(ws0, vb * NW) - ws0, hi = std::min(ws1, (vb + 1) * NW) - ws0;
             if (count < capacity) {
-                fka_slot sl = base;
+                fka_slot sl{};
                 sl.slot = vb + i;
-                sl.rows = base.nseq * p->G;
-                sl.tok_begin = std::min(a0 * fka::kSlice, base.n_tok);
-                sl.tok_end = std::min(b1 * fka::kSlice, base.n_tok);
+                sl.seq0 = r.seq0;
+                sl.nseq = r.nseq;
+                sl.kv_head = g;
+                sl.rows = r.nseq * p->G;
+                sl.prefix_begin = std::min(fka::pre_split(lo, W, P) * fka::kSlice, r.plen);
+                sl.prefix_end = std::min(fka::pre_split(hi, W, P) * fka::kSlice, r.plen);
+                sl.suffix_begin = fka::suf_split(lo, W, P, S);
+                sl.suffix_end = fka::suf_split(hi, W, P, S);
+                sl.prefix_len = r.plen;
                 slots[count] = sl;
             }
             ++count;
@@ -577,7 +541,7 @@ fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, 
                         float *part_lse, void *stream)
 {
     REQUIRE(p != nullptr, "plan is null");
-    REQUIRE(!p->paged, "fka_partials takes a contiguous plan");
+    REQUIRE(!p->paged, "plan is paged: use fka_partials_paged");
     REQUIRE_PTR16(q);
     if (p->prefix_len > 0) {
         REQUIRE_PTR16(prefix_k);
@@ -594,6 +558,32 @@ fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, 
     a.prefix_v = static_cast<const uint16_t *>(prefix_v);
     a.suffix_k = static_cast<const uint16_t *>(suffix_k);
     a.suffix_v = static_cast<const uint16_t *>(suffix_v);
+    a.suffix_len = suffix_len;
+    a.part_o = part_o;
+    a.part_lse = part_lse;
+    hipError_t e = fka::launch_partials(a, p->n_blocks * p->rounds, p->d, p->row_tiles, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "partials kernel launch");
+    return ok();
+}
+
+fka_status fka_partials_paged(const fka_plan *p, const void *q, const void *k_pool, const void *v_pool,
+                              const int32_t *page_table, const int32_t *suffix_len, float *part_o, float *part_lse,
+                              void *stream)
+{
+    REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(p->paged, "plan is contiguous: use fka_partials");
+    REQUIRE_PTR16(q);
+    REQUIRE_PTR16(k_pool);
+    REQUIRE_PTR16(v_pool);
+    REQUIRE(page_table != nullptr, "page_table is null");
+    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR16(part_o);
+    REQUIRE(part_lse != nullptr, "part_lse is null");
+    fka::AttnArgs a = attn_args(p);
+    a.q = static_cast<const uint16_t *>(q);
+    a.k_pool = static_cast<const uint16_t *>(k_pool);
+    a.v_pool = static_cast<const uint16_t *>(v_pool);
+    a.page_table = page_table;
     a.suffix_len = suffix_len;
     a.part_o = part_o;
     a.part_lse = part_lse;

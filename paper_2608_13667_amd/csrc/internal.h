@@ -1,4 +1,4 @@
-// Internal interface between the C ABI layer (api.hip) and the kernels (kernels.hip).
+// Internal interface between the C ABI layer (api.hip) and the kernels (kernels.hip, partials.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -15,58 +15,55 @@ constexpr int kMaxSeqs = 512;   // sequences per plan (per-sequence schedule tab
 // ---------------------------------------------------------------------------------------
 // Work schedule shared by the partial kernel, the merge kernel and the host.
 //
-// The keys are cut into items, in this fixed order:
-//   prefix items  i = u * Hkv + g            (u = prefix unit: a sequence group when the
-//                                              prefix is shared, else one sequence)
-//   suffix items  i = n_pre + s * Hkv + g    (sequence s, KV head g)
-// Item i holds size_i = ceil(tokens_i / kSlice) slices; C_i is the number of slices of the
-// items before it and K_i the number of non-empty items before it.  Suffix sizes follow
-// the suffix lengths on the device, so the schedule is rebuilt by every launch.
+// A unit is a run of sequences that share one prefix (the whole fork when the prefix is
+// shared, else a single sequence).  Item i = u * Hkv + g holds every key of unit u and KV head
+// g: first the unit's prefix slices (read by all the unit's query rows, nseq * G of them, so
+// each prefix byte is fetched once for all branches), then the suffix slices of the unit's
+// sequences in order (each read by its own sequence's G rows only).  With P prefix slices and
+// S suffix slices (S follows the suffix lengths on the device), the item's work list has
+// P + S slices.
 //
-// The launch has NV workers (waves), NV = waves per block x virtual blocks.  With
-// T = total slices, A = NV - (non-empty items) and the 32.32 fixed-point ratio
-// R = floor(A * 2^32 / T), item i owns workers [WS(i), WS(i+1)) with
-// WS(i) = floor(C_i * R / 2^32) + K_i: an empty item owns none, every other item at least
-// one and about size_i * A / T of them; the items end at WS(n_items), NV - 1 or NV, and a
-// worker past that end has no work.  Worker j of an item with w workers scores slices
-// [floor(j*size/w), floor((j+1)*size/w)).
+// The launch has NV workers (waves), NV = waves per block x virtual blocks.
+//   * One unit (static split): item g owns workers [floor(g NV / Hkv), floor((g+1) NV / Hkv)).
+//     All items have the same keys, so this is balanced whatever the lengths, and the merge
+//     finds every row's partials without reading anything.
+//   * Several units (proportional split): with T = total slices, A = NV - (non-empty items)
+//     and the 32.32 fixed-point ratio R = floor(A * 2^32 / T), item i owns workers
+//     [WS(i), WS(i+1)), WS(i) = floor(C_i * R / 2^32) + K_i, where C_i counts the slices of the
+//     items before i and K_i the non-empty items before it: an empty item owns none, every
+//     other item at least one and about size_i * A / T of them.
+// Within an item of W workers, worker j owns prefix slices [pre_split(j), pre_split(j+1)) and
+// suffix slices [suf_split(j), suf_split(j+1)): the prefix part of each worker depends only on
+// the plan (so the first prefix loads need no lengths), and when S >= W the suffix part makes
+// each worker's total floor((j+1)(P+S)/W) - floor(j(P+S)/W), the balance of one joint split.
 //
-// The waves of block vb are workers [vb*NW, (vb+1)*NW).  They combine their
-// results per item, and the partial of (vb, item i) goes to slot vb + i: along the
-// order of work each step advances vb, i or both, so slots are distinct and fewer than
-// (blocks + items).  The merge reads, for an item, the slots of every block that owns
-// one of its workers; each of those blocks writes its slot, empty or not.
+// The waves of block vb are workers [vb*NW, (vb+1)*NW).  Those on the same item form a group:
+// its prefix range and suffix range are the unions of its workers' ranges, and its waves deal
+// the slices of [prefix range ; suffix range] in turn.  The group writes one partial (o, lse)
+// per row of the item to slot vb + i: along the order of work each step advances vb, i or
+// both, so slots are distinct and fewer than (blocks + items).  Every block of a static split
+// writes its slot, empty or not; under a proportional split the block holding an item's first
+// worker records, for each row of the item, where its partials start and how many there are.
 // ---------------------------------------------------------------------------------------
-struct PrefixItem {  // eight int32 fields, read field by field on the device
-    int32_t seq0;     // first sequence of the item's rows
-    int32_t nseq;     // sequences of the item's rows (rows = nseq * G)
-    int32_t kv_head;
-    int32_t n_tok;    // prefix length of the unit
-    int32_t c0;       // slices of the prefix items before this one
-    int32_t k0;       // non-empty prefix items before this one
-    int32_t pad0, pad1;
+struct UnitRec {  // four int32 fields, read field by field on the device
+    int32_t seq0;       // first sequence of the unit
+    int32_t nseq;       // sequences of the unit (rows = nseq * G)
+    int32_t plen;       // prefix length of the unit
+    int32_t ps_before;  // prefix slices of the units before this one
 };
 
-// Schedule cache.  The schedule depends only on the plan and on the clamped suffix lengths.  The
-// merge kernel of each launch builds, into the other half of a ping-pong pair, the schedule for
-// two candidates of the next launch's lengths: candidate 0 = this launch's lengths (the next
-// call of a multi-layer model, or a decode without append) and, after a fused step, candidate 1
-// = the lengths after the append (the same layer's next step).  Per candidate:
-//   table  [workers][kTabWords]: what the partial kernel's placement puts in LDS for each
-//          worker (its item, the item's rows and keys, and its group in the block);
-//   key    [S]: the clamped suffix lengths the table is for (-1 at [0]: none);
-//   rowrec [S * Hq][kRowRec]: for merge row (s, h) the offset (slot * slot_rows + row within the
-//          slot) of its first prefix part and the count of prefix parts, then the same for its
-//          suffix item; parts of one item sit in consecutive slots.
-// A launch reads half `cur` (the host alternates it after each merge).  The partial kernel
-// takes the first candidate whose key equals the clamped lengths it reads; if none does, it
-// builds the schedule itself and writes its slot records to a separate live buffer.  Block 0
-// records the choice (sel: 0, 1, or 2 for the live records) and the clamped lengths (lens) for
-// the merge.  Only the merge writes a candidate, so a key always describes its table and records.
-constexpr int kTabWords = 9;
-constexpr int kRowRec = 4;
+constexpr int kRowRec = 2;  // merge record of a row under a proportional split: first part offset, count
 
 __host__ __device__ inline int32_t slices_of(int32_t tokens) { return (tokens + kSlice - 1) / kSlice; }
+
+// floor(a * b / c) for 0 <= a <= c, b >= 0, c > 0: 32-bit arithmetic whenever the product fits
+// (the common case, far cheaper on the GPU than a 64-bit division).
+__host__ __device__ inline int32_t mul_div(int32_t a, int32_t b, int32_t c)
+{
+    const uint64_t p = (uint64_t)(uint32_t)a * (uint32_t)b;
+    if (p < ((uint64_t)1 << 32)) return (int32_t)((uint32_t)p / (uint32_t)c);
+    return (int32_t)(p / (uint64_t)c);
+}
 
 // Fixed-point ratio workers per slice, R = floor(A * 2^32 / T) (0 <= A < 2^31, 0 < T < 2^31).
 // Exact, without a 64-bit integer division (a long software sequence on the GPU): a double
@@ -87,64 +84,43 @@ __host__ __device__ inline uint64_t sched_ratio(int64_t A, int64_t T)
 }
 
 // First worker of an item that starts at slice C (C <= T, so C * R < 2^63) with K
-// non-empty items before it.
+// non-empty items before it (proportional split).
 __host__ __device__ inline int32_t worker_start(int64_t C, int64_t K, uint64_t R)
 {
     return (int32_t)(((uint64_t)C * R) >> 32) + (int32_t)K;
 }
 
-// Slice range [lo, hi) of worker j of an item with `size` slices and w workers (exact floor
-// divisions; 32-bit arithmetic whenever w * size fits, which gives the same result cheaper).
-__host__ __device__ inline void worker_range(int32_t j, int32_t w, int32_t size, int32_t &lo, int32_t &hi)
+// First worker of item g under the static split of NV workers over Hkv items.
+__host__ __device__ inline int32_t static_start(int32_t g, int32_t NV, int32_t Hkv) { return mul_div(g, NV, Hkv); }
+
+// Item of worker w under the static split.
+__host__ __device__ inline int32_t static_item(int32_t w, int32_t NV, int32_t Hkv)
 {
-    if ((uint64_t)w * (uint64_t)size < ((uint64_t)1 << 32)) {
-        lo = (int32_t)((uint32_t)j * (uint32_t)size / (uint32_t)w);
-        hi = (int32_t)((uint32_t)(j + 1) * (uint32_t)size / (uint32_t)w);
-    } else {
-        lo = (int32_t)((int64_t)j * size / w);
-        hi = (int32_t)((int64_t)(j + 1) * size / w);
-    }
+    int32_t g = mul_div(w, Hkv, NV);
+    if (g + 1 < Hkv && static_start(g + 1, NV, Hkv) <= w) ++g;
+    return g;
 }
 
-// The group of virtual block vb on an item with workers [ws0, ws1) and `size` slices: the
-// block's workers [lo, hi) of the item and the union [glo, ghi) of their slice ranges.
-__host__ __device__ inline void block_group(int32_t vb, int32_t nw, int32_t ws0, int32_t ws1, int32_t size,
-                                            int32_t &lo, int32_t &hi, int32_t &glo, int32_t &ghi)
-{
-    lo = ws0 > vb * nw ? ws0 : vb * nw;
-    hi = ws1 < (vb + 1) * nw ? ws1 : (vb + 1) * nw;
-    int32_t dummy;
-    worker_range(lo - ws0, ws1 - ws0, size, glo, dummy);
-    worker_range(hi - 1 - ws0, ws1 - ws0, size, dummy, ghi);
-}
+// First prefix slice of worker j (0 <= j <= W) of an item with P prefix slices.
+__host__ __device__ inline int32_t pre_split(int32_t j, int32_t W, int32_t P) { return mul_div(j, P, W); }
 
-// Slot records (kRowRec) of the rows of item i, whose parts are `count` consecutive slots from
-// slot vb0 + i: a prefix item's rows are (s, g*G + r) for s in [seq0, seq0 + nseq), a suffix
-// item's (seq0, g*G + r); the record's row within the slot is (s - seq0) * G + r.
-__host__ __device__ inline void write_rowrecs(int32_t *rowrec, int32_t i, int32_t n_pre, int32_t seq0, int32_t nseq,
-                                              int32_t g, int32_t G, int32_t Hq, int32_t slot_rows, int32_t vb0,
-                                              int32_t count)
+// First suffix slice of worker j (0 <= j <= W) of an item with P prefix and S suffix slices.
+// Non-decreasing in j from 0 to S: for S >= W, floor(T/W) >= ceil(P/W), so each worker's joint
+// count floor((j+1)T/W) - floor(jT/W) covers its prefix count.
+__host__ __device__ inline int32_t suf_split(int32_t j, int32_t W, int32_t P, int32_t S)
 {
-    const int32_t field = i < n_pre ? 0 : 2;
-    for (int32_t s = 0; s < nseq; ++s)
-        for (int32_t r = 0; r < G; ++r) {
-            int32_t *rr = rowrec + ((size_t)(seq0 + s) * Hq + g * G + r) * kRowRec + field;
-            rr[0] = (vb0 + i) * slot_rows + s * G + r;
-            rr[1] = count;
-        }
+    if (S >= W) return mul_div(j, P + S, W) - mul_div(j, P, W);
+    return mul_div(j, S, W);
 }
 
 struct AttnArgs {
-    const PrefixItem *pre_items;  // [n_pre]
-    int32_t n_pre;
-    int32_t pre_slices;   // sum of the prefix items' slices
-    int32_t pre_nonempty; // non-empty prefix items
+    const UnitRec *units;  // [n_units]
+    int32_t n_units;
+    int32_t static_split;  // 1: one unit, items split statically
+    int32_t ps_total;      // prefix slices of all units
     const int32_t *seq_prefix_len;  // [S] prefix length of each sequence's unit (paged page offsets)
-    const int32_t *tab[2];  // schedule cache of this launch: candidate tables and keys
-    const int32_t *key[2];
-    int32_t *rowrec_live;   // slot records written when no candidate is taken
-    int32_t *sel;           // block 0 writes the choice: candidate 0 / 1, or 2 (live records)
-    int32_t *lens;          // [S] clamped suffix lengths of this launch, for the merge
+    int32_t *rowrec;        // proportional split: [S * Hq][kRowRec], written by this launch
+    int32_t *lens;          // [S] clamped suffix lengths of this launch, for the merge (block 0)
     const uint16_t *q;  // [S][Hq][d]
     // contiguous layout
     const uint16_t *prefix_k, *prefix_v;  // [Hkv][Lp][d]
@@ -178,22 +154,16 @@ struct MergeArgs {
     float *out_lse;         // [rows] or null
     int32_t rows;
     int32_t n_q_heads;       // rows of one sequence (plan mode)
-    // explicit mode (rowrec == null): every row merges parts 0..n_parts-1
+    // explicit mode (plan == 0): every row merges parts 0..n_parts-1
     int32_t n_parts;
-    // plan mode: row (s, h) merges the slots of its prefix item and of its suffix item
-    const int32_t *rowrec[3];  // slot records: candidates 0 and 1 of this launch, live (see kRowRec)
-    const int32_t *sel;        // which of them this launch's partial kernel used
+    // plan mode: row (s, h) merges the partials of its item (see the work schedule above)
+    int32_t plan;
+    int32_t static_split;      // 1: slots from the static split; 0: from rowrec
+    const int32_t *rowrec;     // proportional split: written by this launch's partial kernel
     const int32_t *lens;       // this launch's clamped suffix lengths
     int32_t slot_rows;
     int32_t n_slots;           // records pointing outside [0, n_slots * slot_rows) are not followed
     int32_t *err;
-    // schedule cache for the next launch (tab_next[0] null: none is built)
-    int32_t *tab_next[2], *key_next[2], *rowrec_next[2];
-    const PrefixItem *pre_items;
-    int32_t n_pre;
-    int32_t pre_slices;
-    int32_t pre_nonempty;
-    int32_t n_seqs;
     int32_t waves;      // NW: workers per virtual block
     int32_t n_workers;  // NV
     // fused step: the token in k_new / v_new (not yet in the cache) joins each row as one

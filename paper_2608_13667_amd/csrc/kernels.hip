@@ -12,118 +12,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.442695040888963407f;
 
-// One candidate of the schedule cache for the next launch (internal.h), built by merge blocks
-// that hold no row: block pb of npb handles items pb, pb + npb, ...  Candidate 0 is for this
-// launch's lengths, candidate 1 for the lengths after this fused step's append (one longer where
-// there is room).  The key is the lengths a candidate is built for, so lengths that differ at
-// the next launch only cost the cache.
-__device__ void build_next_schedule(const MergeArgs &a, int cand, int pb, int npb)
-{
-    constexpr int NTH = 256;
-    __shared__ int32_t s_ln[kMaxSeqs], s_cs[kMaxSeqs], s_ne[kMaxSeqs];
-    __shared__ int32_t s_sum[2][NTH / 64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int N = a.n_seqs, Hkv = a.n_kv_heads, G = a.group, NW = a.waves;
-    int carry_cs = 0, carry_ne = 0;
-    for (int base = 0; base < N; base += NTH) {
-        const int s = base + tid;
-        int L = 0;
-        if (s < N) {
-            L = a.lens[s];
-            if (cand == 1 && L < a.max_suffix_len) ++L;
-            if (pb == 0) a.key_next[cand][s] = L;
-        }
-        const int xs = slices_of(L) * Hkv, xe = (L > 0) ? Hkv : 0;
-        int x = xs, y = xe;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const int ux = __shfl_up(x, off), uy = __shfl_up(y, off);
-            if (lane >= off) {
-                x += ux;
-                y += uy;
-            }
-        }
-        if (lane == 63) {
-            s_sum[0][wave] = x;
-            s_sum[1][wave] = y;
-        }
-        __syncthreads();
-        int px = carry_cs, py = carry_ne;
-        for (int w = 0; w < NTH / 64; ++w) {
-            if (w < wave) {
-                px += s_sum[0][w];
-                py += s_sum[1][w];
-            }
-            carry_cs += s_sum[0][w];
-            carry_ne += s_sum[1][w];
-        }
-        if (s < N) {
-            s_ln[s] = L;
-            s_cs[s] = px + x - xs;
-            s_ne[s] = py + y - xe;
-        }
-        __syncthreads();
-    }
-    const int T = a.pre_slices + carry_cs, NNE = a.pre_nonempty + carry_ne, NV = a.n_workers;
-    const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
-    const int n_items = a.n_pre + N * Hkv;
-    // workers past the last item have no work
-    const int ws_end = T > 0 ? worker_start(T, NNE, R) : 0;
-    if (pb == 0)
-        for (int gw = ws_end + tid; gw < NV; gw += NTH) a.tab_next[cand][(size_t)gw * kTabWords] = -1;
-    for (int i = pb; i < n_items; i += npb) {
-        int seq0, nseq, kvh, n_tok, size, C, K;
-        if (i < a.n_pre) {
-            const PrefixItem it = a.pre_items[i];
-            seq0 = it.seq0;
-            nseq = it.nseq;
-            kvh = it.kv_head;
-            n_tok = it.n_tok;
-            size = slices_of(n_tok);
-            C = it.c0;
-            K = it.k0;
-        } else {
-            const int j = i - a.n_pre, sq = j / Hkv;
-            seq0 = sq;
-            nseq = 1;
-            kvh = j % Hkv;
-            n_tok = s_ln[sq];
-            size = slices_of(n_tok);
-            C = a.pre_slices + s_cs[sq] + kvh * size;
-            K = a.pre_nonempty + s_ne[sq] + (size > 0 ? kvh : 0);
-        }
-        int ws0 = 0, ws1 = 0;
-        if (size > 0 && T > 0) {
-            ws0 = worker_start(C, K, R);
-            ws1 = worker_start(C + size, K + 1, R);
-        }
-        // slot records of the item's rows
-        const int field = i < a.n_pre ? 0 : 2;
-        const int vb0 = ws0 / NW, count = ws1 > ws0 ? (ws1 - 1) / NW - vb0 + 1 : 0;
-        for (int r = tid; r < nseq * G; r += NTH) {
-            int32_t *rr = a.rowrec_next[cand] + ((size_t)(seq0 + r / G) * a.n_q_heads + kvh * G + r % G) * kRowRec + field;
-            rr[0] = (vb0 + i) * a.slot_rows + r;
-            rr[1] = count;
-        }
-        // table rows of the item's workers
-        for (int gw = ws0 + tid; gw < ws1; gw += NTH) {
-            const int vb = gw / NW;
-            int lo, hi, glo, ghi;
-            block_group(vb, NW, ws0, ws1, size, lo, hi, glo, ghi);
-            int32_t *t = a.tab_next[cand] + (size_t)gw * kTabWords;
-            t[0] = i;
-            t[1] = seq0;
-            t[2] = nseq;
-            t[3] = kvh;
-            t[4] = n_tok;
-            t[5] = lo - vb * NW;
-            t[6] = glo;
-            t[7] = ghi;
-            t[8] = hi - vb * NW;
-        }
-    }
-}
-
 template <int HD>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 {
@@ -136,70 +24,64 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int chunk = tid % CH, slice = tid / CH;
     const int row = blockIdx.x;
-    if (row >= a.rows) {  // the blocks past the rows build the schedule cache of the next launch
-        const int per = a.step_mode ? ((int)gridDim.x - a.rows) / 2 : (int)gridDim.x - a.rows;
-        const int pb = row - a.rows;
-        if (pb < per) {
-            if (!a.step_mode && pb == 0 && tid == 0) a.key_next[1][0] = -1;  // no candidate 1
-            build_next_schedule(a, 0, pb, per);
-        } else {
-            build_next_schedule(a, 1, pb - per, per);
-        }
-        return;
-    }
 
-    // Everything this block reads first is requested together: the row's slot records and the
-    // schedule choice (plan mode) and, in a fused step, q and the appended key and value.
-    // Parts of this row, as offsets (part index * row stride + row) into part_o / part_lse:
-    // parts [0, np) start at p_first with stride p_step; parts [np, n) at s_first.
-    int np = 0, n = 0, L = 0, seq = 0, g = 0;
-    int64_t p_first = 0, p_step = 0, s_first = 0;
+    // Everything this block reads is requested together: under a static split the row's parts
+    // (their slots follow from the plan) with, in a fused step, the length, q and the appended
+    // key and value; under a proportional split the row's record first.
+    // Parts j = 0 .. n-1 of this row sit at offsets p_first + j * p_step into part_o / part_lse.
+    int n = 0, L = 0, seq = 0, g = 0;
+    int64_t p_first = 0, p_step = 0;
     bool with_new = false;  // fused step: the appended token is one more part, read from k_new / v_new
     float dot = 0.f;
     uint4 app_k = {0, 0, 0, 0}, app_v = {0, 0, 0, 0};  // fused step, block (s, 0): the token to store
     uint2 new_v = {0, 0};                              // fused step: this thread's 4 values of v_new
     constexpr int APP = HD / 8;                        // 16-byte chunks of one K/V row
-    if (a.rowrec[0]) {
+    if (a.plan) {
         seq = row / a.n_q_heads;
-        g = (row % a.n_q_heads) / a.group;
-        // the records of the schedule the partial kernel used (loaded together, then chosen)
-        const int sel = *a.sel;
-        const int4 r0 = *reinterpret_cast<const int4 *>(a.rowrec[0] + (size_t)row * kRowRec);
-        const int4 r1 = *reinterpret_cast<const int4 *>(a.rowrec[1] + (size_t)row * kRowRec);
-        const int4 r2 = *reinterpret_cast<const int4 *>(a.rowrec[2] + (size_t)row * kRowRec);
-        const int4 rec = sel == 0 ? r0 : sel == 1 ? r1 : r2;
-        L = a.lens[seq];
-        if (a.step_mode && row % a.n_q_heads == 0 && tid < a.n_kv_heads * APP) {
-            const size_t src = ((size_t)seq * a.n_kv_heads + tid / APP) * HD + 8 * (tid % APP);
-            app_k = *reinterpret_cast<const uint4 *>(a.k_new + src);
-            app_v = *reinterpret_cast<const uint4 *>(a.v_new + src);
-        }
-        with_new = a.step_mode && L < a.max_suffix_len;
-        if (a.step_mode && slice == 0)
-            new_v = *reinterpret_cast<const uint2 *>(a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk);
-        if (with_new && wave == 0) {  // q . k_new, wave 0
-            const uint16_t *qr = a.q + (size_t)row * HD;
-            const uint16_t *kr = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
-            for (int c = lane; c < HD; c += 64)
-                dot += __uint_as_float((uint32_t)qr[c] << 16) * __uint_as_float((uint32_t)kr[c] << 16);
-        }
-        // a record that points outside the workspace (it cannot, unless the cache was
-        // overwritten from outside) is dropped and flagged rather than followed
-        const int64_t lim = (int64_t)a.n_slots * a.slot_rows;
-        const bool p_ok = rec.y >= 0 && rec.x >= 0 && (int64_t)rec.x + (int64_t)max(rec.y - 1, 0) * a.slot_rows < lim;
-        const bool s_ok = rec.w >= 0 && rec.z >= 0 && (int64_t)rec.z + (int64_t)max(rec.w - 1, 0) * a.slot_rows < lim;
-        if ((!p_ok || !s_ok) && tid == 0) atomicOr(a.err, kErrBadSchedule);
-        p_first = rec.x;
-        np = p_ok ? rec.y : 0;
-        s_first = rec.z;
-        n = np + (s_ok ? rec.w : 0);
+        const int h = row % a.n_q_heads;
+        g = h / a.group;
         p_step = a.slot_rows;
+        if (a.static_split) {
+            // item g owns workers [floor(g NV / Hkv), floor((g+1) NV / Hkv)); its blocks write
+            // their partials to slots vb + g; the one unit starts at sequence 0
+            const int ws0 = static_start(g, a.n_workers, a.n_kv_heads);
+            const int ws1 = static_start(g + 1, a.n_workers, a.n_kv_heads);
+            const int vb0 = ws0 / a.waves;
+            n = ws1 > ws0 ? (ws1 - 1) / a.waves - vb0 + 1 : 0;
+            p_first = (int64_t)(vb0 + g) * a.slot_rows + (int64_t)seq * a.group + (h - g * a.group);
+        } else {
+            const int2 rec = *reinterpret_cast<const int2 *>(a.rowrec + (size_t)row * kRowRec);
+            // a record that points outside the workspace (it cannot, unless the workspace was
+            // overwritten from outside) is dropped and flagged rather than followed
+            const int64_t lim = (int64_t)a.n_slots * a.slot_rows;
+            const bool ok = rec.y >= 0 && rec.x >= 0 && (int64_t)rec.x + (int64_t)max(rec.y - 1, 0) * a.slot_rows < lim;
+            if (!ok && tid == 0) atomicOr(a.err, kErrBadSchedule);
+            p_first = rec.x;
+            n = ok ? rec.y : 0;
+        }
+        if (a.step_mode) {
+            L = a.lens[seq];
+            if (row % a.n_q_heads == 0 && tid < a.n_kv_heads * APP) {
+                const size_t src = ((size_t)seq * a.n_kv_heads + tid / APP) * HD + 8 * (tid % APP);
+                app_k = *reinterpret_cast<const uint4 *>(a.k_new + src);
+                app_v = *reinterpret_cast<const uint4 *>(a.v_new + src);
+            }
+            if (slice == 0)
+                new_v = *reinterpret_cast<const uint2 *>(a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk);
+            if (wave == 0) {  // q . k_new, wave 0 (used only when the token fits)
+                const uint16_t *qr = a.q + (size_t)row * HD;
+                const uint16_t *kr = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
+                for (int c = lane; c < HD; c += 64)
+                    dot += __uint_as_float((uint32_t)qr[c] << 16) * __uint_as_float((uint32_t)kr[c] << 16);
+            }
+            with_new = L < a.max_suffix_len;
+        }
     } else {
-        np = n = a.n_parts;
+        n = a.n_parts;
         p_first = row;
         p_step = a.rows;
     }
-    auto part_off = [&](int j) -> int64_t { return j < np ? p_first + j * p_step : s_first + (j - np) * p_step; };
+    auto part_off = [&](int j) -> int64_t { return p_first + j * p_step; };
 
     // Online merge of this slice's parts: running max m, weight sum w and accumulator (each
     // part's lse and o are loaded together).  An empty part (lse = -inf) has weight 0; a NaN
@@ -409,9 +291,7 @@ hipError_t launch_scatter(const ScatterArgs &a, hipStream_t s)
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s)
 {
     if (a.rows <= 0) return hipSuccess;
-    const int n_items = a.n_pre + a.n_seqs * a.n_kv_heads;
-    const int producers = a.tab_next[0] ? (n_items < 64 ? n_items : 64) * (a.step_mode ? 2 : 1) : 0;
-    const dim3 grid(a.rows + producers), block(256);
+    const dim3 grid(a.rows), block(256);
     if (head_dim == 128)
         merge_kernel<128><<<grid, block, 0, s>>>(a);
     else if (head_dim == 64)

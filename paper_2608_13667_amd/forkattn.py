@@ -32,25 +32,26 @@ class Heads(C.Structure):
 
 class ContigDesc(C.Structure):
     _fields_ = [("n_branches", C.c_int32), ("prefix_len", C.c_int32), ("suffix_cap", C.c_int32),
-                ("max_suffix_len", C.c_int32), ("share_prefix", C.c_int32), ("rounds", C.c_int32)]
+                ("max_suffix_len", C.c_int32), ("share_prefix", C.c_int32), ("rounds", C.c_int32),
+                ("blocks", C.c_int32)]
 
 
 class PagedDesc(C.Structure):
     _fields_ = [("n_seqs", C.c_int32), ("n_groups", C.c_int32), ("page_size", C.c_int32),
                 ("max_pages_per_seq", C.c_int32), ("n_pool_pages", C.c_int32), ("max_suffix_len", C.c_int32),
-                ("share_prefix", C.c_int32), ("rounds", C.c_int32)]
+                ("share_prefix", C.c_int32), ("rounds", C.c_int32), ("blocks", C.c_int32)]
 
 
 class PlanInfo(C.Structure):
-    _fields_ = [("n_items", C.c_int32), ("n_prefix_items", C.c_int32), ("waves_per_block", C.c_int32),
+    _fields_ = [("n_items", C.c_int32), ("n_units", C.c_int32), ("waves_per_block", C.c_int32),
                 ("n_blocks", C.c_int32), ("rounds", C.c_int32), ("n_slots", C.c_int32), ("slot_rows", C.c_int32),
-                ("workspace_bytes", C.c_size_t)]
+                ("static_split", C.c_int32), ("workspace_bytes", C.c_size_t)]
 
 
 class Slot(C.Structure):
-    _fields_ = [("slot", C.c_int32), ("kind", C.c_int32), ("seq0", C.c_int32), ("nseq", C.c_int32),
-                ("kv_head", C.c_int32), ("rows", C.c_int32), ("tok_begin", C.c_int32), ("tok_end", C.c_int32),
-                ("n_tok", C.c_int32)]
+    _fields_ = [("slot", C.c_int32), ("seq0", C.c_int32), ("nseq", C.c_int32), ("kv_head", C.c_int32),
+                ("rows", C.c_int32), ("prefix_begin", C.c_int32), ("prefix_end", C.c_int32),
+                ("suffix_begin", C.c_int32), ("suffix_end", C.c_int32), ("prefix_len", C.c_int32)]
 
 
 _vp = C.c_void_p
@@ -70,6 +71,7 @@ _sig = {
     "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
     "fka_plan_slots": ([_vp, _vp, _vp, C.c_int32, C.POINTER(C.c_int32)], C.c_int),
     "fka_partials": ([_vp] * 10, C.c_int),
+    "fka_partials_paged": ([_vp] * 9, C.c_int),
     "fka_lse_merge": ([C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp], C.c_int),
     "fka_plan_device_error": ([_vp, C.POINTER(C.c_int32)], C.c_int),
     "fka_plan_destroy": ([_vp], None),
@@ -115,9 +117,22 @@ def version() -> int:
     return _lib.fka_version()
 
 
-def _p(t: Optional[torch.Tensor]):
+_KIND_DTYPES = {"bf16": torch.bfloat16, "i32": torch.int32, "f32": torch.float32}
+
+
+def _p(t: Optional[torch.Tensor], kind: Optional[str] = None, device: Optional[int] = None):
+    """Device pointer of a contiguous tensor on the plan's GPU, of the dtype the C ABI expects
+    for this argument (bf16 q/K/V, int32 lengths and page tables, fp32 outputs)."""
     if t is None:
         return None
+    if not isinstance(t, torch.Tensor):
+        raise ValueError("expected a torch tensor")
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU (the library reads device memory)")
+    if device is not None and t.get_device() != device:
+        raise ValueError(f"tensor is on cuda:{t.get_device()}, the plan's device is cuda:{device}")
+    if kind is not None and t.dtype != _KIND_DTYPES[kind]:
+        raise ValueError(f"tensor must be {kind}, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError("tensor must be contiguous")
     return _vp(t.data_ptr())
@@ -134,15 +149,16 @@ class Plan:
 
     def __init__(self, handle: int, paged: bool, heads: Heads, n_seqs: int):
         self._h = _vp(handle)
+        self.device = torch.cuda.current_device() if torch.cuda.is_available() else None
         self.paged = paged
         self.heads = heads
         self.n_seqs = n_seqs
 
     @classmethod
     def contig(cls, n_q_heads, n_kv_heads, head_dim, n_branches, prefix_len, suffix_cap, max_suffix_len,
-               share_prefix=True, rounds=0, softmax_scale=0.0) -> "Plan":
+               share_prefix=True, rounds=0, softmax_scale=0.0, blocks=0) -> "Plan":
         h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
-        d = ContigDesc(n_branches, prefix_len, suffix_cap, max_suffix_len, int(bool(share_prefix)), rounds)
+        d = ContigDesc(n_branches, prefix_len, suffix_cap, max_suffix_len, int(bool(share_prefix)), rounds, blocks)
         out = _vp()
         _check(_lib.fka_plan_create_contig(C.byref(h), C.byref(d), C.byref(out)))
         return cls(out.value, False, h, n_branches)
@@ -150,12 +166,12 @@ class Plan:
     @classmethod
     def paged_plan(cls, n_q_heads, n_kv_heads, head_dim, group_start, group_prefix_len, max_pages_per_seq,
                    n_pool_pages, max_suffix_len, share_prefix=True, rounds=0, softmax_scale=0.0,
-                   page_size=16) -> "Plan":
+                   page_size=16, blocks=0) -> "Plan":
         gs = np.ascontiguousarray(group_start, np.int32)
         gl = np.ascontiguousarray(group_prefix_len, np.int32)
         h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
         d = PagedDesc(int(gs[-1]), len(gl), page_size, max_pages_per_seq, n_pool_pages, max_suffix_len,
-                      int(bool(share_prefix)), rounds)
+                      int(bool(share_prefix)), rounds, blocks)
         out = _vp()
         _check(_lib.fka_plan_create_paged(C.byref(h), C.byref(d), gs.ctypes.data_as(_vp), gl.ctypes.data_as(_vp),
                                           C.byref(out)))
@@ -200,42 +216,67 @@ class Plan:
 
     # ---- contiguous
     def decode(self, q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, out, out_lse=None, stream=None):
-        _check(_lib.fka_fork_decode(self._h, _p(q), _p(prefix_k), _p(prefix_v), _p(suffix_k), _p(suffix_v),
-                                    _p(suffix_len), _p(out), _p(out_lse), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_fork_decode(self._h, _p(q, "bf16", d), _p(prefix_k, "bf16", d), _p(prefix_v, "bf16", d),
+                                    _p(suffix_k, "bf16", d), _p(suffix_v, "bf16", d), _p(suffix_len, "i32", d),
+                                    _p(out, "f32", d), _p(out_lse, "f32", d), _stream(stream)))
 
     def append(self, k_new, v_new, suffix_k, suffix_v, suffix_len, stream=None):
-        _check(_lib.fka_append_kv(self._h, _p(k_new), _p(v_new), _p(suffix_k), _p(suffix_v), _p(suffix_len),
-                                  _stream(stream)))
+        d = self.device
+        _check(_lib.fka_append_kv(self._h, _p(k_new, "bf16", d), _p(v_new, "bf16", d), _p(suffix_k, "bf16", d),
+                                  _p(suffix_v, "bf16", d), _p(suffix_len, "i32", d), _stream(stream)))
 
     def step(self, q, k_new, v_new, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, out, out_lse=None,
              stream=None):
-        _check(_lib.fka_fork_step(self._h, _p(q), _p(k_new), _p(v_new), _p(prefix_k), _p(prefix_v), _p(suffix_k),
-                                  _p(suffix_v), _p(suffix_len), _p(out), _p(out_lse), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_fork_step(self._h, _p(q, "bf16", d), _p(k_new, "bf16", d), _p(v_new, "bf16", d),
+                                  _p(prefix_k, "bf16", d), _p(prefix_v, "bf16", d), _p(suffix_k, "bf16", d),
+                                  _p(suffix_v, "bf16", d), _p(suffix_len, "i32", d), _p(out, "f32", d),
+                                  _p(out_lse, "f32", d), _stream(stream)))
 
     def partials(self, q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, part_o, part_lse, stream=None):
-        _check(_lib.fka_partials(self._h, _p(q), _p(prefix_k), _p(prefix_v), _p(suffix_k), _p(suffix_v),
-                                 _p(suffix_len), _p(part_o), _p(part_lse), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_partials(self._h, _p(q, "bf16", d), _p(prefix_k, "bf16", d), _p(prefix_v, "bf16", d),
+                                 _p(suffix_k, "bf16", d), _p(suffix_v, "bf16", d), _p(suffix_len, "i32", d),
+                                 _p(part_o, "f32", d), _p(part_lse, "f32", d), _stream(stream)))
 
     # ---- paged
+    def partials_paged(self, q, k_pool, v_pool, page_table, suffix_len, part_o, part_lse, stream=None):
+        d = self.device
+        _check(_lib.fka_partials_paged(self._h, _p(q, "bf16", d), _p(k_pool, "bf16", d), _p(v_pool, "bf16", d),
+                                       _p(page_table, "i32", d), _p(suffix_len, "i32", d), _p(part_o, "f32", d),
+                                       _p(part_lse, "f32", d), _stream(stream)))
+
     def decode_paged(self, q, k_pool, v_pool, page_table, suffix_len, out, out_lse=None, stream=None):
-        _check(_lib.fka_fork_decode_paged(self._h, _p(q), _p(k_pool), _p(v_pool), _p(page_table), _p(suffix_len),
-                                          _p(out), _p(out_lse), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_fork_decode_paged(self._h, _p(q, "bf16", d), _p(k_pool, "bf16", d), _p(v_pool, "bf16", d),
+                                          _p(page_table, "i32", d), _p(suffix_len, "i32", d), _p(out, "f32", d),
+                                          _p(out_lse, "f32", d), _stream(stream)))
 
     def step_paged(self, q, k_new, v_new, k_pool, v_pool, page_table, suffix_len, out, out_lse=None, stream=None):
-        _check(_lib.fka_fork_step_paged(self._h, _p(q), _p(k_new), _p(v_new), _p(k_pool), _p(v_pool),
-                                        _p(page_table), _p(suffix_len), _p(out), _p(out_lse), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_fork_step_paged(self._h, _p(q, "bf16", d), _p(k_new, "bf16", d), _p(v_new, "bf16", d),
+                                        _p(k_pool, "bf16", d), _p(v_pool, "bf16", d), _p(page_table, "i32", d),
+                                        _p(suffix_len, "i32", d), _p(out, "f32", d), _p(out_lse, "f32", d),
+                                        _stream(stream)))
 
     def append_paged(self, k_new, v_new, k_pool, v_pool, page_table, suffix_len, stream=None):
-        _check(_lib.fka_append_kv_paged(self._h, _p(k_new), _p(v_new), _p(k_pool), _p(v_pool), _p(page_table),
-                                        _p(suffix_len), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_append_kv_paged(self._h, _p(k_new, "bf16", d), _p(v_new, "bf16", d), _p(k_pool, "bf16", d),
+                                        _p(v_pool, "bf16", d), _p(page_table, "i32", d), _p(suffix_len, "i32", d),
+                                        _stream(stream)))
 
     def gather_paged_range(self, seq, begin, out_len, k_pool, v_pool, page_table, k_out, v_out, stream=None):
-        _check(_lib.fka_gather_paged_range(self._h, int(seq), int(begin), int(out_len), _p(k_pool), _p(v_pool),
-                                           _p(page_table), _p(k_out), _p(v_out), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_gather_paged_range(self._h, int(seq), int(begin), int(out_len), _p(k_pool, "bf16", d),
+                                           _p(v_pool, "bf16", d), _p(page_table, "i32", d), _p(k_out, "bf16", d),
+                                           _p(v_out, "bf16", d), _stream(stream)))
 
     def gather_paged(self, seq, k_pool, v_pool, page_table, out_len, k_out, v_out, stream=None):
-        _check(_lib.fka_gather_paged(self._h, int(seq), _p(k_pool), _p(v_pool), _p(page_table), int(out_len),
-                                     _p(k_out), _p(v_out), _stream(stream)))
+        d = self.device
+        _check(_lib.fka_gather_paged(self._h, int(seq), _p(k_pool, "bf16", d), _p(v_pool, "bf16", d),
+                                     _p(page_table, "i32", d), int(out_len), _p(k_out, "bf16", d),
+                                     _p(v_out, "bf16", d), _stream(stream)))
 
 
 def _host_i32(a: np.ndarray) -> _vp:
@@ -310,14 +351,14 @@ class Pool:
 def scatter_pages(k_src, v_src, frm, page_row, n_pool_pages, k_pool, v_pool, err=None, stream=None):
     """Positions [frm, frm + n) held in k_src / v_src bf16 [Hkv][n][d] -> pool pages of page_row (device int32)."""
     Hkv, n, d = k_src.shape
-    _check(_lib.fka_scatter_pages(_p(k_src), _p(v_src), int(frm) + n, int(frm), _p(page_row), Hkv, d, int(n_pool_pages),
-                                  _p(k_pool), _p(v_pool), _p(err), _stream(stream)))
+    _check(_lib.fka_scatter_pages(_p(k_src, "bf16"), _p(v_src, "bf16"), int(frm) + n, int(frm), _p(page_row, "i32"), Hkv, d, int(n_pool_pages),
+                                  _p(k_pool, "bf16"), _p(v_pool, "bf16"), _p(err, "i32"), _stream(stream)))
 
 
 def lse_merge(part_o, part_lse, out, out_lse=None, stream=None):
     """part_o fp32 [P][R][d], part_lse fp32 [P][R] -> out fp32 [R][d], out_lse fp32 [R]."""
     P, R, d = part_o.shape
-    _check(_lib.fka_lse_merge(R, P, d, _p(part_o), _p(part_lse), _p(out), _p(out_lse), _stream(stream)))
+    _check(_lib.fka_lse_merge(R, P, d, _p(part_o, "f32"), _p(part_lse, "f32"), _p(out, "f32"), _p(out_lse, "f32"), _stream(stream)))
 
 
 def raw_call(name: str, *args) -> int:

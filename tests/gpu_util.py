@@ -11,11 +11,11 @@ def dev_i32(a: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, np.int32)).cuda()
 
 
-def contig_plan(fa, w, share_prefix=True, rounds=0, max_suffix_len=None):
+def contig_plan(fa, w, share_prefix=True, rounds=0, max_suffix_len=None, blocks=0):
     s = w.spec
     msl = w.suffix_cap if max_suffix_len is None else max_suffix_len
     return fa.Plan.contig(s.n_q_heads, s.n_kv_heads, s.head_dim, w.n_branches, w.prefix_len, w.suffix_cap, msl,
-                          share_prefix=share_prefix, rounds=rounds)
+                          share_prefix=share_prefix, rounds=rounds, blocks=blocks)
 
 
 def to_dev_contig(w) -> dict:
@@ -32,12 +32,12 @@ def run_contig(plan, dv, rows_hq):
     return out.cpu().numpy(), lse.cpu().numpy()
 
 
-def paged_plan(fa, w, share_prefix=True, rounds=0, max_suffix_len=None):
+def paged_plan(fa, w, share_prefix=True, rounds=0, max_suffix_len=None, blocks=0):
     s = w.spec
     msl = int(w.suffix_len.max()) + s.page_headroom if max_suffix_len is None else max_suffix_len
     return fa.Plan.paged_plan(s.n_q_heads, s.n_kv_heads, s.head_dim, w.group_start, w.prefix_len,
                               w.page_table.shape[1], w.k_pool.shape[0], msl, share_prefix=share_prefix,
-                              rounds=rounds)
+                              rounds=rounds, blocks=blocks)
 
 
 def to_dev_paged(w) -> dict:

@@ -121,3 +121,20 @@ def test_lse_merge_rejects_head_dim(fa):
     assert fa.raw_call("fka_lse_merge", 4, 2, 96, None, None, None, None, None) == -2
     assert fa.raw_call("fka_lse_merge", -1, 2, 64, None, None, None, None, None) == -1
     assert fa.raw_call("fka_lse_merge", 0, 2, 64, None, None, None, None, None) == 0
+
+
+def test_binding_rejects_host_and_mistyped_tensors(fa):
+    """The binding hands the library device pointers only: a host tensor, a wrong dtype or a
+    non-contiguous view is refused before any call (an int64 length array would otherwise be
+    read as int32 pairs, a host pointer would reach the kernels)."""
+    import torch
+    with pytest.raises(ValueError, match="GPU"):
+        fa._p(torch.zeros(4, dtype=torch.int32), "i32")
+    with pytest.raises(ValueError):
+        fa._p(torch.zeros(4).numpy(), "f32")
+    assert fa._p(None, "f32") is None
+
+
+def test_plan_create_rejects_negative_blocks(fa):
+    st, out = _create(fa, _heads(fa), fa.ContigDesc(5, 512, 64, 64, 1, 0, -1))
+    assert st == -1 and "blocks" in fa.last_error() and not out.value

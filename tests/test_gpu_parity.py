@@ -209,8 +209,58 @@ def test_repeatable(fa):
         assert np.array_equal(al, bl), _max_diff(al, bl)
 
 
+def _slot_key_ranges(sl, lens, G):
+    """Per row of a slot (fka_plan_slots): the sequence, its prefix key range and its suffix key
+    range.  The unit's suffix list holds each sequence's ceil(len / 32) slices in order."""
+    out = []
+    cs = 0
+    for i in range(sl["nseq"]):
+        s = sl["seq0"] + i
+        L = int(lens[s])
+        n = -(-L // 32)
+        a, b = max(sl["suffix_begin"], cs), min(sl["suffix_end"], cs + n)
+        sr = (32 * (a - cs), min(32 * (b - cs), L)) if b > a else (0, 0)
+        for r in range(G):
+            out.append((s, (sl["prefix_begin"], sl["prefix_end"]), sr))
+        cs += n
+    return out
+
+
+def _check_slot_values(po, pl, slots, info, ref_fn, lens, G, note):
+    """Every slot equals the oracle's attention of its rows over their key ranges, and the slots
+    of each item tile its prefix and its suffix list exactly."""
+    assert len(slots) > 0
+    seen = set()
+    cover = {}
+    for sl in slots:
+        assert sl["slot"] not in seen and 0 <= sl["slot"] < info.n_slots
+        seen.add(sl["slot"])
+        cover.setdefault((sl["seq0"], sl["kv_head"]), []).append(sl)
+        g = sl["kv_head"]
+        for r, (s, pr, sr) in enumerate(_slot_key_ranges(sl, lens, G)):
+            h = g * G + r % G
+            what = f"{note} slot {sl['slot']} row {r} seq {s} prefix {pr} suffix {sr}"
+            if pr[1] > pr[0] or sr[1] > sr[0]:
+                ref, ref_lse = ref_fn(s, h, pr, sr)
+                gates.assert_gates(po[sl["slot"], r][None], ref[None], what=what)
+                gates.assert_lse(pl[sl["slot"], r][None], np.array([ref_lse]), what=what)
+            else:
+                assert np.all(po[sl["slot"], r] == 0) and np.isneginf(pl[sl["slot"], r]), what
+    for key, sls in cover.items():
+        P = sls[0]["prefix_len"]
+        pre = sorted((x["prefix_begin"], x["prefix_end"]) for x in sls)
+        suf = sorted((x["suffix_begin"], x["suffix_end"]) for x in sls)
+        nsuf = sum(-(-int(lens[sls[0]["seq0"] + i]) // 32) for i in range(sls[0]["nseq"]))
+        assert pre[0][0] == 0 and pre[-1][1] == P, (key, pre[:3], pre[-3:])
+        assert suf[0][0] == 0 and suf[-1][1] == nsuf, (key, suf[:3], suf[-3:])
+        for (a0, a1), (b0, b1) in zip(pre, pre[1:]):
+            assert a1 == b0, key
+        for (a0, a1), (b0, b1) in zip(suf, suf[1:]):
+            assert a1 == b0, key
+
+
 def _check_slots(fa, w, plan, note):
-    """Every slot a decode writes equals the oracle's attention of its rows over its key range."""
+    """Contiguous plan: the first stage's partials against the oracle, slot by slot."""
     info = plan.info()
     dv = to_dev_contig(w)
     N, Hq, d = w.q.shape
@@ -220,45 +270,54 @@ def _check_slots(fa, w, plan, note):
     plan.partials(dv["q"], dv["prefix_k"], dv["prefix_v"], dv["suffix_k"], dv["suffix_v"], dv["suffix_len"], po, pl)
     torch.cuda.synchronize()
     po, pl = po.cpu().numpy(), pl.cpu().numpy()
-    slots = plan.slots(w.suffix_len)
-    assert len(slots) > 0
-    seen = set()
-    cover = {}
-    for sl in slots:
-        assert sl["slot"] not in seen and 0 <= sl["slot"] < info.n_slots
-        seen.add(sl["slot"])
-        key = (sl["kind"], sl["seq0"], sl["kv_head"])
-        cover.setdefault(key, []).append((sl["tok_begin"], sl["tok_end"], sl["n_tok"]))
-        if sl["kind"] == 0:
-            pr, sr = (sl["tok_begin"], sl["tok_end"]), (0, 0)
-        else:
-            pr, sr = (0, 0), (sl["tok_begin"], sl["tok_end"])
+
+    def ref_fn(s, h, pr, sr):
         ref, ref_lse = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, w.suffix_len,
-                                            w.spec.softmax_scale, prefix_range=pr, suffix_range=sr)
-        g = sl["kv_head"]
-        for r in range(sl["rows"]):
-            b = sl["seq0"] + r // G
-            h = g * G + r % G
-            what = f"{note} slot {sl['slot']} kind {sl['kind']} row {r} keys {sl['tok_begin']}:{sl['tok_end']}"
-            if sl["tok_end"] > sl["tok_begin"]:
-                gates.assert_gates(po[sl["slot"], r][None], ref[b, h][None], what=what)
-                gates.assert_lse(pl[sl["slot"], r][None], ref_lse[b, h][None], what=what)
-            else:
-                assert np.all(po[sl["slot"], r] == 0) and np.isneginf(pl[sl["slot"], r]), what
-    # the slots of each item tile its keys exactly
-    for key, ranges in cover.items():
-        ranges.sort()
-        n_tok = ranges[0][2]
-        assert ranges[0][0] == 0 and ranges[-1][1] == n_tok, key
-        for (a0, a1, _), (b0, b1, _) in zip(ranges, ranges[1:]):
-            assert a1 == b0, key
+                                            w.spec.softmax_scale, prefix_range=pr, suffix_range=sr,
+                                            rows=[s * Hq + h])
+        return ref[s, h], ref_lse[s, h]
+
+    _check_slot_values(po, pl, plan.slots(w.suffix_len), info, ref_fn, w.suffix_len, G, note)
 
 
-def test_schedule_cache_follows_length_changes(fa):
-    """Each decode builds the schedule of the next one for the lengths it expects, keyed by them.
-    Lengths set by the host between calls (new ones, empty suffixes, an earlier set again), a
-    partial stage launched in between, and repeated calls at the same lengths (which take the
-    cached schedule) all match the oracle."""
+def _check_slots_paged(fa, w, plan, note):
+    """Paged plan: each sequence's prefix and suffix gathered on the host (the oracle's page
+    walk) into the contiguous layout, then as for a contiguous plan."""
+    info = plan.info()
+    dv = to_dev_paged(w)
+    S, Hq, d = w.q.shape
+    G = Hq // w.spec.n_kv_heads
+    po = torch.full((info.n_slots, info.slot_rows, d), float("nan"), device="cuda")
+    pl = torch.full((info.n_slots, info.slot_rows), float("nan"), device="cuda")
+    plan.partials_paged(dv["q"], dv["k_pool"], dv["v_pool"], dv["page_table"], dv["suffix_len"], po, pl)
+    torch.cuda.synchronize()
+    po, pl = po.cpu().numpy(), pl.cpu().numpy()
+    cache = {}
+
+    def seq_kv(s):
+        if s not in cache:
+            Lp, L = int(w.seq_prefix_len[s]), int(w.suffix_len[s])
+            cache[s] = (Lp, L) + oracle.gather_paged(w.k_pool, w.v_pool, w.page_table, s, Lp, L)
+        return cache[s]
+
+    def ref_fn(s, h, pr, sr):
+        Lp, L, k, v = seq_kv(s)
+        cap = max(L, 1)
+        sk = np.full((1, k.shape[0], cap, d), W.BF16_NAN, np.uint16)
+        sv = sk.copy()
+        sk[0, :, :L], sv[0, :, :L] = k[:, Lp:], v[:, Lp:]
+        ref, ref_lse = oracle.decode_contig(w.q[s:s + 1], np.ascontiguousarray(k[:, :Lp]),
+                                            np.ascontiguousarray(v[:, :Lp]), sk, sv, np.array([L], np.int32),
+                                            w.spec.softmax_scale, prefix_range=pr, suffix_range=sr, rows=[h])
+        return ref[0, h], ref_lse[0, h]
+
+    _check_slot_values(po, pl, plan.slots(w.suffix_len), info, ref_fn, w.suffix_len, G, note)
+
+
+def test_lengths_change_between_calls(fa):
+    """Every launch schedules from the lengths it finds on the device: lengths set by the host
+    between calls (new ones, empty suffixes, an earlier set again), a partial stage launched in
+    between, and repeated calls all match the oracle."""
     w = W.make("mid", steps=0, seed=83)
     plan = contig_plan(fa, w)
     dv = to_dev_contig(w)
@@ -270,7 +329,7 @@ def test_schedule_cache_follows_length_changes(fa):
     sets = [w.suffix_len.copy(), rng.integers(0, full + 1).astype(np.int32), w.suffix_len.copy(),
             np.zeros(N, np.int32), np.minimum(rng.integers(0, 40, N), full).astype(np.int32), w.suffix_len.copy()]
     for i, ln in enumerate(sets):
-        print(f"[cache] set {i}: {ln.tolist()}", flush=True)
+        print(f"[lengths] set {i}: {ln.tolist()}", flush=True)
         dv["suffix_len"].copy_(torch.from_numpy(ln))
         ref, ref_lse = oracle.decode_contig(w.q, w.prefix_k, w.prefix_v, w.suffix_k, w.suffix_v, ln,
                                             w.spec.softmax_scale)
@@ -288,7 +347,7 @@ def test_schedule_cache_follows_length_changes(fa):
 
 @pytest.mark.parametrize("rounds", [0, 5])
 def test_partials_stage(fa, rounds):
-    """Each first-stage partial equals the oracle's attention over that slot's key range."""
+    """Each first-stage partial equals the oracle's attention over that slot's key ranges."""
     w = W.make("mid", prefix_len=5000, seed=81)
     _check_slots(fa, w, contig_plan(fa, w, rounds=rounds), f"rounds={rounds}")
 
@@ -296,6 +355,27 @@ def test_partials_stage(fa, rounds):
 def test_partials_stage_naive_plan(fa):
     w = W.make("tiny-unscaled", prefix_len=700, suffix_range=(0, 90), seed=82)
     _check_slots(fa, w, contig_plan(fa, w, share_prefix=False), "naive")
+
+
+@pytest.mark.parametrize("blocks", [3, 16])
+def test_partials_stage_few_blocks(fa, blocks):
+    """Grids that do not divide the KV heads evenly: blocks straddle two items."""
+    w = W.make("mid", prefix_len=3000, seed=84)
+    _check_slots(fa, w, contig_plan(fa, w, blocks=blocks), f"blocks={blocks}")
+
+
+def test_partials_stage_paged(fa):
+    """The paged first stage, slot by slot (several groups: the proportional split)."""
+    w = _small_paged(seed=91)
+    _check_slots_paged(fa, w, paged_plan(fa, w), "paged")
+
+
+def test_partials_stage_paged_one_group(fa):
+    """A paged plan with one group takes the static split."""
+    w = W.make(W.CONFIGS["paged"].replace(n_tasks=1, prefix_range=(1500, 1500), suffix_range=(0, 300), seed=92))
+    plan = paged_plan(fa, w)
+    assert plan.info().static_split == 1
+    _check_slots_paged(fa, w, plan, "paged one group")
 
 
 @pytest.mark.parametrize("d", [64, 128])

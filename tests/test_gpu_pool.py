@@ -158,7 +158,8 @@ def test_branch_instruction_prefill(fa):
     gates.assert_lse(lse.cpu().numpy(), ref_lse, what="instruction prefill")
     assert int(err.item()) == 0 and plan.device_error() == 0
     info = plan.info()
-    assert info.n_items == Hkv + N * n * Hkv  # one prefix item per KV head: the prefix is read once
+    # one item per KV head holding all N * n * G rows: the prefix is read once per chunk
+    assert info.n_units == 1 and info.n_items == Hkv and info.slot_rows == N * n * (Hq // Hkv)
 
 
 def test_ranged_gather_bit_exact(fa):
