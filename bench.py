@@ -7,7 +7,11 @@ context: 32768-token shared prefix, 5 sequences, 40 query / 8 KV heads, head_dim
 suffixes of 512..2048 tokens, 256 appended tokens per layer.  Layers are replicated
 so that the working set (>= 1 GiB) exceeds the 256 MB Infinity Cache and every step
 reads HBM; step i runs on replica i % R.  Inputs are resident in HBM before the timed
-region.  Prints one JSON line.
+region.  The timed region is K steps launched as one HIP graph (captured once, so host
+launch overhead is not measured); it runs in several trials, each from the same suffix
+lengths, and the median trial is reported.  The same JSON line carries sub-records for
+the other workloads (128k prefix, 16 paged forks, 8k prefix), each timed the same way,
+a read-only bandwidth probe and the CPU oracle's rate.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -26,9 +30,9 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 MALL_BYTES = 256 << 20
-COPY_PROBE_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_13667_amd", "csrc", "partials.hip")
+SUB_WORKLOADS = ("very-long", "paged", "mid")
 
 
 def measured_traffic(workload: str):
@@ -46,6 +50,7 @@ def measured_traffic(workload: str):
     if not entry or entry.get("kernel_sha256") != digest:
         return None
     return entry.get("bytes_per_launch")
+
 
 DESCRIPTIONS = {
     "long": "long agent context: 32768-token shared prefix, 5 sequences (main + 4 branches), 40 q / 8 kv heads, "
@@ -69,19 +74,258 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: 256 appends per replica)")
-    # 200 untimed steps: on the 128k-prefix workload the first ~20 ms of back-to-back launches run
-    # a transient (steps 5-10% slower, then settling); shorter workloads are unaffected
-    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps per trial (default: 256 appends per replica for the long workload)")
+    ap.add_argument("--warmup", type=int, default=20, help="untimed steps before the timed trials")
+    ap.add_argument("--trials", type=int, default=5, help="timed trials; the median is reported")
     ap.add_argument("--workload", default="long", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--sub", default=",".join(SUB_WORKLOADS),
+                    help="comma-separated workloads timed as sub-records ('' for none)")
     ap.add_argument("--replicas", type=int, default=0, help="layer replicas (0: enough for >= 1 GiB)")
     ap.add_argument("--rounds", type=int, default=0, help="schedule rounds of the resident waves (0: automatic)")
+    ap.add_argument("--eager", action="store_true", help="launch the timed steps one by one instead of as a graph")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-naive", action="store_true", help="skip the naive per-branch GPU baseline")
+    ap.add_argument("--no-probe", action="store_true", help="skip the read-bandwidth probe")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--lifecycle", action="store_true",
                     help="also time the fork lifecycle on the page pool (contiguous workloads' shapes)")
     return ap.parse_args()
+
+
+class Bench:
+    """One workload on the device: layer replicas, plans, step and partial-kernel timing."""
+
+    def __init__(self, torch, fa, W, name, args):
+        self.torch, self.fa, self.W, self.name, self.args = torch, fa, W, name, args
+        t0 = time.time()
+        w = self.w = W.make(name)
+        log(f"[bench] generated {name} in {time.time() - t0:.1f}s")
+        spec = self.spec = w.spec
+        self.paged = spec.paged
+        self.appends = spec.steps > 0
+        self.kvb = W.kv_bytes_paged(w) if self.paged else W.kv_bytes_contig(w)
+        self.R = args.replicas or max(1, math.ceil((1 << 30) / self.kvb["total"]))
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        if self.paged:
+            base = dict(q=dev(w.q), k_pool=dev(w.k_pool), v_pool=dev(w.v_pool),
+                        page_table=torch.from_numpy(w.page_table).cuda(),
+                        suffix_len=torch.from_numpy(w.suffix_len).cuda())
+        else:
+            base = dict(q=dev(w.q), prefix_k=dev(w.prefix_k), prefix_v=dev(w.prefix_v), suffix_k=dev(w.suffix_k),
+                        suffix_v=dev(w.suffix_v), suffix_len=torch.from_numpy(w.suffix_len).cuda())
+        self.reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(self.R - 1)]
+        self.n_seq = w.q.shape[0]
+        self.out = torch.empty((self.n_seq, spec.n_q_heads, spec.head_dim), device="cuda")
+        self.lse = torch.empty((self.n_seq, spec.n_q_heads), device="cuda")
+        if self.appends:
+            self.step_q, self.step_k, self.step_v = dev(w.step_q), dev(w.step_k), dev(w.step_v)
+        self.len0 = torch.from_numpy(w.suffix_len).cuda()
+        self.per_tok = 2 * spec.n_kv_heads * spec.head_dim * 2
+        log(f"[bench] {name}: {self.R} replicas x {self.kvb['total'] / 2**20:.1f} MiB")
+
+    def default_steps(self):
+        return 256 * self.R if self.appends else max(200, 20 * self.R)
+
+    def plan(self, share=True):
+        spec, w, fa = self.spec, self.w, self.fa
+        if self.paged:
+            return fa.Plan.paged_plan(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.group_start, w.prefix_len,
+                                      w.page_table.shape[1], w.k_pool.shape[0], int(w.suffix_len.max()),
+                                      share_prefix=share, rounds=self.args.rounds)
+        return fa.Plan.contig(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.n_branches, w.prefix_len,
+                              w.suffix_cap, w.suffix_cap, share_prefix=share, rounds=self.args.rounds)
+
+    def run(self, plan, i):
+        r = self.reps[i % self.R]
+        if self.paged:
+            plan.decode_paged(r["q"], r["k_pool"], r["v_pool"], r["page_table"], r["suffix_len"], self.out, self.lse)
+        elif self.appends:
+            j = i // self.R
+            plan.step(self.step_q[j], self.step_k[j], self.step_v[j], r["prefix_k"], r["prefix_v"], r["suffix_k"],
+                      r["suffix_v"], r["suffix_len"], self.out, self.lse)
+        else:
+            plan.decode(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"], self.out,
+                        self.lse)
+
+    def reset(self):
+        for r in self.reps:
+            r["suffix_len"].copy_(self.len0)
+
+    def timed(self, body, n, warmup_body=None, trials=5):
+        """Seconds of each trial of body(n).  With graphs, the n calls are captured once and each
+        trial replays them; the suffix lengths are reset before every trial (outside the timing)."""
+        torch = self.torch
+        if warmup_body is not None:
+            warmup_body()
+        torch.cuda.synchronize()
+        graph = None
+        if not self.args.eager:
+            self.reset()
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                body(n)
+            torch.cuda.synchronize()
+        out = []
+        for _ in range(trials):
+            self.reset()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            if graph is not None:
+                graph.replay()
+            else:
+                body(n)
+            e1.record()
+            torch.cuda.synchronize()
+            out.append(e0.elapsed_time(e1) * 1e-3)
+        return out
+
+    def step_bytes(self, n_steps):
+        """Algorithmic K/V bytes of n steps: each group's prefix once per step plus every suffix at its length."""
+        total = 0
+        sl0 = int(np.sum(self.w.suffix_len))
+        for i in range(n_steps):
+            extra = (i // self.R + 1) * self.n_seq if self.appends else 0
+            total += self.kvb["prefix"] + (sl0 + extra) * self.per_tok
+        return total
+
+    def partial_kernel(self, plan):
+        """Average duration of the partial-attention kernel alone (its launches replayed as one graph on
+        the stream they run on), as the suffix lengths of the first step leave it."""
+        torch = self.torch
+        info = plan.info()
+        d = self.spec.head_dim
+        po = torch.empty((info.n_slots, info.slot_rows, d), device="cuda")
+        pl = torch.empty((info.n_slots, info.slot_rows), device="cuda")
+
+        def part(n):
+            for i in range(n):
+                r = self.reps[i % self.R]
+                if self.paged:
+                    plan.partials_paged(r["q"], r["k_pool"], r["v_pool"], r["page_table"], r["suffix_len"], po, pl)
+                else:
+                    plan.partials(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"],
+                                  po, pl)
+        kp = max(20, min(200, 4 * self.R))
+        secs = self.timed(part, kp, warmup_body=lambda: part(5), trials=3)
+        return float(np.median(secs)) / kp
+
+    def measure(self, n_steps, warmup, trials, naive=True, mall_warm=False):
+        """Fork-aware steps (median of trials), the partial kernel alone, the naive baseline."""
+        plan = self.plan(True)
+        info = plan.info()
+        secs = self.timed(lambda n: [self.run(plan, i) for i in range(n)], n_steps,
+                          warmup_body=lambda: [self.run(plan, i) for i in range(warmup)], trials=trials)
+        assert plan.device_error() == 0, "device error flag raised"
+        med = float(np.median(secs))
+        alg = self.step_bytes(n_steps)
+        gbps = alg / med / 1e9
+        k_secs = self.partial_kernel(plan)
+        k_gbps = self.kvb["total"] / k_secs / 1e9
+        rec = {"steps_per_s": n_steps / med, "us_per_step": med / n_steps * 1e6,
+               "trials_us_per_step": [s / n_steps * 1e6 for s in secs], "steps": n_steps, "warmup": warmup,
+               "effective_kv_gbps": gbps, "hbm_peak_frac": gbps / HBM_PEAK_GBPS,
+               "roofline": {"bound": "hbm", "kernel": "partials_kernel (prefix + suffix partial attention)",
+                            "achieved": k_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": k_gbps / HBM_PEAK_GBPS,
+                            "traffic": measured_traffic(self.name), "avg_launch_us": k_secs * 1e6,
+                            "bytes_per_launch": self.kvb["total"]},
+               "config": {"workload": DESCRIPTIONS[self.name], "name": self.name, "replicas": self.R,
+                          "working_set_gib": self.R * self.kvb["total"] / 2**30, "blocks": info.n_blocks,
+                          "waves_per_block": info.waves_per_block, "rounds": info.rounds, "work_items": info.n_items,
+                          "static_split": bool(info.static_split),
+                          "launch": "eager" if self.args.eager else "hip graph of the timed steps"}}
+        log(f"[bench] {self.name} fork-aware: {rec['steps_per_s']:.1f} steps/s, {rec['us_per_step']:.2f} us/step, "
+            f"{gbps:.0f} GB/s ({rec['hbm_peak_frac'] * 100:.1f}% of 8 TB/s); partial kernel {k_secs * 1e6:.2f} us, "
+            f"{k_gbps / HBM_PEAK_GBPS * 100:.1f}%")
+        if naive:
+            nplan = self.plan(False)
+            kn = max(self.R, n_steps // 4)
+            nsecs = self.timed(lambda n: [self.run(nplan, i) for i in range(n)], kn,
+                               warmup_body=lambda: [self.run(nplan, i) for i in range(min(warmup, kn))], trials=3)
+            nmed = float(np.median(nsecs))
+            nalg = self.step_bytes(kn)
+            rec["naive_per_branch"] = {
+                "steps_per_s": kn / nmed, "us_per_step": nmed / kn * 1e6, "effective_kv_gbps": nalg / nmed / 1e9,
+                "requested_kv_gbps": (nalg + (self.kvb["naive"] - self.kvb["total"]) * kn) / nmed / 1e9,
+                "prefix_reuse_speedup": (nmed / kn) / (med / n_steps)}
+            log(f"[bench] {self.name} naive: {kn / nmed:.1f} steps/s, speed-up of sharing "
+                f"{rec['naive_per_branch']['prefix_reuse_speedup']:.2f}x")
+            nplan.close()
+        if mall_warm and not self.paged and self.kvb["total"] < MALL_BYTES:
+            r0 = self.reps[0]
+            nw = min(n_steps, 200)
+            ws = self.timed(lambda n: [plan.decode(r0["q"], r0["prefix_k"], r0["prefix_v"], r0["suffix_k"],
+                                                   r0["suffix_v"], r0["suffix_len"], self.out, self.lse)
+                                       for _ in range(n)], nw, trials=3)
+            wmed = float(np.median(ws))
+            rec["mall_warm_single_replica"] = {"steps_per_s": nw / wmed, "kv_gbps": self.kvb["total"] * nw / wmed / 1e9}
+        self.plan_info = info
+        plan.close()
+        return rec
+
+    def release(self):
+        self.reps = None
+        self.torch.cuda.empty_cache()
+
+
+def read_probe(torch, fa, sizes):
+    """Achievable read bandwidth: the library's streaming read kernel over buffers rotated so that
+    >= 1 GiB is touched between repeats of one buffer, for a few launch shapes; the best is kept."""
+    sink = torch.zeros(64, dtype=torch.int32, device="cuda")
+    out = {}
+    for label, nbytes in sizes.items():
+        nbytes = nbytes // 4096 * 4096
+        R = max(2, math.ceil((1 << 30) / nbytes))
+        bufs = [torch.empty(nbytes // 4, dtype=torch.int32, device="cuda").fill_(i) for i in range(R)]
+        best = None
+        for blocks, threads, unroll in ((4096, 512, 4), (2048, 256, 8), (1024, 512, 8), (256, 512, 4)):
+            def go(n):
+                for i in range(n):
+                    fa.read_probe(bufs[i % R], blocks, threads, unroll, sink)
+            go(4)
+            torch.cuda.synchronize()
+            n = max(20, 2 * R)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            go(n)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / n
+            g = nbytes / us / 1e3
+            if best is None or g > best["gbps"]:
+                best = {"gbps": g, "us": us, "bytes": nbytes, "blocks": blocks, "threads": threads, "unroll": unroll}
+        out[label] = best
+        del bufs
+        torch.cuda.empty_cache()
+        log(f"[bench] read probe {label}: {best['gbps']:.0f} GB/s ({best['us']:.2f} us for {nbytes / 2**20:.1f} MiB)")
+    return out
+
+
+def cpu_oracle(oracle, w, n_seq, hq, seconds):
+    """The fp64 oracle on the host: all rows of full decode steps at the initial lengths, on every
+    host thread and on one."""
+    oracle.build(force=False)
+    res = {}
+    for label, threads in (("all", None), ("one", 1)):
+        if threads is not None:
+            oracle.set_threads(threads)
+        n, t0 = 0, time.time()
+        budget = seconds if threads is None else seconds / 2
+        while True:
+            oracle.decode_workload(w)
+            n += 1
+            if time.time() - t0 >= budget:
+                break
+        res[label] = (n / (time.time() - t0), oracle.threads(), n)
+    oracle.set_threads(len(os.sched_getaffinity(0)))
+    v, cores, n = res["all"]
+    v1, _, n1 = res["one"]
+    log(f"[bench] cpu oracle: {v:.3f} steps/s on {cores} threads, {v1:.4f} steps/s on 1")
+    return {"value": v, "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} full decode steps (all {n_seq} x {hq} rows) at the initial lengths, fp64 on the host",
+            "single_thread": {"value": v1, "unit": "steps/s", "cores": 1, "sample": f"{n1} full decode steps"}}
 
 
 def lifecycle_timing(fa, torch, w):
@@ -204,218 +448,67 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
 
-    t0 = time.time()
-    w = W.make(args.workload)
-    spec = w.spec
-    log(f"[bench] generated {args.workload} in {time.time() - t0:.1f}s")
-    paged = spec.paged
-    appends = spec.steps > 0
-    if paged:
-        kvb = W.kv_bytes_paged(w)
-    else:
-        kvb = W.kv_bytes_contig(w)
-    R = args.replicas or max(1, math.ceil((1 << 30) / kvb["total"]))
-    K = args.steps if args.steps is not None else (256 * R if appends else max(200, 20 * R))
-    if appends and math.ceil(K / R) > spec.steps:
-        sys.exit(f"--steps {K} over {R} replicas exceeds the {spec.steps} appends each suffix buffer holds")
-
-    # device replicas of the layer (same values, distinct memory)
-    per_tok = 2 * spec.n_kv_heads * spec.head_dim * 2
-    if paged:
-        base = dict(q=dev(w.q), k_pool=dev(w.k_pool), v_pool=dev(w.v_pool),
-                    page_table=torch.from_numpy(w.page_table).cuda(), suffix_len=torch.from_numpy(w.suffix_len).cuda())
-        reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(R - 1)]
-
-        def mk_plan(share):
-            return fa.Plan.paged_plan(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.group_start, w.prefix_len,
-                                      w.page_table.shape[1], w.k_pool.shape[0], int(w.suffix_len.max()),
-                                      share_prefix=share, rounds=args.rounds)
-    else:
-        base = dict(q=dev(w.q), prefix_k=dev(w.prefix_k), prefix_v=dev(w.prefix_v), suffix_k=dev(w.suffix_k),
-                    suffix_v=dev(w.suffix_v), suffix_len=torch.from_numpy(w.suffix_len).cuda())
-        reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(R - 1)]
-
-        def mk_plan(share):
-            return fa.Plan.contig(spec.n_q_heads, spec.n_kv_heads, spec.head_dim, w.n_branches, w.prefix_len,
-                                  w.suffix_cap, w.suffix_cap, share_prefix=share, rounds=args.rounds)
-    n_seq = w.q.shape[0]
-    out = torch.empty((n_seq, spec.n_q_heads, spec.head_dim), device="cuda")
-    lse = torch.empty((n_seq, spec.n_q_heads), device="cuda")
-    if appends:
-        step_q, step_k, step_v = dev(w.step_q), dev(w.step_k), dev(w.step_v)
-    len0 = torch.from_numpy(w.suffix_len).cuda()
-    log(f"[bench] {R} replicas x {kvb['total'] / 2**20:.1f} MiB, {K} timed steps")
-
-    def run(plan, i):
-        r = reps[i % R]
-        if paged:
-            plan.decode_paged(r["q"], r["k_pool"], r["v_pool"], r["page_table"], r["suffix_len"], out, lse)
-        elif appends:
-            j = i // R
-            plan.step(step_q[j], step_k[j], step_v[j], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"],
-                      r["suffix_len"], out, lse)
-        else:
-            plan.decode(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"], out, lse)
-
-    def reset():
-        for r in reps:
-            r["suffix_len"].copy_(len0)
-
-    def timed_loop(plan, n_steps, warmup):
-        reset()
-        for i in range(warmup):
-            run(plan, i)
-        torch.cuda.synchronize()
-        reset()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(n_steps):
-            run(plan, i)
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e-3
-
-    def step_bytes(n_steps):
-        """Algorithmic K/V bytes of the timed loop: prefix once per step plus every suffix at its length."""
-        total = 0
-        sl0 = int(np.sum(w.suffix_len))
-        for i in range(n_steps):
-            extra = (i // R + 1) * n_seq if appends else 0
-            total += kvb["prefix"] + (sl0 + extra) * per_tok
-        return total
-
-    plan = mk_plan(True)
-    info = plan.info()
-    secs = timed_loop(plan, K, args.warmup)
-    assert plan.device_error() == 0
-    alg = step_bytes(K)
-    gbps = alg / secs / 1e9
-    log(f"[bench] fork-aware: {K / secs:.1f} steps/s, {secs / K * 1e6:.2f} us/step, {gbps:.0f} GB/s")
-
-    # dominant kernel alone: the partial-attention kernel, timed on the stream it runs on
-    po = torch.empty((info.n_slots, info.slot_rows, spec.head_dim), device="cuda")
-    pl = torch.empty((info.n_slots, info.slot_rows), device="cuda")
-    reset()
-    kp = max(50, min(K, 400))
-    if not paged:
-        def part(i):
-            r = reps[i % R]
-            plan.partials(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"], po, pl)
-        # as inside a step, the partial kernel runs on the schedule the previous launch cached: one
-        # decode at these lengths (all replicas hold the same ones) builds it
-        r0 = reps[0]
-        plan.decode(r0["q"], r0["prefix_k"], r0["prefix_v"], r0["suffix_k"], r0["suffix_v"], r0["suffix_len"], out, lse)
-        for i in range(5):
-            part(i)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(kp):
-            part(i)
-        e1.record()
-        torch.cuda.synchronize()
-        k_secs = e0.elapsed_time(e1) * 1e-3 / kp
-        k_bytes = kvb["total"]
-        roof_name = "partials_kernel (prefix + suffix partial attention)"
-    else:
-        k_secs = secs / K
-        k_bytes = kvb["total"]
-        roof_name = "whole paged step (partials + merge)"
-    k_gbps = k_bytes / k_secs / 1e9
-
-    result_extra = {}
-    if not args.no_naive:
-        nplan = mk_plan(False)
-        kn = max(R, K // 4)
-        nsecs = timed_loop(nplan, kn, min(args.warmup, kn))
-        nalg = step_bytes(kn)
-        result_extra["naive_per_branch"] = {
-            "steps_per_s": kn / nsecs, "us_per_step": nsecs / kn * 1e6,
-            "effective_kv_gbps": nalg / nsecs / 1e9,
-            "requested_kv_gbps": (nalg + (kvb["naive"] - kvb["total"]) * kn) / nsecs / 1e9,
-            "prefix_reuse_speedup": (nsecs / kn) / (secs / K)}
-        log(f"[bench] naive: {kn / nsecs:.1f} steps/s, speed-up of sharing {(nsecs / kn) / (secs / K):.2f}x")
-        nplan.close()
-
-    # MALL-warm single-replica figure (labelled: the working set fits in the 256 MB Infinity Cache)
-    if not paged and kvb["total"] < MALL_BYTES:
-        r0 = reps[0]
-        reset()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        nw = min(K, 200)
-        e0.record()
-        for i in range(nw):
-            plan.decode(r0["q"], r0["prefix_k"], r0["prefix_v"], r0["suffix_k"], r0["suffix_v"], r0["suffix_len"], out,
-                        lse)
-        e1.record()
-        torch.cuda.synchronize()
-        ws = e0.elapsed_time(e1) * 1e-3
-        result_extra["mall_warm_single_replica"] = {"steps_per_s": nw / ws, "kv_gbps": kvb["total"] * nw / ws / 1e9}
-
-    # context probes: a plain 256 MiB device copy (its FETCH_SIZE / WRITE_SIZE counters are the
-    # yardstick that turns counter readings into bytes) and its achieved copy bandwidth
-    x = torch.empty(COPY_PROBE_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
-    y = torch.empty_like(x)
-    y.copy_(x)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(10):
-        y.copy_(x)
-    e1.record()
-    torch.cuda.synchronize()
-    result_extra["copy_probe_gbps"] = 10 * 2 * COPY_PROBE_BYTES / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del x, y
-
+    main_b = Bench(torch, fa, W, args.workload, args)
+    K = args.steps if args.steps is not None else main_b.default_steps()
+    if main_b.appends and math.ceil(K / main_b.R) > main_b.spec.steps:
+        sys.exit(f"--steps {K} over {main_b.R} replicas exceeds the {main_b.spec.steps} appends each suffix buffer holds")
+    rec = main_b.measure(K, args.warmup, args.trials, naive=not args.no_naive, mall_warm=True)
+    main_bytes = main_b.kvb["total"]
     cpu = None
     if not args.no_cpu:
-        oracle.build(force=False)
-        t_start = time.time()
-        n = 0
-        while True:
-            oracle.decode_workload(w)
-            n += 1
-            if time.time() - t_start >= args.cpu_seconds:
-                break
-        cs = time.time() - t_start
-        cpu = {"value": n / cs, "unit": "steps/s", "cores": oracle.threads(), "kind": "oracle",
-               "sample": f"{n} full decode steps (all {n_seq} x {spec.n_q_heads} rows) at the initial lengths, "
-                         f"fp64 on the host"}
-        log(f"[bench] cpu oracle: {n / cs:.3f} steps/s on {cpu['cores']} threads")
+        cpu = cpu_oracle(oracle, main_b.w, main_b.n_seq, main_b.spec.n_q_heads, args.cpu_seconds)
+    lifecycle = None
+    if args.lifecycle and not main_b.paged:
+        lifecycle = lifecycle_timing(fa, torch, main_b.w)
+    main_b.release()
 
-    cfg = {"workload": DESCRIPTIONS[args.workload], "name": args.workload, "replicas": R,
-           "working_set_gib": R * kvb["total"] / 2**30, "blocks": info.n_blocks,
-           "waves_per_block": info.waves_per_block, "rounds": info.rounds, "work_items": info.n_items}
+    subs = {}
+    for name in [s for s in args.sub.split(",") if s and s != args.workload]:
+        b = Bench(torch, fa, W, name, args)
+        k = args.steps if args.steps is not None else b.default_steps()
+        if b.appends:
+            k = min(k, 256 * b.R)
+        subs[name] = b.measure(k, args.warmup, args.trials, naive=not args.no_naive)
+        b.release()
+        del b
+
+    probe = None
+    if not args.no_probe:
+        probe = read_probe(torch, fa, {"main_workload_bytes": main_bytes, "1GiB": 1 << 30})
+
     res = {
         "metric": "fork-decode attention steps/s and effective KV GB/s (% of HBM peak), 1 GPU",
-        "value": K / secs,
+        "value": rec["steps_per_s"],
         "unit": "steps/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
-        "ms_per_step": secs / K * 1e3,
+        "ms_per_step": rec["us_per_step"] / 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": cfg,
-        "effective_kv_gbps": gbps,
-        "hbm_peak_frac": gbps / HBM_PEAK_GBPS,
-        "roofline": {"bound": "hbm", "kernel": roof_name, "achieved": k_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": k_gbps / HBM_PEAK_GBPS, "traffic": measured_traffic(args.workload),
-                     "avg_launch_us": k_secs * 1e6, "bytes_per_launch": k_bytes},
+        "config": rec["config"],
+        "trials": args.trials,
+        "trials_us_per_step": rec["trials_us_per_step"],
+        "effective_kv_gbps": rec["effective_kv_gbps"],
+        "hbm_peak_frac": rec["hbm_peak_frac"],
+        "roofline": rec["roofline"],
         "cpu_baseline": cpu,
     }
-    res.update(result_extra)
-    if args.lifecycle and not paged:
-        res["lifecycle"] = lifecycle_timing(fa, torch, w)
-        log(f"[bench] lifecycle: {res['lifecycle']}")
-    plan.close()
+    for key in ("naive_per_branch", "mall_warm_single_replica"):
+        if key in rec:
+            res[key] = rec[key]
+    if probe:
+        res["read_probe"] = probe
+        best = max(p["gbps"] for p in probe.values())
+        res["achievable_read_frac"] = {"step": rec["effective_kv_gbps"] / best,
+                                       "partial_kernel": rec["roofline"]["achieved"] / best}
+    res["sub_workloads"] = subs
+    if lifecycle:
+        res["lifecycle"] = lifecycle
     print(json.dumps(res), flush=True)
 
 

@@ -367,6 +367,17 @@ fka_status fka_partials_paged(const fka_plan *plan, const void *q, const void *k
 fka_status fka_lse_merge(int32_t rows, int32_t n_parts, int32_t head_dim, const float *part_o,
                          const float *part_lse, float *out, float *out_lse, void *stream);
 
+/* ------------------------------------------------------------------ measurement */
+
+/* Read-only streaming probe (the achievable read bandwidth of the device, a yardstick for the
+ * partial kernel's K/V stream): `blocks` blocks of `threads` threads each read a contiguous
+ * share of the device buffer buf[bytes] with non-temporal 16-byte loads, `unroll` loads in
+ * flight per thread, and fold the words into a value written to sink (device uint32 [64]) only
+ * in a case that practically never occurs.  bytes a positive multiple of 16, buf 16-byte
+ * aligned, threads a multiple of 64 in [64, 1024], unroll 4, 8 or 16. */
+fka_status fka_read_probe(const void *buf, size_t bytes, int32_t blocks, int32_t threads, int32_t unroll,
+                          uint32_t *sink, void *stream);
+
 /* Read and clear the plan's device error flag (synchronises with the device):
  * *flags receives a bit mask: 1 = a suffix length above max_suffix_len was
  * clamped, 2 = an append found no room (length at max_suffix_len or no page),

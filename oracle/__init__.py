@@ -40,9 +40,11 @@ def _load():
         i = C.c_int
         lib.oracle_decode_contig.argtypes = [i, i, i, i, C.c_double, p, i, p, p, i, p, p, p, i, i, i, i, p, i, p, p]
         lib.oracle_decode_paged.argtypes = [i, i, i, i, C.c_double, p, i, p, p, C.c_long, p, i, p, p, p, i, p, p]
-        lib.oracle_gather_paged.argtypes = [i, i, i, p, p, p, i, i, i, i, p, p]
+        lib.oracle_gather_paged.argtypes = [i, i, i, p, p, C.c_long, p, i, i, i, i, p, p]
         lib.oracle_lse_merge.argtypes = [i, i, i, p, p, p, p]
         lib.oracle_threads.argtypes = []
+        lib.oracle_set_threads.argtypes = [C.c_int]
+        lib.oracle_set_threads.restype = None
         for f in (lib.oracle_decode_contig, lib.oracle_decode_paged, lib.oracle_gather_paged,
                   lib.oracle_lse_merge, lib.oracle_threads):
             f.restype = C.c_int
@@ -60,6 +62,11 @@ def _c(a, dtype):
 
 def threads() -> int:
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads of the following oracle calls (OpenMP)."""
+    _load().oracle_set_threads(int(n))
 
 
 def decode_contig(q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, scale: float,
@@ -86,6 +93,8 @@ def decode_contig(q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, scale: 
     rc = _load().oracle_decode_contig(N, Hq, Hkv, d, float(scale), _ptr(q), Lp, _ptr(pk), _ptr(pv), cap,
                                       _ptr(sk), _ptr(sv), _ptr(sl), int(plo), int(phi), int(slo), int(shi),
                                       _ptr(r), 0 if r is None else len(r), _ptr(out), _ptr(lse))
+    if rc == -3:
+        raise ValueError("a suffix length is outside [0, suffix capacity]")
     if rc != 0:
         raise RuntimeError(f"oracle_decode_contig failed: {rc}")
     return out, lse
@@ -118,8 +127,8 @@ def gather_paged(k_pool, v_pool, page_table, seq: int, prefix_len: int, suffix_l
     L = prefix_len + suffix_len
     ko = np.empty((Hkv, L, d), np.uint16)
     vo = np.empty((Hkv, L, d), np.uint16)
-    rc = _load().oracle_gather_paged(Hkv, d, P, _ptr(kp), _ptr(vp), _ptr(pt), pt.shape[1], seq, prefix_len,
-                                     suffix_len, _ptr(ko), _ptr(vo))
+    rc = _load().oracle_gather_paged(Hkv, d, P, _ptr(kp), _ptr(vp), kp.shape[0], _ptr(pt), pt.shape[1], seq,
+                                     prefix_len, suffix_len, _ptr(ko), _ptr(vo))
     if rc != 0:
         raise RuntimeError(f"oracle_gather_paged failed: {rc}")
     return ko, vo

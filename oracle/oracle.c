@@ -95,8 +95,11 @@ int oracle_decode_contig(int N, int Hq, int Hkv, int d, double scale, const uint
     for (int t = 0; t < total; ++t) {
         const int row = rows ? rows[t] : t;
         const int b = row / Hq, h = row % Hq, g = h / G;
-        int len = suffix_len[b];
-        if (len > cap) len = cap;
+        const int len = suffix_len[b];
+        if (len < 0 || len > cap) {  /* a suffix holds 0..cap tokens: anything else is not an input */
+            bad |= 2;
+            continue;
+        }
         int shi = s_hi < len ? s_hi : len;
         int nsuf = shi > s_lo ? shi - s_lo : 0;
         long n = (long)(p_hi - p_lo) + nsuf;
@@ -122,12 +125,12 @@ int oracle_decode_contig(int N, int Hq, int Hkv, int d, double scale, const uint
         free(vr);
         free(s);
     }
-    return bad ? -2 : 0;
+    return (bad & 2) ? -3 : bad ? -2 : 0;
 }
 
 /* Pool address of logical position p of sequence `seq` (prefix length Lp). */
-static const uint16_t *paged_row(const uint16_t *pool, const int32_t *page_table, int max_pages, int seq,
-                                 int Lp, int P, int Hkv, int d, int g, long p)
+static const uint16_t *paged_row(const uint16_t *pool, long n_pages, const int32_t *page_table, int max_pages,
+                                 int seq, int Lp, int P, int Hkv, int d, int g, long p)
 {
     long page_idx, slot;
     if (p < Lp) {
@@ -140,7 +143,7 @@ static const uint16_t *paged_row(const uint16_t *pool, const int32_t *page_table
     }
     if (page_idx >= max_pages) return NULL;
     int32_t page = page_table[(size_t)seq * max_pages + page_idx];
-    if (page < 0) return NULL;
+    if (page < 0 || page >= n_pages) return NULL;
     return pool + (((size_t)page * Hkv + g) * P + slot) * d;
 }
 
@@ -164,6 +167,10 @@ int oracle_decode_paged(int S, int Hq, int Hkv, int d, double scale, const uint1
         const int row = rows ? rows[t] : t;
         const int i = row / Hq, h = row % Hq, g = h / G;
         const int Lp = seq_prefix_len[i];
+        if (suffix_len[i] < 0 || Lp < 0) {  /* not an input: lengths are counts */
+            bad |= 4;
+            continue;
+        }
         long n = (long)Lp + suffix_len[i];
         const uint16_t **kr = malloc(sizeof(*kr) * (size_t)(n ? n : 1));
         const uint16_t **vr = malloc(sizeof(*vr) * (size_t)(n ? n : 1));
@@ -173,11 +180,10 @@ int oracle_decode_paged(int S, int Hq, int Hkv, int d, double scale, const uint1
         } else {
             int ok = 1;
             for (long p = 0; p < n; ++p) {
-                kr[p] = paged_row(k_pool, page_table, max_pages, i, Lp, P, Hkv, d, g, p);
-                vr[p] = paged_row(v_pool, page_table, max_pages, i, Lp, P, Hkv, d, g, p);
+                kr[p] = paged_row(k_pool, n_pages, page_table, max_pages, i, Lp, P, Hkv, d, g, p);
+                vr[p] = paged_row(v_pool, n_pages, page_table, max_pages, i, Lp, P, Hkv, d, g, p);
                 if (!kr[p] || !vr[p]) ok = 0;
             }
-            (void)n_pages;
             if (ok)
                 attend_row(q + ((size_t)i * Hq + h) * d, d, scale, n, kr, vr, s, out + (size_t)row * d,
                            out_lse + row);
@@ -195,15 +201,16 @@ int oracle_decode_paged(int S, int Hq, int Hkv, int d, double scale, const uint1
  * Copy the K and V rows of one paged sequence, in logical order, into contiguous
  * [Hkv][L][d] arrays, L = prefix + suffix length.  Pure data movement.
  */
-int oracle_gather_paged(int Hkv, int d, int P, const uint16_t *k_pool, const uint16_t *v_pool,
+int oracle_gather_paged(int Hkv, int d, int P, const uint16_t *k_pool, const uint16_t *v_pool, long n_pages,
                         const int32_t *page_table, int max_pages, int seq, int Lp, int Ls, uint16_t *k_out,
                         uint16_t *v_out)
 {
+    if (Lp < 0 || Ls < 0) return -1;
     long L = (long)Lp + Ls;
     for (int g = 0; g < Hkv; ++g)
         for (long p = 0; p < L; ++p) {
-            const uint16_t *kr = paged_row(k_pool, page_table, max_pages, seq, Lp, P, Hkv, d, g, p);
-            const uint16_t *vr = paged_row(v_pool, page_table, max_pages, seq, Lp, P, Hkv, d, g, p);
+            const uint16_t *kr = paged_row(k_pool, n_pages, page_table, max_pages, seq, Lp, P, Hkv, d, g, p);
+            const uint16_t *vr = paged_row(v_pool, n_pages, page_table, max_pages, seq, Lp, P, Hkv, d, g, p);
             if (!kr || !vr) return -3;
             memcpy(k_out + ((size_t)g * L + p) * d, kr, sizeof(uint16_t) * (size_t)d);
             memcpy(v_out + ((size_t)g * L + p) * d, vr, sizeof(uint16_t) * (size_t)d);
@@ -249,6 +256,18 @@ int oracle_lse_merge(int rows, int n_parts, int d, const double *o_parts, const 
         out_lse[r] = M + log(wsum);
     }
     return 0;
+}
+
+/* Sets the threads of the following parallel regions (n >= 1); used to time the oracle on one
+ * core and on all of them. */
+void oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
 }
 
 /* Threads an OpenMP parallel region uses (reported next to oracle timings). */

@@ -806,6 +806,21 @@ fka_status fka_lse_merge(int32_t rows, int32_t n_parts, int32_t head_dim, const 
     return ok();
 }
 
+fka_status fka_read_probe(const void *buf, size_t bytes, int32_t blocks, int32_t threads, int32_t unroll,
+                          uint32_t *sink, void *stream)
+{
+    REQUIRE_PTR16(buf);
+    REQUIRE(sink != nullptr, "sink is null");
+    REQUIRE(bytes > 0 && bytes % 16 == 0, "bytes (%zu) must be a positive multiple of 16", bytes);
+    REQUIRE(blocks >= 1, "blocks (%d) must be >= 1", blocks);
+    REQUIRE(threads >= 64 && threads <= 1024 && threads % 64 == 0, "threads (%d) must be a multiple of 64 in [64, 1024]",
+            threads);
+    REQUIRE(unroll == 4 || unroll == 8 || unroll == 16, "unroll (%d) must be 4, 8 or 16", unroll);
+    hipError_t e = fka::launch_read_probe(buf, bytes, blocks, threads, unroll, sink, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "read probe launch");
+    return ok();
+}
+
 fka_status fka_plan_device_error(const fka_plan *p, int32_t *flags)
 {
     REQUIRE(p != nullptr && flags != nullptr, "null argument");

@@ -243,5 +243,7 @@ hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs &a, hipStream_t s);
+hipError_t launch_read_probe(const void *buf, size_t bytes, int blocks, int threads, int unroll, uint32_t *sink,
+                             hipStream_t s);
 
 }  // namespace fka

@@ -74,6 +74,7 @@ _sig = {
     "fka_partials_paged": ([_vp] * 9, C.c_int),
     "fka_lse_merge": ([C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp], C.c_int),
     "fka_plan_device_error": ([_vp, C.POINTER(C.c_int32)], C.c_int),
+    "fka_read_probe": ([_vp, C.c_size_t, C.c_int32, C.c_int32, C.c_int32, _vp, _vp], C.c_int),
     "fka_plan_destroy": ([_vp], None),
     "fka_pool_create": ([C.c_int32, C.POINTER(_vp)], C.c_int),
     "fka_pool_destroy": ([_vp], None),
@@ -353,6 +354,12 @@ def scatter_pages(k_src, v_src, frm, page_row, n_pool_pages, k_pool, v_pool, err
     Hkv, n, d = k_src.shape
     _check(_lib.fka_scatter_pages(_p(k_src, "bf16"), _p(v_src, "bf16"), int(frm) + n, int(frm), _p(page_row, "i32"), Hkv, d, int(n_pool_pages),
                                   _p(k_pool, "bf16"), _p(v_pool, "bf16"), _p(err, "i32"), _stream(stream)))
+
+
+def read_probe(buf, blocks, threads, unroll, sink, stream=None):
+    """Read-only streaming probe over the device tensor buf (fka_read_probe)."""
+    _check(_lib.fka_read_probe(_p(buf), buf.numel() * buf.element_size(), int(blocks), int(threads), int(unroll),
+                               _p(sink), _stream(stream)))
 
 
 def lse_merge(part_o, part_lse, out, out_lse=None, stream=None):

@@ -659,3 +659,48 @@ def test_nan_input_propagates_to_its_branch_only(fa):
     assert np.all(np.isfinite(out[~bad]))
     ref, _ = oracle.decode_workload(w)
     gates.assert_gates(out[~bad], ref[~bad], what="rows without the NaN")
+
+
+def test_graph_replay_matches_eager(fa):
+    """The benchmark launches its timed steps as a captured HIP graph.  Fused steps captured once
+    and replayed several times (with the lengths reset, and eager work and synchronisations in
+    between) give, in every replay, exactly what the same steps give when launched one by one."""
+    w = W.make("mid", steps=6, seed=96)
+    plan = contig_plan(fa, w)
+    dv = to_dev_contig(w)
+    N, Hq, d = w.q.shape
+    kn, vn, qn = dev_bf16(w.step_k), dev_bf16(w.step_v), dev_bf16(w.step_q)
+    len0 = dv["suffix_len"].clone()
+    outs = [torch.empty((N, Hq, d), device="cuda") for _ in range(6)]
+    lses = [torch.empty((N, Hq), device="cuda") for _ in range(6)]
+
+    def steps():
+        for t in range(6):
+            plan.step(qn[t], kn[t], vn[t], dv["prefix_k"], dv["prefix_v"], dv["suffix_k"], dv["suffix_v"],
+                      dv["suffix_len"], outs[t], lses[t])
+
+    steps()
+    torch.cuda.synchronize()
+    ref = [o.cpu().numpy().copy() for o in outs]
+    ref_lse = [x.cpu().numpy().copy() for x in lses]
+    ref_k = dv["suffix_k"].view(torch.int16).cpu().numpy().copy()
+    dv["suffix_len"].copy_(len0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        steps()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        dv["suffix_len"].copy_(len0)
+        for o in outs:
+            o.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for t in range(6):
+            assert np.array_equal(outs[t].cpu().numpy(), ref[t]), f"replay {rep} step {t}"
+            assert np.array_equal(lses[t].cpu().numpy(), ref_lse[t]), f"replay {rep} step {t} lse"
+        assert np.array_equal(dv["suffix_k"].view(torch.int16).cpu().numpy(), ref_k)
+        assert np.array_equal(dv["suffix_len"].cpu().numpy(), (len0 + 6).cpu().numpy())
+        _ = torch.randn(1000, device="cuda").sum().item()  # eager work between replays
+    assert plan.device_error() == 0
