@@ -207,6 +207,9 @@ fka_status finish_plan(fka_plan *p)
     const size_t b_err = 256;
     const size_t b_rec = up(rows * fka::kRowRec * sizeof(int32_t));
     const size_t b_po = up((size_t)p->n_slots * p->slot_rows * p->d * sizeof(float));
+    // the merge addresses the partials with 32-bit byte offsets
+    if (b_po >= ((size_t)1 << 31))
+        return fail(FKA_ERR_UNSUPPORTED, "partial results of %zu bytes exceed the 2 GiB the merge addresses", b_po);
     const size_t b_pl = up((size_t)p->n_slots * p->slot_rows * sizeof(float));
     const size_t b_zero = b_err + b_rec + b_seq;  // err, records, lengths: zeroed
     const size_t total = b_units + b_seq + b_zero + b_po + b_pl;

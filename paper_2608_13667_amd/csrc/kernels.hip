@@ -4,51 +4,42 @@
 // merge_kernel: log-sum-exp combination of the partials of each (sequence, head).
 // append_kernel / gather_kernel: suffix append and paged gather (data movement).
 #include "internal.h"
+#include "merge_row.h"
 
 namespace fka {
 namespace {
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr float kLog2e = 1.442695040888963407f;
-
 template <int HD>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 {
-    constexpr int CH = HD / 4;    // float4 chunks per row
-    constexpr int SL = 256 / CH;  // part slices: slice k takes parts k, k + SL, ...
-    __shared__ float s_m[SL], s_w[SL];
-    __shared__ f32x4 s_acc[SL][CH];
-    __shared__ float s_new;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int chunk = tid % CH, slice = tid / CH;
+    __shared__ MergeLds<HD> lds;
+    constexpr int APP = HD / 8;  // 16-byte chunks of one K/V row
+    const int tid = threadIdx.x;
     const int row = blockIdx.x;
 
     // Everything this block reads is requested together: under a static split the row's parts
     // (their slots follow from the plan) with, in a fused step, the length, q and the appended
     // key and value; under a proportional split the row's record first.
-    // Parts j = 0 .. n-1 of this row sit at offsets p_first + j * p_step into part_o / part_lse.
-    int n = 0, L = 0, seq = 0, g = 0;
-    int64_t p_first = 0, p_step = 0;
-    bool with_new = false;  // fused step: the appended token is one more part, read from k_new / v_new
-    float dot = 0.f;
+    RowMerge m{};
+    m.part_o = a.part_o;
+    m.part_lse = a.part_lse;
+    m.out_row = a.out + (size_t)row * HD;
+    m.out_lse = a.out_lse ? a.out_lse + row : nullptr;
+    int seq = 0;
     uint4 app_k = {0, 0, 0, 0}, app_v = {0, 0, 0, 0};  // fused step, block (s, 0): the token to store
-    uint2 new_v = {0, 0};                              // fused step: this thread's 4 values of v_new
-    constexpr int APP = HD / 8;                        // 16-byte chunks of one K/V row
     if (a.plan) {
         seq = row / a.n_q_heads;
         const int h = row % a.n_q_heads;
-        g = h / a.group;
-        p_step = a.slot_rows;
+        const int g = h / a.group;
+        m.p_step = a.slot_rows;
         if (a.static_split) {
             // item g owns workers [floor(g NV / Hkv), floor((g+1) NV / Hkv)); its blocks write
             // their partials to slots vb + g; the one unit starts at sequence 0
             const int ws0 = static_start(g, a.n_workers, a.n_kv_heads);
             const int ws1 = static_start(g + 1, a.n_workers, a.n_kv_heads);
             const int vb0 = ws0 / a.waves;
-            n = ws1 > ws0 ? (ws1 - 1) / a.waves - vb0 + 1 : 0;
-            p_first = (int64_t)(vb0 + g) * a.slot_rows + (int64_t)seq * a.group + (h - g * a.group);
+            m.n = ws1 > ws0 ? (ws1 - 1) / a.waves - vb0 + 1 : 0;
+            m.p_first = (int64_t)(vb0 + g) * a.slot_rows + (int64_t)seq * a.group + (h - g * a.group);
         } else {
             const int2 rec = *reinterpret_cast<const int2 *>(a.rowrec + (size_t)row * kRowRec);
             // a record that points outside the workspace (it cannot, unless the workspace was
@@ -56,105 +47,35 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
             const int64_t lim = (int64_t)a.n_slots * a.slot_rows;
             const bool ok = rec.y >= 0 && rec.x >= 0 && (int64_t)rec.x + (int64_t)max(rec.y - 1, 0) * a.slot_rows < lim;
             if (!ok && tid == 0) atomicOr(a.err, kErrBadSchedule);
-            p_first = rec.x;
-            n = ok ? rec.y : 0;
+            m.p_first = rec.x;
+            m.n = ok ? rec.y : 0;
         }
         if (a.step_mode) {
-            L = a.lens[seq];
-            if (row % a.n_q_heads == 0 && tid < a.n_kv_heads * APP) {
+            m.step = 1;
+            m.L = a.lens[seq];
+            m.max_len = a.max_suffix_len;
+            m.q_row = a.q + (size_t)row * HD;
+            m.k_row = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
+            m.v_row = a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD;
+            m.scale = a.scale;
+            if (h == 0 && tid < a.n_kv_heads * APP) {
                 const size_t src = ((size_t)seq * a.n_kv_heads + tid / APP) * HD + 8 * (tid % APP);
                 app_k = *reinterpret_cast<const uint4 *>(a.k_new + src);
                 app_v = *reinterpret_cast<const uint4 *>(a.v_new + src);
             }
-            if (slice == 0)
-                new_v = *reinterpret_cast<const uint2 *>(a.v_new + ((size_t)seq * a.n_kv_heads + g) * HD + 4 * chunk);
-            if (wave == 0) {  // q . k_new, wave 0 (used only when the token fits)
-                const uint16_t *qr = a.q + (size_t)row * HD;
-                const uint16_t *kr = a.k_new + ((size_t)seq * a.n_kv_heads + g) * HD;
-                for (int c = lane; c < HD; c += 64)
-                    dot += __uint_as_float((uint32_t)qr[c] << 16) * __uint_as_float((uint32_t)kr[c] << 16);
-            }
-            with_new = L < a.max_suffix_len;
         }
     } else {
-        n = a.n_parts;
-        p_first = row;
-        p_step = a.rows;
+        m.n = a.n_parts;
+        m.p_first = row;
+        m.p_step = a.rows;
     }
-    auto part_off = [&](int j) -> int64_t { return p_first + j * p_step; };
-
-    // Online merge of this slice's parts: running max m, weight sum w and accumulator (each
-    // part's lse and o are loaded together).  An empty part (lse = -inf) has weight 0; a NaN
-    // lse propagates.
-    float m = -INFINITY, w = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    constexpr int U = 4;  // parts loaded ahead of their use
-    for (int j0 = slice; j0 < n; j0 += U * SL) {
-        float l[U];
-        f32x4 o[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int j = j0 + u * SL;
-            l[u] = -INFINITY;
-            o[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (j < n) {
-                const int64_t off = part_off(j);
-                l[u] = a.part_lse[off];
-                o[u] = *reinterpret_cast<const f32x4 *>(a.part_o + (size_t)off * HD + 4 * chunk);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (l[u] == -INFINITY) continue;
-            const float mn = fmaxf(m, l[u]);
-            const float sc = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((m - mn) * kLog2e);
-            const float e = __builtin_amdgcn_exp2f((l[u] - mn) * kLog2e);
-            w = w * sc + e;
-            acc = acc * sc + e * o[u];
-            m = mn;
-        }
-    }
-    if (chunk == 0) {
-        s_m[slice] = m;
-        s_w[slice] = w;
-    }
-    s_acc[slice][chunk] = acc;
-    if (with_new && wave == 0) {
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) dot += __shfl_xor(dot, off);
-        if (lane == 0) s_new = dot * a.scale;
-    }
-    __syncthreads();
-    const float lse_new = with_new ? s_new : -INFINITY;
-    float M = lse_new;
-#pragma unroll
-    for (int k = 0; k < SL; ++k) M = fmaxf(M, s_m[k]);
-    if (slice == 0) {
-        f32x4 t = {0.f, 0.f, 0.f, 0.f};
-        float W = 0.f;
-        if (M != -INFINITY) {
-#pragma unroll
-            for (int k = 0; k < SL; ++k) {
-                const float sc = (s_m[k] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((s_m[k] - M) * kLog2e);
-                t += sc * s_acc[k][chunk];
-                W += sc * s_w[k];
-            }
-            if (with_new) {
-                const float e = __builtin_amdgcn_exp2f((lse_new - M) * kLog2e);
-                W += e;
-                t += e * f32x4{__uint_as_float(new_v.x << 16), __uint_as_float(new_v.x & 0xffff0000u),
-                               __uint_as_float(new_v.y << 16), __uint_as_float(new_v.y & 0xffff0000u)};
-            }
-        }
-        const f32x4 r = (W == 0.f) ? f32x4{0.f, 0.f, 0.f, 0.f} : t * __builtin_amdgcn_rcpf(W);
-        *reinterpret_cast<f32x4 *>(a.out + (size_t)row * HD + 4 * chunk) = r;
-        if (a.out_lse && chunk == 0) a.out_lse[row] = (W == 0.f) ? -INFINITY : M + logf(W);
-    }
+    merge_row<HD>(m, lds);
 
     // Fused step: block (s, head 0) stores the token sequence s appended (already attended
     // to from k_new / v_new) and advances suffix_len[s].  No block of this kernel reads the
     // suffix cache or suffix_len (the lengths come from the partial kernel), so nothing races.
     if (!a.step_mode || row % a.n_q_heads != 0) return;
+    const int L = m.L;
     bool ok = L < a.max_suffix_len;
     int page = 0;
     if (ok && a.paged) {
