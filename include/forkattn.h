@@ -122,6 +122,31 @@ fka_status fka_fork_decode(const fka_plan *plan, const void *q, const void *pref
                            float *out_lse, void *stream);
 
 /*
+ * fka_fork_decode without a plan and without allocating: for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * it).  heads and desc are those of fka_plan_create_contig, with share_prefix = 1; the
+ * schedule is the one such a plan gets (the same blocks and rounds for the same desc, so
+ * the same results bit for bit).  The partial results, the clamped lengths and a spare error
+ * word live in a 16 MiB array of the library's own, one per device, which a device holds from
+ * the first call on it until the process ends.  Nothing in it needs to start at zero, but
+ * every call on a device uses the same array: calls that overlap on one device (two streams,
+ * two threads) race and return garbage; order them.  The first call on each device looks up
+ * the array's address; later ones touch no allocator at all.
+ *   q ... out_lse   as in fka_fork_decode
+ *   err             int32 (device) or NULL: the call ORs into *err the flag bits that
+ *                   fka_plan_device_error describes (1: a suffix length was clamped); the
+ *                   caller clears it
+ * Errors: those of fka_plan_create_contig and fka_fork_decode; FKA_ERR_INVALID_ARG for
+ * share_prefix = 0; FKA_ERR_UNSUPPORTED when the decode needs more than the 16 MiB (the
+ * message says how much: (blocks x rounds + Hkv) x N x G x (d + 1) x 4 bytes of partials plus
+ * 4 N + 256 bytes) or the device id is 64 or more.
+ */
+fka_status fka_fork_decode_noalloc(const fka_heads *heads, const fka_contig_desc *desc, const void *q,
+                                   const void *prefix_k, const void *prefix_v, const void *suffix_k,
+                                   const void *suffix_v, const int32_t *suffix_len, float *out, float *out_lse,
+                                   int32_t *err, void *stream);
+
+/*
  * Append one token per branch (each branch decodes its own continuation,
  * Sec. 3.2): for every branch b, K/V row suffix_len[b] of every KV head is set to
  * k_new[b] / v_new[b] and suffix_len[b] is incremented.  A branch already at

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <set>
 #include <vector>
@@ -57,6 +58,10 @@ struct fka_pool {
     std::vector<int32_t> pending;  // references a call is about to drop, per page (zero between calls)
     std::vector<int32_t> touched;  // pages with a pending count
 };
+
+// Scratch of the no-allocation decode, one copy per device (see scratch_of below).
+constexpr size_t kScratchBytes = size_t(16) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
 
 namespace {
 
@@ -130,42 +135,16 @@ fka_status check_grid(int32_t rounds, int32_t blocks)
 // device.
 constexpr int32_t kMinSlicesPerWave = 2;
 
-// Prefix units in order: unit u covers sequences [seq0, seq0 + nseq) that share a prefix of
-// n_tok tokens.  Builds the unit table, the per-sequence prefix lengths, the slot geometry,
-// the grid and the round count.
-fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>> &units, int32_t rounds_req,
-                          int32_t blocks_req)
+// The grid for a schedule with n_units units of at most max_nseq sequences and est slices per
+// KV head with every suffix at max_suffix_len: slot geometry, blocks, rounds and slots.  Touches
+// no memory beyond the plan's fields (the no-allocation decode calls it too).
+fka_status set_grid(fka_plan *p, int64_t est, int32_t max_nseq, int32_t n_units, int32_t rounds_req, int32_t blocks_req)
 {
-    p->units.clear();
-    p->seq_prefix_len.assign(p->n_seqs, 0);
-    // token counts stay far enough below 2^31 that ceil(tokens / kSlice) cannot overflow
-    constexpr int32_t kMaxTokens = 1 << 30;
-    if (p->max_suffix_len > kMaxTokens)
-        return fail(FKA_ERR_UNSUPPORTED, "max_suffix_len %d is too long (limit %d)", p->max_suffix_len, kMaxTokens);
-    for (const auto &u : units)
-        if (u[2] > kMaxTokens) return fail(FKA_ERR_UNSUPPORTED, "prefix of %d tokens is too long (limit %d)", u[2], kMaxTokens);
-    int64_t c = 0;
-    int32_t max_nseq = 1;
-    int64_t est = 0;  // slices per KV head with every suffix at max_suffix_len
-    for (size_t u = 0; u < units.size(); ++u) {
-        const int32_t seq0 = units[u][0], nseq = units[u][1], n_tok = units[u][2];
-        max_nseq = std::max(max_nseq, nseq);
-        for (int32_t i = seq0; i < seq0 + nseq; ++i) p->seq_prefix_len[i] = n_tok;
-        fka::UnitRec r{};
-        r.seq0 = seq0;
-        r.nseq = nseq;
-        r.plen = n_tok;
-        r.ps_before = (int32_t)c;
-        p->units.push_back(r);
-        c += fka::slices_of(n_tok);
-        est += fka::slices_of(n_tok) + (int64_t)nseq * fka::slices_of(p->max_suffix_len);
-    }
     // the schedule's total slices (every item at its longest, over all KV heads) stay in int32
     if (est * p->Hkv > (int64_t)1 << 30)
         return fail(FKA_ERR_UNSUPPORTED, "prefix and suffixes of %lld slices are too long", (long long)(est * p->Hkv));
-    p->ps_total = (int32_t)c;
-    p->static_split = units.size() == 1;
-    p->n_items = (int32_t)units.size() * p->Hkv;
+    p->static_split = n_units == 1;
+    p->n_items = n_units * p->Hkv;
     p->slot_rows = max_nseq * p->G;
     p->row_tiles = ceil_div(p->slot_rows, 16);
 
@@ -193,6 +172,41 @@ fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>>
     p->rounds = std::max<int32_t>(std::max<int32_t>(1, need), rounds_req);
     p->n_slots = p->n_blocks * p->rounds + p->n_items;
     return FKA_OK;
+}
+
+// token counts stay far enough below 2^31 that ceil(tokens / kSlice) cannot overflow
+constexpr int32_t kMaxTokens = 1 << 30;
+
+// Prefix units in order: unit u covers sequences [seq0, seq0 + nseq) that share a prefix of
+// n_tok tokens.  Builds the unit table, the per-sequence prefix lengths, the slot geometry,
+// the grid and the round count.
+fka_status build_schedule(fka_plan *p, const std::vector<std::array<int32_t, 3>> &units, int32_t rounds_req,
+                          int32_t blocks_req)
+{
+    p->units.clear();
+    p->seq_prefix_len.assign(p->n_seqs, 0);
+    if (p->max_suffix_len > kMaxTokens)
+        return fail(FKA_ERR_UNSUPPORTED, "max_suffix_len %d is too long (limit %d)", p->max_suffix_len, kMaxTokens);
+    for (const auto &u : units)
+        if (u[2] > kMaxTokens) return fail(FKA_ERR_UNSUPPORTED, "prefix of %d tokens is too long (limit %d)", u[2], kMaxTokens);
+    int64_t c = 0;
+    int32_t max_nseq = 1;
+    int64_t est = 0;  // slices per KV head with every suffix at max_suffix_len
+    for (size_t u = 0; u < units.size(); ++u) {
+        const int32_t seq0 = units[u][0], nseq = units[u][1], n_tok = units[u][2];
+        max_nseq = std::max(max_nseq, nseq);
+        for (int32_t i = seq0; i < seq0 + nseq; ++i) p->seq_prefix_len[i] = n_tok;
+        fka::UnitRec r{};
+        r.seq0 = seq0;
+        r.nseq = nseq;
+        r.plen = n_tok;
+        r.ps_before = (int32_t)c;
+        p->units.push_back(r);
+        c += fka::slices_of(n_tok);
+        est += fka::slices_of(n_tok) + (int64_t)nseq * fka::slices_of(p->max_suffix_len);
+    }
+    p->ps_total = (int32_t)c;
+    return set_grid(p, est, max_nseq, (int32_t)units.size(), rounds_req, blocks_req);
 }
 
 // Allocate device memory for the unit table, the error flag, the merge records, the lengths
@@ -246,6 +260,27 @@ fka_status finish_plan(fka_plan *p)
                   "hipMemcpy(sequence tables)")) != FKA_OK)
         return st;
     if ((e = hipMemset(zero, 0, b_zero)) != hipSuccess) return hip_fail(e, "hipMemset(flags and records)");
+    return FKA_OK;
+}
+
+fka_status check_contig(const fka_heads *heads, const fka_contig_desc *desc)
+{
+    fka_status st = check_heads(heads);
+    if (st != FKA_OK) return st;
+    REQUIRE(desc != nullptr, "desc is null");
+    REQUIRE(desc->n_branches >= 1, "n_branches (%d) must be >= 1", desc->n_branches);
+    REQUIRE(desc->prefix_len >= 0, "prefix_len (%d) must be >= 0", desc->prefix_len);
+    REQUIRE(desc->suffix_cap >= 1, "suffix_cap (%d) must be >= 1", desc->suffix_cap);
+    REQUIRE(desc->max_suffix_len >= 0 && desc->max_suffix_len <= desc->suffix_cap,
+            "max_suffix_len (%d) must be in [0, suffix_cap=%d]", desc->max_suffix_len, desc->suffix_cap);
+    REQUIRE(desc->share_prefix == 0 || desc->share_prefix == 1, "share_prefix must be 0 or 1");
+    if ((st = check_grid(desc->rounds, desc->blocks)) != FKA_OK) return st;
+    if (desc->n_branches > fka::kMaxSeqs)
+        return fail(FKA_ERR_UNSUPPORTED, "%d sequences exceed the limit of %d", desc->n_branches, fka::kMaxSeqs);
+    const int G = heads->n_q_heads / heads->n_kv_heads;
+    const int rows = (desc->share_prefix ? desc->n_branches : 1) * G;
+    if (G > fka::kMaxRows || rows > fka::kMaxRows)
+        return fail(FKA_ERR_UNSUPPORTED, "%d query rows per KV head exceed the limit of %d", rows, fka::kMaxRows);
     return FKA_OK;
 }
 
@@ -322,6 +357,33 @@ fka_status run_decode(const fka_plan *p, const fka::AttnArgs &a, const int32_t *
     return ok();
 }
 
+// ---------------------------------------------------------------------------------------
+// Scratch of the no-allocation decode (fka_fork_decode_noalloc): the device memory one decode
+// needs beyond its inputs and outputs -- the partial results, the clamped lengths and an error
+// word -- in a file-scope array, so that the call allocates nothing.  Each device holds its own
+// copy from the library's load until the process ends.  Host code reaches it only through the
+// device address hipGetSymbolAddress returns (the array's name is a host-side stand-in).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices];  // device address of each device's scratch, once looked up
+
+// This device's scratch address, looked up on the first call on the device (which is current).
+fka_status scratch_of(int device, char **out)
+{
+    if (device < 0 || device >= kMaxDevices)
+        return fail(FKA_ERR_UNSUPPORTED, "device %d: the no-allocation decode serves devices 0..%d", device, kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return fail(FKA_ERR_HIP, "hipGetSymbolAddress(scratch) returned null");
+        g_scratch_ptr[device] = static_cast<char *>(ptr);
+    }
+    *out = g_scratch_ptr[device];
+    return FKA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -334,22 +396,8 @@ fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc 
 {
     REQUIRE(out != nullptr, "out is null");
     *out = nullptr;
-    fka_status st = check_heads(heads);
+    fka_status st = check_contig(heads, desc);
     if (st != FKA_OK) return st;
-    REQUIRE(desc != nullptr, "desc is null");
-    REQUIRE(desc->n_branches >= 1, "n_branches (%d) must be >= 1", desc->n_branches);
-    REQUIRE(desc->prefix_len >= 0, "prefix_len (%d) must be >= 0", desc->prefix_len);
-    REQUIRE(desc->suffix_cap >= 1, "suffix_cap (%d) must be >= 1", desc->suffix_cap);
-    REQUIRE(desc->max_suffix_len >= 0 && desc->max_suffix_len <= desc->suffix_cap,
-            "max_suffix_len (%d) must be in [0, suffix_cap=%d]", desc->max_suffix_len, desc->suffix_cap);
-    REQUIRE(desc->share_prefix == 0 || desc->share_prefix == 1, "share_prefix must be 0 or 1");
-    if ((st = check_grid(desc->rounds, desc->blocks)) != FKA_OK) return st;
-    if (desc->n_branches > fka::kMaxSeqs)
-        return fail(FKA_ERR_UNSUPPORTED, "%d sequences exceed the limit of %d", desc->n_branches, fka::kMaxSeqs);
-    const int G = heads->n_q_heads / heads->n_kv_heads;
-    const int rows = (desc->share_prefix ? desc->n_branches : 1) * G;
-    if (G > fka::kMaxRows || rows > fka::kMaxRows)
-        return fail(FKA_ERR_UNSUPPORTED, "%d query rows per KV head exceed the limit of %d", rows, fka::kMaxRows);
 
     fka_plan *p = new (std::nothrow) fka_plan();
     if (!p) return fail(FKA_ERR_NOMEM, "host allocation failed");
@@ -537,6 +585,64 @@ fka_status fka_fork_decode(const fka_plan *p, const void *q, const void *prefix_
     a.suffix_v = static_cast<const uint16_t *>(suffix_v);
     a.suffix_len = suffix_len;
     return run_decode(p, a, suffix_len, out, out_lse, static_cast<hipStream_t>(stream));
+}
+
+fka_status fka_fork_decode_noalloc(const fka_heads *heads, const fka_contig_desc *desc, const void *q,
+                                   const void *prefix_k, const void *prefix_v, const void *suffix_k,
+                                   const void *suffix_v, const int32_t *suffix_len, float *out, float *out_lse,
+                                   int32_t *err, void *stream)
+{
+    fka_status st = check_contig(heads, desc);
+    if (st != FKA_OK) return st;
+    REQUIRE(desc->share_prefix == 1, "the no-allocation decode takes a shared prefix (share_prefix = 1)");
+    if (desc->prefix_len > kMaxTokens || desc->max_suffix_len > kMaxTokens)
+        return fail(FKA_ERR_UNSUPPORTED, "prefix or suffix longer than %d tokens", kMaxTokens);
+    REQUIRE_PTR16(q);
+    if (desc->prefix_len > 0) {
+        REQUIRE_PTR16(prefix_k);
+        REQUIRE_PTR16(prefix_v);
+    }
+    REQUIRE_PTR16(suffix_k);
+    REQUIRE_PTR16(suffix_v);
+    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR16(out);
+    // The plan of fka_plan_create_contig, built on the stack: the scalar fields only (its tables
+    // stay empty and unallocated; the one-unit schedule reads none of them).
+    fka_plan p;
+    init_heads(&p, heads);
+    p.n_seqs = desc->n_branches;
+    p.share_prefix = 1;
+    p.prefix_len = desc->prefix_len;
+    p.suffix_cap = desc->suffix_cap;
+    p.max_suffix_len = desc->max_suffix_len;
+    p.ps_total = fka::slices_of(desc->prefix_len);
+    const int64_t est = fka::slices_of(desc->prefix_len) + (int64_t)desc->n_branches * fka::slices_of(desc->max_suffix_len);
+    if ((st = set_grid(&p, est, desc->n_branches, 1, desc->rounds, desc->blocks)) != FKA_OK) return st;
+    // scratch: lengths, error word, partial lse, partial o; every word a call reads, the same
+    // call writes first, so nothing needs clearing
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    const size_t parts = (size_t)p.n_slots * p.slot_rows;
+    const size_t b_lens = up((size_t)p.n_seqs * sizeof(int32_t)), b_err = 256;
+    const size_t b_pl = up(parts * sizeof(float)), b_po = up(parts * p.d * sizeof(float));
+    const size_t need = b_lens + b_err + b_pl + b_po;
+    if (need > kScratchBytes)
+        return fail(FKA_ERR_UNSUPPORTED, "this decode needs %zu bytes of scratch; the no-allocation decode has %zu (use a plan)",
+                    need, kScratchBytes);
+    char *base = nullptr;
+    if ((st = scratch_of(p.device, &base)) != FKA_OK) return st;
+    p.d_lens = reinterpret_cast<int32_t *>(base);
+    p.d_rowrec = p.d_lens;  // not read by a one-unit schedule
+    p.err = err ? err : reinterpret_cast<int32_t *>(base + b_lens);
+    p.part_lse = reinterpret_cast<float *>(base + b_lens + b_err);
+    p.part_o = reinterpret_cast<float *>(base + b_lens + b_err + b_pl);
+    fka::AttnArgs a = attn_args(&p);
+    a.q = static_cast<const uint16_t *>(q);
+    a.prefix_k = static_cast<const uint16_t *>(prefix_k);
+    a.prefix_v = static_cast<const uint16_t *>(prefix_v);
+    a.suffix_k = static_cast<const uint16_t *>(suffix_k);
+    a.suffix_v = static_cast<const uint16_t *>(suffix_v);
+    a.suffix_len = suffix_len;
+    return run_decode(&p, a, suffix_len, out, out_lse, static_cast<hipStream_t>(stream));
 }
 
 fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, const void *prefix_v,

@@ -69,6 +69,7 @@ _sig = {
     "fka_gather_paged": ([_vp, C.c_int32, _vp, _vp, _vp, C.c_int32, _vp, _vp, _vp], C.c_int),
     "fka_gather_paged_range": ([_vp, C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp], C.c_int),
     "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
+    "fka_fork_decode_noalloc": ([C.POINTER(Heads), C.POINTER(ContigDesc)] + [_vp] * 10, C.c_int),
     "fka_plan_slots": ([_vp, _vp, _vp, C.c_int32, C.POINTER(C.c_int32)], C.c_int),
     "fka_partials": ([_vp] * 10, C.c_int),
     "fka_partials_paged": ([_vp] * 9, C.c_int),
@@ -360,6 +361,20 @@ def read_probe(buf, blocks, threads, unroll, sink, stream=None):
     """Read-only streaming probe over the device tensor buf (fka_read_probe)."""
     _check(_lib.fka_read_probe(_p(buf), buf.numel() * buf.element_size(), int(blocks), int(threads), int(unroll),
                                _p(sink), _stream(stream)))
+
+
+def decode_noalloc(n_q_heads, n_kv_heads, head_dim, prefix_len, suffix_cap, max_suffix_len, q, prefix_k, prefix_v,
+                   suffix_k, suffix_v, suffix_len, out, out_lse=None, err=None, rounds=0, softmax_scale=0.0, blocks=0,
+                   stream=None):
+    """fka_fork_decode_noalloc: a shared-prefix decode without a plan, on the library's static scratch
+    (the sizes are those of Plan.contig with share_prefix=True; n_branches is q's first dimension)."""
+    dev = q.get_device() if isinstance(q, torch.Tensor) and q.is_cuda else None
+    h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
+    d = ContigDesc(q.shape[0], prefix_len, suffix_cap, max_suffix_len, 1, rounds, blocks)
+    _check(_lib.fka_fork_decode_noalloc(C.byref(h), C.byref(d), _p(q, "bf16", dev), _p(prefix_k, "bf16", dev),
+                                        _p(prefix_v, "bf16", dev), _p(suffix_k, "bf16", dev), _p(suffix_v, "bf16", dev),
+                                        _p(suffix_len, "i32", dev), _p(out, "f32", dev), _p(out_lse, "f32", dev),
+                                        _p(err, "i32", dev), _stream(stream)))
 
 
 def lse_merge(part_o, part_lse, out, out_lse=None, stream=None):
