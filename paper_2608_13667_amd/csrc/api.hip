@@ -88,6 +88,7 @@ fka_status hip_fail(hipError_t e, const char *what)
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 #define REQUIRE(cond, ...)                                  \
     do {                                                    \
@@ -98,6 +99,17 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
     do {                                                                          \
         if (!(p)) return fail(FKA_ERR_INVALID_ARG, "%s is null", #p);             \
         if (!aligned16(p)) return fail(FKA_ERR_INVALID_ARG, "%s is not 16-byte aligned", #p); \
+    } while (0)
+
+// int32 / fp32 arrays: non-null and 4-byte aligned (REQUIRE_OPT4: or null)
+#define REQUIRE_PTR4(p)                                                           \
+    do {                                                                          \
+        if (!(p)) return fail(FKA_ERR_INVALID_ARG, "%s is null", #p);             \
+        if (!aligned4(p)) return fail(FKA_ERR_INVALID_ARG, "%s is not 4-byte aligned", #p); \
+    } while (0)
+#define REQUIRE_OPT4(p)                                                           \
+    do {                                                                          \
+        if ((p) && !aligned4(p)) return fail(FKA_ERR_INVALID_ARG, "%s is not 4-byte aligned", #p); \
     } while (0)
 
 fka_status check_heads(const fka_heads *h)
@@ -575,8 +587,9 @@ fka_status fka_fork_decode(const fka_plan *p, const void *q, const void *prefix_
     }
     REQUIRE_PTR16(suffix_k);
     REQUIRE_PTR16(suffix_v);
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(suffix_len);
     REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
     fka::AttnArgs a = attn_args(p);
     a.q = static_cast<const uint16_t *>(q);
     a.prefix_k = static_cast<const uint16_t *>(prefix_k);
@@ -604,8 +617,10 @@ fka_status fka_fork_decode_noalloc(const fka_heads *heads, const fka_contig_desc
     }
     REQUIRE_PTR16(suffix_k);
     REQUIRE_PTR16(suffix_v);
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(suffix_len);
     REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
+    REQUIRE_OPT4(err);
     // The plan of fka_plan_create_contig, built on the stack: the scalar fields only (its tables
     // stay empty and unallocated; the one-unit schedule reads none of them).
     fka_plan p;
@@ -658,9 +673,9 @@ fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, 
     }
     REQUIRE_PTR16(suffix_k);
     REQUIRE_PTR16(suffix_v);
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(suffix_len);
     REQUIRE_PTR16(part_o);
-    REQUIRE(part_lse != nullptr, "part_lse is null");
+    REQUIRE_PTR4(part_lse);
     fka::AttnArgs a = attn_args(p);
     a.q = static_cast<const uint16_t *>(q);
     a.prefix_k = static_cast<const uint16_t *>(prefix_k);
@@ -684,10 +699,10 @@ fka_status fka_partials_paged(const fka_plan *p, const void *q, const void *k_po
     REQUIRE_PTR16(q);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
-    REQUIRE(page_table != nullptr, "page_table is null");
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(page_table);
+    REQUIRE_PTR4(suffix_len);
     REQUIRE_PTR16(part_o);
-    REQUIRE(part_lse != nullptr, "part_lse is null");
+    REQUIRE_PTR4(part_lse);
     fka::AttnArgs a = attn_args(p);
     a.q = static_cast<const uint16_t *>(q);
     a.k_pool = static_cast<const uint16_t *>(k_pool);
@@ -710,7 +725,7 @@ fka_status fka_append_kv(const fka_plan *p, const void *k_new, const void *v_new
     REQUIRE_PTR16(v_new);
     REQUIRE_PTR16(suffix_k);
     REQUIRE_PTR16(suffix_v);
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(suffix_len);
     fka::AppendArgs a{};
     a.k_new = static_cast<const uint16_t *>(k_new);
     a.v_new = static_cast<const uint16_t *>(v_new);
@@ -743,8 +758,9 @@ fka_status fka_fork_step(const fka_plan *p, const void *q, const void *k_new, co
     }
     REQUIRE_PTR16(suffix_k);
     REQUIRE_PTR16(suffix_v);
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(suffix_len);
     REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
     fka::AttnArgs a = attn_args(p);
     a.q = static_cast<const uint16_t *>(q);
     a.prefix_k = static_cast<const uint16_t *>(prefix_k);
@@ -773,9 +789,10 @@ fka_status fka_fork_step_paged(const fka_plan *p, const void *q, const void *k_n
     REQUIRE_PTR16(v_new);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
-    REQUIRE(page_table != nullptr, "page_table is null");
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(page_table);
+    REQUIRE_PTR4(suffix_len);
     REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
     fka::AttnArgs a = attn_args(p);
     a.q = static_cast<const uint16_t *>(q);
     a.k_pool = static_cast<const uint16_t *>(k_pool);
@@ -802,9 +819,10 @@ fka_status fka_fork_decode_paged(const fka_plan *p, const void *q, const void *k
     REQUIRE_PTR16(q);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
-    REQUIRE(page_table != nullptr, "page_table is null");
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(page_table);
+    REQUIRE_PTR4(suffix_len);
     REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
     fka::AttnArgs a = attn_args(p);
     a.q = static_cast<const uint16_t *>(q);
     a.k_pool = static_cast<const uint16_t *>(k_pool);
@@ -823,8 +841,8 @@ fka_status fka_append_kv_paged(const fka_plan *p, const void *k_new, const void 
     REQUIRE_PTR16(v_new);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
-    REQUIRE(page_table != nullptr, "page_table is null");
-    REQUIRE(suffix_len != nullptr, "suffix_len is null");
+    REQUIRE_PTR4(page_table);
+    REQUIRE_PTR4(suffix_len);
     fka::AppendArgs a{};
     a.k_new = static_cast<const uint16_t *>(k_new);
     a.v_new = static_cast<const uint16_t *>(v_new);
@@ -860,7 +878,7 @@ fka_status fka_gather_paged_range(const fka_plan *p, int32_t seq, int32_t begin,
     REQUIRE(seq >= 0 && seq < p->n_seqs, "seq %d out of range [0, %d)", seq, p->n_seqs);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
-    REQUIRE(page_table != nullptr, "page_table is null");
+    REQUIRE_PTR4(page_table);
     REQUIRE_PTR16(k_out);
     REQUIRE_PTR16(v_out);
     int t = 0;
@@ -899,9 +917,14 @@ fka_status fka_lse_merge(int32_t rows, int32_t n_parts, int32_t head_dim, const 
         return fail(FKA_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", head_dim);
     if (rows == 0) return ok();
     if (n_parts > 0) {
-        REQUIRE(part_o != nullptr && part_lse != nullptr, "part arrays are null");
+        REQUIRE_PTR16(part_o);
+        REQUIRE_PTR4(part_lse);
+        // the merge addresses the parts with 32-bit byte offsets
+        if ((int64_t)n_parts * rows * head_dim * 4 >= ((int64_t)1 << 31))
+            return fail(FKA_ERR_UNSUPPORTED, "%d parts of %d rows exceed the 2 GiB the merge addresses", n_parts, rows);
     }
-    REQUIRE(out != nullptr, "out is null");
+    REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
     fka::MergeArgs m{};
     m.part_o = part_o;
     m.part_lse = part_lse;
@@ -919,7 +942,7 @@ fka_status fka_read_probe(const void *buf, size_t bytes, int32_t blocks, int32_t
                           uint32_t *sink, void *stream)
 {
     REQUIRE_PTR16(buf);
-    REQUIRE(sink != nullptr, "sink is null");
+    REQUIRE_PTR4(sink);
     REQUIRE(bytes > 0 && bytes % 16 == 0, "bytes (%zu) must be a positive multiple of 16", bytes);
     REQUIRE(blocks >= 1, "blocks (%d) must be >= 1", blocks);
     REQUIRE(threads >= 64 && threads <= 1024 && threads % 64 == 0, "threads (%d) must be a multiple of 64 in [64, 1024]",
@@ -1183,7 +1206,8 @@ fka_status fka_scatter_pages(const void *k_src, const void *v_src, int32_t len, 
     REQUIRE_PTR16(v_src);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
-    REQUIRE(page_row != nullptr, "page_row is null");
+    REQUIRE_PTR4(page_row);
+    REQUIRE_OPT4(err);
     fka::ScatterArgs s{};
     s.k_src = static_cast<const uint16_t *>(k_src);
     s.v_src = static_cast<const uint16_t *>(v_src);

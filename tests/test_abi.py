@@ -138,3 +138,66 @@ def test_binding_rejects_host_and_mistyped_tensors(fa):
 def test_plan_create_rejects_negative_blocks(fa):
     st, out = _create(fa, _heads(fa), fa.ContigDesc(5, 512, 64, 64, 1, 0, -1))
     assert st == -1 and "blocks" in fa.last_error() and not out.value
+
+
+def test_misaligned_pointers_are_rejected(fa):
+    """Pointers are checked for alignment before anything is launched or dereferenced: 16 bytes for
+    bf16 rows and fp32 outputs, 4 for int32 / fp32 arrays.  The addresses here are never read (the
+    checks run first), so no GPU is needed."""
+    vp = C.c_void_p
+    a16, a8, a2 = vp(0x10000), vp(0x10008), vp(0x10002)
+    assert fa.raw_call("fka_lse_merge", 4, 2, 64, a8, a16, a16, None, None) == -1
+    assert "part_o is not 16-byte aligned" in fa.last_error()
+    assert fa.raw_call("fka_lse_merge", 4, 2, 64, a16, a2, a16, None, None) == -1
+    assert "part_lse is not 4-byte aligned" in fa.last_error()
+    assert fa.raw_call("fka_lse_merge", 4, 2, 64, a16, a16, a8, None, None) == -1
+    assert "out is not 16-byte aligned" in fa.last_error()
+    assert fa.raw_call("fka_lse_merge", 4, 2, 64, a16, a16, a16, a2, None) == -1
+    assert "out_lse is not 4-byte aligned" in fa.last_error()
+    assert fa.raw_call("fka_read_probe", a8, C.c_size_t(4096), 1, 64, 4, a16, None) == -1
+    assert "buf is not 16-byte aligned" in fa.last_error()
+    assert fa.raw_call("fka_scatter_pages", a8, a16, 16, 0, a16, 1, 128, 4, a16, a16, None, None) == -1
+    assert "k_src is not 16-byte aligned" in fa.last_error()
+    assert fa.raw_call("fka_scatter_pages", a16, a16, 16, 0, a2, 1, 128, 4, a16, a16, None, None) == -1
+    assert "page_row is not 4-byte aligned" in fa.last_error()
+    h = _heads(fa)
+    d = fa.ContigDesc(5, 512, 64, 64, 1, 0, 0)
+    good = [a16] * 5 + [a16, a16, None, None]  # q, prefix k/v, suffix k/v, suffix_len, out, out_lse, err
+    for i, name, bad in [(0, "q", a8), (1, "prefix_k", a8), (4, "suffix_v", a8), (5, "suffix_len", a2),
+                         (6, "out", a8), (7, "out_lse", a2), (8, "err", a2)]:
+        args = list(good)
+        args[i] = bad
+        assert fa.raw_call("fka_fork_decode_noalloc", C.byref(h), C.byref(d), *args, None) == -1, name
+        assert f"{name} is not" in fa.last_error(), (name, fa.last_error())
+
+
+@pytest.mark.gpu
+def test_misaligned_pointers_are_rejected_by_plan_calls(fa):
+    """The plan entry points refuse views offset from 16-byte (bf16 rows, fp32 outputs) or 4-byte
+    (lengths, tables, lse) alignment with FKA_ERR_INVALID_ARG and launch nothing."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    plan = fa.Plan.contig(8, 2, 64, 3, 128, 32, 32)
+    N, Hq, d = 3, 8, 64
+    buf = torch.zeros(1 << 20, dtype=torch.bfloat16, device="cuda")
+    i32 = torch.zeros(64, dtype=torch.int32, device="cuda")
+    f32 = torch.zeros(1 << 16, dtype=torch.float32, device="cuda")
+    vp = C.c_void_p
+    b16, b8 = vp(buf.data_ptr()), vp(buf.data_ptr() + 8)
+    i4, i2 = vp(i32.data_ptr()), vp(i32.data_ptr() + 2)
+    f16, f8, f2 = vp(f32.data_ptr()), vp(f32.data_ptr() + 8), vp(f32.data_ptr() + 2)
+    h = vp(plan._h)
+    good = [b16, b16, b16, b16, b16, i4, f16, f16]  # q, prefix k/v, suffix k/v, suffix_len, out, out_lse
+    for i, name, bad in [(0, "q", b8), (2, "prefix_v", b8), (3, "suffix_k", b8), (5, "suffix_len", i2),
+                         (6, "out", f8), (7, "out_lse", f2)]:
+        args = list(good)
+        args[i] = bad
+        assert fa.raw_call("fka_fork_decode", h, *args, None) == -1, name
+        assert f"{name} is not" in fa.last_error(), (name, fa.last_error())
+    assert fa.raw_call("fka_partials", h, b16, b16, b16, b16, b16, i4, f8, f16, None) == -1
+    assert "part_o is not 16-byte aligned" in fa.last_error()
+    assert fa.raw_call("fka_partials", h, b16, b16, b16, b16, b16, i4, f16, f2, None) == -1
+    assert "part_lse is not 4-byte aligned" in fa.last_error()
+    torch.cuda.synchronize()
+    assert plan.device_error() == 0
