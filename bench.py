@@ -88,6 +88,7 @@ def parse():
     ap.add_argument("--no-naive", action="store_true", help="skip the naive per-branch GPU baseline")
     ap.add_argument("--no-probe", action="store_true", help="skip the read-bandwidth probe")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-prefill", action="store_true", help="skip the instruction-prefill timing")
     ap.add_argument("--lifecycle", action="store_true",
                     help="also time the fork lifecycle on the page pool (contiguous workloads' shapes)")
     return ap.parse_args()
@@ -434,6 +435,72 @@ def lifecycle_timing(fa, torch, w):
             "prefill_chunk": {"tokens_per_branch": n, "us": pf_s * 1e6, "kv_gbps": pf_bytes / pf_s / 1e9}}
 
 
+def prefill_timing(torch, fa, W, ns, trials):
+    """Instruction prefill at the 32k-prefix shape (fka_prefill): every branch takes n instruction
+    tokens at the fork (existing suffixes empty).  HBM-cold: the calls cycle over prefix replicas
+    totalling 3x the 256 MiB MALL.  Per n: us per call and per token, effective K/V GB/s (the
+    prefix once, each branch's instruction once) against 8 TB/s, and MFMA TFLOP/s (4 Lp d per
+    query row: q.k and p.v over the prefix) against the 2.5 PFLOP/s bf16 peak."""
+    n_max = max(ns)
+    w = W.make("long", steps=n_max, suffix_range=(0, 0), seed=2700)
+    s = w.spec
+    N, Hq, Hkv, d, Lp = w.q.shape[0], s.n_q_heads, s.n_kv_heads, s.head_dim, w.prefix_len
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    sk, sv = w.suffix_k.copy(), w.suffix_v.copy()
+    for b in range(N):
+        sk[b, :, :n_max] = w.step_k[:n_max, b].transpose(1, 0, 2)
+        sv[b, :, :n_max] = w.step_v[:n_max, b].transpose(1, 0, 2)
+    q_all = w.step_q.transpose(1, 0, 2, 3)
+    pref_bytes = 2 * Hkv * Lp * d * 2
+    R = max(2, math.ceil(3 * 256 * 2**20 / pref_bytes))
+    pk0, pv0 = dev(w.prefix_k), dev(w.prefix_v)
+    reps = [(pk0, pv0)] + [(pk0.clone(), pv0.clone()) for _ in range(R - 1)]
+    skd, svd = dev(sk), dev(sv)
+    len0 = torch.zeros(N, dtype=torch.int32, device="cuda")
+    cap = w.suffix_cap
+    res = {"workload": "long: 40 query / 8 KV heads, d 128, 32768-token prefix, 5 branches, empty suffixes",
+           "replicas": R, "cold": "calls cycle over prefix replicas of 3x the MALL"}
+    for n in ns:
+        plan = fa.Plan.prefill_plan(Hq, Hkv, d, N, n, Lp, cap, cap)
+        info = plan.info()
+        q = dev(np.ascontiguousarray(q_all[:, :n]))
+        out = torch.empty((N, n, Hq, d), device="cuda")
+        lse = torch.empty((N, n, Hq), device="cuda")
+
+        def body(k):
+            for i in range(k):
+                pk, pv = reps[i % R]
+                plan.prefill(q, pk, pv, skd, svd, len0, out, lse)
+
+        K = 4 * R
+        body(2 * R)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            body(K)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(trials):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3 / K)
+        t = float(np.median(ts))
+        kv = pref_bytes + N * n * 2 * Hkv * d * 2
+        flop = 4.0 * Hq * N * n * Lp * d
+        res[f"n{n}"] = {"us_per_call": t * 1e6, "us_per_token": t * 1e6 / (N * n), "effective_kv_gbps": kv / t / 1e9,
+                        "hbm_peak_frac": kv / t / 8e12, "tflops": flop / t / 1e12, "mfma_bf16_peak_frac": flop / t / 2.5e15,
+                        "units": info.n_units, "blocks": info.n_blocks, "trials_us": [x * 1e6 for x in ts]}
+        log(f"[bench] prefill n={n}: {t * 1e6:.1f} us per call ({t * 1e6 / (N * n):.2f} us/token), "
+            f"{kv / t / 1e9:.0f} GB/s ({kv / t / 8e12:.1%} of 8 TB/s), {flop / t / 1e12:.0f} TFLOP/s "
+            f"({flop / t / 2.5e15:.1%} of 2.5 PFLOP/s); {info.n_units} units, {info.n_blocks} blocks")
+        del plan, graph
+    del reps
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -473,6 +540,10 @@ def main():
         b.release()
         del b
 
+    prefill = None
+    if not args.no_prefill:
+        prefill = prefill_timing(torch, fa, W, (1, 16, 64), args.trials)
+
     probe = None
     if not args.no_probe:
         probe = read_probe(torch, fa, {"main_workload_bytes": main_bytes, "1GiB": 1 << 30})
@@ -507,6 +578,8 @@ def main():
         res["achievable_read_frac"] = {"step": rec["effective_kv_gbps"] / best,
                                        "partial_kernel": rec["roofline"]["achieved"] / best}
     res["sub_workloads"] = subs
+    if prefill:
+        res["instruction_prefill"] = prefill
     if lifecycle:
         res["lifecycle"] = lifecycle
     print(json.dumps(res), flush=True)

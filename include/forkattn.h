@@ -310,6 +310,53 @@ fka_status fka_scatter_pages(const void *k_src, const void *v_src, int32_t len, 
                              const int32_t *page_row, int32_t n_kv_heads, int32_t head_dim, int32_t n_pool_pages,
                              void *k_pool, void *v_pool, int32_t *err, void *stream);
 
+/* -------------------------------------------------------------- instruction prefill */
+
+/* Branch-instruction prefill at the fork (Sec. 3.3: each branch continues from the snapshot
+ * of the shared context followed by a short instruction of its own; Sec. 4.4: a branch's load
+ * is dominated by prefill over the cached prefix).  Every branch b takes n_tokens instruction
+ * tokens at once: token t's queries attend to the whole shared prefix and, causally, to b's
+ * suffix up to and including its own position (suffix positions [0, suffix_len[b] + t]).
+ * The plan splits the N x n_tokens tokens into units of consecutive tokens, at most 64 query
+ * rows (tokens x G) per KV head each; all units stream the same prefix, and the blocks that
+ * read one prefix range for different units run together on one XCD (block vb holds work
+ * item vb mod n_items), so each prefix tile is fetched from HBM once and served to the other
+ * units from that XCD's L2.  Then the merge stage combines each row's partials. */
+typedef struct {
+    int32_t n_branches;      /* N, >= 1 */
+    int32_t n_tokens;        /* n instruction tokens per branch, >= 1; N x n <= 512 */
+    int32_t prefix_len;      /* Lp, >= 0 */
+    int32_t suffix_cap;      /* rows of each branch's suffix buffer */
+    int32_t max_suffix_len;  /* bound on suffix_len[b] + n_tokens, in [n_tokens, suffix_cap] */
+    int32_t blocks;          /* 0 = automatic (fill the device); else about this many blocks */
+} fka_prefill_desc;
+
+/* Build an instruction-prefill plan (device workspace as fka_plan_create_contig).  Only
+ * fka_prefill, fka_plan_get_info, fka_plan_device_error and fka_plan_destroy take it.
+ * Errors: FKA_ERR_INVALID_ARG (null pointer, sizes out of range), FKA_ERR_UNSUPPORTED
+ * (head_dim not 64/128, more than 64 query heads per KV head, more than 512 tokens),
+ * FKA_ERR_NOMEM, FKA_ERR_HIP. */
+fka_status fka_plan_create_prefill(const fka_heads *heads, const fka_prefill_desc *desc, fka_plan **out);
+
+/*
+ * Instruction prefill (two kernel launches: the partial kernel, then the merge).
+ *   q          bf16 [N][n][Hq][d]                 the instruction tokens' queries
+ *   prefix_k   bf16 [Hkv][Lp][d]                  shared prefix keys (prefix_v likewise)
+ *   suffix_k   bf16 [N][Hkv][suffix_cap][d]       each branch's suffix followed by the keys of its
+ *                                                 n instruction tokens at positions
+ *                                                 [suffix_len[b], suffix_len[b] + n) (suffix_v likewise)
+ *   suffix_len int32 [N] (device)                 each branch's suffix before the instruction; not
+ *                                                 changed (the caller advances it by n afterwards);
+ *                                                 a value outside [0, max_suffix_len - n] is
+ *                                                 clamped into it and flagged (1)
+ *   out        fp32 [N][n][Hq][d]                 attention output of every instruction token
+ *   out_lse    fp32 [N][n][Hq] or NULL            natural-log log-sum-exp of its scaled scores
+ * The plan's workspace is used: one stream at a time per plan.
+ */
+fka_status fka_prefill(const fka_plan *plan, const void *q, const void *prefix_k, const void *prefix_v,
+                       const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *out,
+                       float *out_lse, void *stream);
+
 /* -------------------------------------------------------------- stage entry points */
 
 /* The first stage (Sec. 3.3: the prefix is read once for all branches) runs as one kernel

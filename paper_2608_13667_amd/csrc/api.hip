@@ -20,6 +20,8 @@ struct fka_plan {
     float scale = 0.f;
     int32_t n_seqs = 0;
     int32_t share_prefix = 1;
+    int32_t prefill_n = 0;     // instruction prefill plan: tokens per branch (sequences are b * n + t)
+    int32_t n_branches = 0;    // instruction prefill plan: branches
     int32_t max_suffix_len = 0;
     // contiguous
     int32_t prefix_len = 0, suffix_cap = 0;
@@ -432,6 +434,90 @@ fka_status fka_plan_create_contig(const fka_heads *heads, const fka_contig_desc 
     return ok();
 }
 
+fka_status fka_plan_create_prefill(const fka_heads *heads, const fka_prefill_desc *desc, fka_plan **out)
+{
+    REQUIRE(out != nullptr, "out is null");
+    *out = nullptr;
+    fka_status st = check_heads(heads);
+    if (st != FKA_OK) return st;
+    REQUIRE(desc != nullptr, "desc is null");
+    REQUIRE(desc->n_branches >= 1, "n_branches (%d) must be >= 1", desc->n_branches);
+    REQUIRE(desc->n_tokens >= 1, "n_tokens (%d) must be >= 1", desc->n_tokens);
+    REQUIRE(desc->prefix_len >= 0, "prefix_len (%d) must be >= 0", desc->prefix_len);
+    REQUIRE(desc->suffix_cap >= 1, "suffix_cap (%d) must be >= 1", desc->suffix_cap);
+    REQUIRE(desc->max_suffix_len >= desc->n_tokens && desc->max_suffix_len <= desc->suffix_cap,
+            "max_suffix_len (%d) must be in [n_tokens=%d, suffix_cap=%d]", desc->max_suffix_len, desc->n_tokens,
+            desc->suffix_cap);
+    REQUIRE(desc->blocks >= 0, "blocks (%d) must be >= 0", desc->blocks);
+    const int64_t S = (int64_t)desc->n_branches * desc->n_tokens;  // virtual sequences
+    if (S > fka::kMaxSeqs)
+        return fail(FKA_ERR_UNSUPPORTED, "%lld instruction tokens (n_branches x n_tokens) exceed the limit of %d",
+                    (long long)S, fka::kMaxSeqs);
+    const int G = heads->n_q_heads / heads->n_kv_heads;
+    if (G > fka::kMaxRows)
+        return fail(FKA_ERR_UNSUPPORTED, "%d query heads per KV head exceed the limit of %d", G, fka::kMaxRows);
+    if (desc->prefix_len > kMaxTokens || desc->max_suffix_len > kMaxTokens)
+        return fail(FKA_ERR_UNSUPPORTED, "prefix or suffix longer than %d tokens", kMaxTokens);
+
+    fka_plan *p = new (std::nothrow) fka_plan();
+    if (!p) return fail(FKA_ERR_NOMEM, "host allocation failed");
+    auto bail = [&](fka_status e) {
+        fka_plan_destroy(p);
+        return e;
+    };
+    init_heads(p, heads);
+    p->prefill_n = desc->n_tokens;
+    p->n_branches = desc->n_branches;
+    p->n_seqs = (int32_t)S;
+    p->share_prefix = 1;
+    p->prefix_len = desc->prefix_len;
+    p->suffix_cap = desc->suffix_cap;
+    p->max_suffix_len = desc->max_suffix_len;
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) return bail(hip_fail(e, "hipGetDevice"));
+    int cus = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
+        return bail(hip_fail(e, "hipDeviceGetAttribute"));
+    // Units of consecutive instruction tokens, at most kMaxRows query rows each, all over the one
+    // prefix: as few as that allows.  Each unit's waves load every prefix tile once more (from L2)
+    // and score it against the unit's 16-row tiles, so fewer, taller units keep the matrix cores
+    // busy per byte loaded (one tile per slice does not cover the loads; four do).  Each of the
+    // U x Hkv items then takes B = resident / items blocks (at least one); with U x Hkv a multiple
+    // of the 8 XCDs the blocks of a KV head all run on one XCD and share its prefix tiles in L2.
+    const int32_t best_U = ceil_div(S, fka::kMaxRows / G);
+    const int32_t best_tiles = ceil_div(ceil_div(S, best_U) * G, 16);
+    const int per_cu = fka::prefill_blocks_per_cu(p->d, best_tiles);
+    if (per_cu <= 0) return bail(fail(FKA_ERR_HIP, "occupancy query of the prefill kernel failed"));
+    const int64_t items = (int64_t)best_U * p->Hkv;
+    const int64_t resident = (int64_t)cus * per_cu;
+    const int32_t best_B = (int32_t)(desc->blocks > 0 ? std::max<int64_t>(1, desc->blocks / items)
+                                                     : std::max<int64_t>(1, resident / items));
+    const int32_t U = best_U;
+    int32_t max_nseq = 0;
+    for (int32_t u = 0; u < U; ++u) {
+        fka::UnitRec r{};
+        r.seq0 = (int32_t)(u * S / U);
+        r.nseq = (int32_t)((u + 1) * S / U) - r.seq0;
+        r.plen = desc->prefix_len;
+        r.ps_before = u * fka::slices_of(desc->prefix_len);
+        max_nseq = std::max(max_nseq, r.nseq);
+        p->units.push_back(r);
+    }
+    p->seq_prefix_len.assign(p->n_seqs, desc->prefix_len);
+    p->ps_total = U * fka::slices_of(desc->prefix_len);
+    p->static_split = false;
+    p->n_items = U * p->Hkv;
+    p->slot_rows = max_nseq * G;
+    p->row_tiles = best_tiles;
+    p->waves = fka::partials_waves_per_block(p->d, p->row_tiles, false);
+    p->n_blocks = best_B * p->n_items;
+    p->rounds = 1;
+    p->n_slots = p->n_blocks;
+    if ((st = finish_plan(p)) != FKA_OK) return bail(st);
+    *out = p;
+    return ok();
+}
+
 fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *desc, const int32_t *host_group_start,
                                  const int32_t *host_group_prefix_len, fka_plan **out)
 {
@@ -516,6 +602,7 @@ fka_status fka_plan_slots(const fka_plan *p, const int32_t *host_suffix_len, fka
                           int32_t *n_slots)
 {
     REQUIRE(p != nullptr && host_suffix_len != nullptr && n_slots != nullptr, "null argument");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: its slots follow the cyclic placement");
     REQUIRE(capacity >= 0 && (capacity == 0 || slots != nullptr), "slots is null");
     const int N = p->n_seqs, Hkv = p->Hkv, NW = p->waves;
     const int32_t NV = p->n_blocks * p->rounds * NW;
@@ -579,6 +666,7 @@ fka_status fka_fork_decode(const fka_plan *p, const void *q, const void *prefix_
                            float *out_lse, void *stream)
 {
     REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill");
     REQUIRE(!p->paged, "plan is paged: use fka_fork_decode_paged");
     REQUIRE_PTR16(q);
     if (p->prefix_len > 0) {
@@ -660,11 +748,44 @@ fka_status fka_fork_decode_noalloc(const fka_heads *heads, const fka_contig_desc
     return run_decode(&p, a, suffix_len, out, out_lse, static_cast<hipStream_t>(stream));
 }
 
+fka_status fka_prefill(const fka_plan *p, const void *q, const void *prefix_k, const void *prefix_v,
+                       const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *out,
+                       float *out_lse, void *stream)
+{
+    REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(p->prefill_n > 0, "plan is not an instruction-prefill plan (fka_plan_create_prefill)");
+    REQUIRE_PTR16(q);
+    if (p->prefix_len > 0) {
+        REQUIRE_PTR16(prefix_k);
+        REQUIRE_PTR16(prefix_v);
+    }
+    REQUIRE_PTR16(suffix_k);
+    REQUIRE_PTR16(suffix_v);
+    REQUIRE_PTR4(suffix_len);
+    REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
+    fka::AttnArgs a = attn_args(p);
+    a.q = static_cast<const uint16_t *>(q);
+    a.prefix_k = static_cast<const uint16_t *>(prefix_k);
+    a.prefix_v = static_cast<const uint16_t *>(prefix_v);
+    a.suffix_k = static_cast<const uint16_t *>(suffix_k);
+    a.suffix_v = static_cast<const uint16_t *>(suffix_v);
+    a.suffix_len = suffix_len;
+    a.prefill_n = p->prefill_n;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = fka::launch_prefill(a, p->n_blocks, p->d, p->row_tiles, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill kernel launch");
+    e = fka::launch_merge(merge_args(p, suffix_len, out, out_lse), p->d, s);
+    if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+    return ok();
+}
+
 fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, const void *prefix_v,
                         const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *part_o,
                         float *part_lse, void *stream)
 {
     REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill");
     REQUIRE(!p->paged, "plan is paged: use fka_partials_paged");
     REQUIRE_PTR16(q);
     if (p->prefix_len > 0) {
@@ -720,6 +841,7 @@ fka_status fka_append_kv(const fka_plan *p, const void *k_new, const void *v_new
                          int32_t *suffix_len, void *stream)
 {
     REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill");
     REQUIRE(!p->paged, "plan is paged: use fka_append_kv_paged");
     REQUIRE_PTR16(k_new);
     REQUIRE_PTR16(v_new);
@@ -748,6 +870,7 @@ fka_status fka_fork_step(const fka_plan *p, const void *q, const void *k_new, co
                          int32_t *suffix_len, float *out, float *out_lse, void *stream)
 {
     REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill");
     REQUIRE(!p->paged, "plan is paged: use fka_fork_step_paged");
     REQUIRE_PTR16(q);
     REQUIRE_PTR16(k_new);

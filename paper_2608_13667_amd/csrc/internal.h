@@ -145,6 +145,9 @@ struct AttnArgs {
     int32_t slot_rows;
     int32_t n_slots;
     int32_t *err;
+    // instruction prefill (the prefill kernel only): sequence s = b n + t is instruction token t of
+    // branch b, reading b's suffix buffer up to position suffix_len[b] + t (n = prefill_n)
+    int32_t prefill_n;
 };
 
 struct MergeArgs {
@@ -239,6 +242,10 @@ hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int ro
 int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged);
 // Waves per block of the partial kernel for this shape.
 int partials_waves_per_block(int head_dim, int row_tiles, bool paged);
+// Instruction prefill: the partial kernel over virtual sequences (AttnArgs::prefill_n) with the
+// cyclic placement (block vb holds item vb mod items), contiguous layout.
+hipError_t launch_prefill(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);
+int prefill_blocks_per_cu(int head_dim, int row_tiles);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);

@@ -75,12 +75,18 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const char *base, int bytes)
 // the line kept in the cache that measured 12% slower on the paged workload, the default policy
 // is kept there.  V arrives by LDS DMA, 1 KiB contiguous per instruction: non-temporal in both
 // layouts (5% faster on the paged workload than the default).
-template <bool PAGED>
+// The instruction prefill reads every prefix tile once per unit, the units of a KV head together
+// on one XCD: there the default policy keeps the tile in L2 for the other units.
+template <bool PAGED, bool PREFILL>
 constexpr int k_policy()
 {
-    return PAGED ? 0 : 2;
+    return (PAGED || PREFILL) ? 0 : 2;
 }
-constexpr int kVPolicy = 2;
+template <bool PREFILL>
+constexpr int v_policy()
+{
+    return PREFILL ? 0 : 2;
+}
 
 // 16 bytes per lane from a buffer into LDS at dst + 16 * lane (LDS DMA).  Kept outside
 // the kernel template: used directly there, the builtin stops the host compiler from
@@ -231,7 +237,7 @@ struct SliceSrc {
     int32_t suffix;       // 1: a suffix slice, read by rows [r_lo, r_hi) only
 };
 
-template <int HD, int NT, bool PAGED>
+template <int HD, int NT, bool PAGED, bool PREFILL>
 __global__ __launch_bounds__((256 * waves_per_simd<HD, NT, PAGED>()))
 __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void partials_kernel(AttnArgs a)
 {
@@ -317,9 +323,19 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
         // one round trip: the suffix lengths and the units; then the scans and the placement
         bool clamped = false;
         for (int s = tid; s < N; s += NTH) {
-            const int raw = a.suffix_len[s];
-            const int L = min(max(raw, 0), max_len);
-            clamped |= (L != raw);
+            int L;
+            if constexpr (PREFILL) {
+                // instruction token t of branch b (s = b n + t) sees b's suffix up to its own position
+                const int n = a.prefill_n;
+                const int raw = a.suffix_len[s / n];
+                const int Lb = min(max(raw, 0), max_len - n);
+                clamped |= (Lb != raw);
+                L = Lb + s % n + 1;
+            } else {
+                const int raw = a.suffix_len[s];
+                L = min(max(raw, 0), max_len);
+                clamped |= (L != raw);
+            }
             s_len[s] = L;
             s_cs[s] = slices_of(L);
             if (vb == 0) a.lens[s] = L;  // what the merge appends at
@@ -333,74 +349,102 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
         }
         if (vb == 0 && clamped) atomicOr(a.err, kErrSuffixClamped);
         if (tid < NW) s_wf[tid][0] = -1;  // waves the placement below does not reach have no item
-        lds_barrier();
-        // exclusive scan of v[0..n) in place, total at v[n] (visible after the next barrier)
-        auto block_scan = [&](int32_t *v, int n) {
-            int carry = 0;
-            for (int base = 0; base < n; base += NTH) {
-                const int i = base + tid;
-                const int x0 = i < n ? v[i] : 0;
-                int x = x0;
-#pragma unroll
-                for (int off = 1; off < 64; off <<= 1) {
-                    const int y = __shfl_up(x, off);
-                    if (lane >= off) x += y;
-                }
-                if (lane == 63) s_wsum[wave] = x;
-                lds_barrier();
-                int pre = carry;
-                for (int w = 0; w < NW; ++w) {
-                    if (w < wave) pre += s_wsum[w];
-                    carry += s_wsum[w];
-                }
-                if (i < n) v[i] = pre + x - x0;
-                lds_barrier();
-            }
-            if (tid == 0) v[n] = carry;
-        };
-        block_scan(s_cs, N);
-        lds_barrier();
-        for (int u = tid; u < a.n_units; u += NTH)
-            s_ne[u] = (slices_of(s_ul[u]) + s_cs[s_u0[u] + s_un[u]] - s_cs[s_u0[u]]) > 0 ? 1 : 0;
-        lds_barrier();
-        block_scan(s_ne, a.n_units);
-        lds_barrier();
-        const int T = __builtin_amdgcn_readfirstlane(Hkv * (a.ps_total + s_cs[N]));  // total slices
-        const int NNE = __builtin_amdgcn_readfirstlane(Hkv * s_ne[a.n_units]);      // non-empty items
-        const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
-        const int n_items = a.n_units * Hkv;
-        // every thread places its items' workers of this block; the block holding an item's
-        // first worker writes the slot records of the item's rows (block 0 those of empty items)
-        for (int i = tid; i < n_items; i += NTH) {
-            const int u = i / Hkv, g = i - u * Hkv;
-            const int u0 = s_u0[u], un = s_un[u];
-            const int size = slices_of(s_ul[u]) + s_cs[u0 + un] - s_cs[u0];
-            const int64_t C = (int64_t)Hkv * (s_up[u] + s_cs[u0]) + (int64_t)g * size;
-            const int64_t K = (int64_t)Hkv * s_ne[u] + (size > 0 ? g : 0);
-            int ws0 = 0, ws1 = 0;
-            if (size > 0 && T > 0) {
-                ws0 = worker_start(C, K, R);
-                ws1 = worker_start(C + size, K + 1, R);
-            }
-            if ((ws1 > ws0 && ws0 >= w_lo && ws0 < w_lo + NW) || (ws1 == ws0 && vb == 0)) {
-                const int first = ws1 > ws0 ? ws0 / NW + i : 0, count = ws1 > ws0 ? (ws1 - 1) / NW - ws0 / NW + 1 : 0;
-                for (int r = 0; r < un * G; ++r) {
-                    int32_t *rr = a.rowrec + ((size_t)(u0 + r / G) * a.n_q_heads + g * G + r % G) * kRowRec;
-                    rr[0] = first * a.slot_rows + r;
-                    rr[1] = count;
-                }
-            }
-            if (ws1 <= w_lo || ws0 >= w_lo + NW || ws1 <= ws0) continue;
-            const int lo = max(ws0, w_lo), hi = min(ws1, w_lo + NW);
-            for (int gw = lo; gw < hi; ++gw) {
-                int32_t *d = s_wf[gw - w_lo];
+        if constexpr (PREFILL) {
+            // Cyclic placement: block vb is block k = vb / n_items of item vb mod n_items (each
+            // item has B = blocks / n_items blocks, all its waves one group); with n_items a
+            // multiple of the 8 XCDs, every block of a KV head runs on one XCD, so the blocks of
+            // one prefix range, one per unit, share its tiles through that XCD's L2.
+            const int n_items = a.n_units * Hkv, B = (int)gridDim.x / n_items;
+            const int i = vb % n_items, k = vb / n_items;
+            lds_barrier();  // the unit table
+            if (tid < NW) {
+                int32_t *d = s_wf[tid];
                 d[0] = i;
-                d[1] = u;
-                d[2] = ws1 - ws0;
-                d[3] = lo - ws0;
-                d[4] = hi - ws0;
-                d[5] = lo - w_lo;
-                d[6] = hi - w_lo;
+                d[1] = i / Hkv;
+                d[2] = B * NW;
+                d[3] = k * NW;
+                d[4] = (k + 1) * NW;
+                d[5] = 0;
+                d[6] = NW;
+            }
+            if (k == 0) {  // the item's rows read their B parts at slots i B .. i B + B - 1
+                const int u = i / Hkv, g = i - u * Hkv;
+                for (int r = tid; r < s_un[u] * G; r += NTH) {
+                    int32_t *rr = a.rowrec + ((size_t)(s_u0[u] + r / G) * a.n_q_heads + g * G + r % G) * kRowRec;
+                    rr[0] = i * B * a.slot_rows + r;
+                    rr[1] = B;
+                }
+            }
+        } else {
+        lds_barrier();
+            // exclusive scan of v[0..n) in place, total at v[n] (visible after the next barrier)
+            auto block_scan = [&](int32_t *v, int n) {
+                int carry = 0;
+                for (int base = 0; base < n; base += NTH) {
+                    const int i = base + tid;
+                    const int x0 = i < n ? v[i] : 0;
+                    int x = x0;
+#pragma unroll
+                    for (int off = 1; off < 64; off <<= 1) {
+                        const int y = __shfl_up(x, off);
+                        if (lane >= off) x += y;
+                    }
+                    if (lane == 63) s_wsum[wave] = x;
+                    lds_barrier();
+                    int pre = carry;
+                    for (int w = 0; w < NW; ++w) {
+                        if (w < wave) pre += s_wsum[w];
+                        carry += s_wsum[w];
+                    }
+                    if (i < n) v[i] = pre + x - x0;
+                    lds_barrier();
+                }
+                if (tid == 0) v[n] = carry;
+            };
+            block_scan(s_cs, N);
+            lds_barrier();
+            for (int u = tid; u < a.n_units; u += NTH)
+                s_ne[u] = (slices_of(s_ul[u]) + s_cs[s_u0[u] + s_un[u]] - s_cs[s_u0[u]]) > 0 ? 1 : 0;
+            lds_barrier();
+            block_scan(s_ne, a.n_units);
+            lds_barrier();
+            const int T = __builtin_amdgcn_readfirstlane(Hkv * (a.ps_total + s_cs[N]));  // total slices
+            const int NNE = __builtin_amdgcn_readfirstlane(Hkv * s_ne[a.n_units]);      // non-empty items
+            const uint64_t R = T > 0 ? sched_ratio((int64_t)NV - NNE, T) : 0;
+            const int n_items = a.n_units * Hkv;
+            // every thread places its items' workers of this block; the block holding an item's
+            // first worker writes the slot records of the item's rows (block 0 those of empty items)
+            for (int i = tid; i < n_items; i += NTH) {
+                const int u = i / Hkv, g = i - u * Hkv;
+                const int u0 = s_u0[u], un = s_un[u];
+                const int size = slices_of(s_ul[u]) + s_cs[u0 + un] - s_cs[u0];
+                const int64_t C = (int64_t)Hkv * (s_up[u] + s_cs[u0]) + (int64_t)g * size;
+                const int64_t K = (int64_t)Hkv * s_ne[u] + (size > 0 ? g : 0);
+                int ws0 = 0, ws1 = 0;
+                if (size > 0 && T > 0) {
+                    ws0 = worker_start(C, K, R);
+                    ws1 = worker_start(C + size, K + 1, R);
+                }
+                if ((ws1 > ws0 && ws0 >= w_lo && ws0 < w_lo + NW) || (ws1 == ws0 && vb == 0)) {
+                    const int first = ws1 > ws0 ? ws0 / NW + i : 0, count = ws1 > ws0 ? (ws1 - 1) / NW - ws0 / NW + 1 : 0;
+                    for (int r = 0; r < un * G; ++r) {
+                        int32_t *rr = a.rowrec + ((size_t)(u0 + r / G) * a.n_q_heads + g * G + r % G) * kRowRec;
+                        rr[0] = first * a.slot_rows + r;
+                        rr[1] = count;
+                    }
+                }
+                if (ws1 <= w_lo || ws0 >= w_lo + NW || ws1 <= ws0) continue;
+                const int lo = max(ws0, w_lo), hi = min(ws1, w_lo + NW);
+                for (int gw = lo; gw < hi; ++gw) {
+                    int32_t *d = s_wf[gw - w_lo];
+                    d[0] = i;
+                    d[1] = u;
+                    d[2] = ws1 - ws0;
+                    d[3] = lo - ws0;
+                    d[4] = hi - ws0;
+                    d[5] = lo - w_lo;
+                    d[6] = hi - w_lo;
+                }
             }
         }
         lds_barrier();
@@ -482,7 +526,8 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
             s.page_off = iss ? (plen + kPageSize - 1) / kPageSize : 0;
         } else {
             const size_t pbase = (size_t)kvh * (size_t)arg_plen * ROWB;
-            const size_t sbase = ((size_t)seq * Hkv + kvh) * (size_t)arg_cap * ROWB;
+            const int buf = PREFILL ? seq / a.prefill_n : seq;  // prefill: branch b's buffer
+            const size_t sbase = ((size_t)buf * Hkv + kvh) * (size_t)arg_cap * ROWB;
             s.kb = iss ? arg_sk + sbase : arg_pk + pbase;
             s.vb = iss ? arg_sv + sbase : arg_pv + pbase;
             s.ptab = arg_pt;
@@ -522,7 +567,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
             const __amdgpu_buffer_rsrc_t r = group_rsrc(s, s.kb, s.tok0 + 16 * u);
 #pragma unroll
             for (int c = 0; c < NC; ++c)
-                kr[u][c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, koff + 64 * c, 0, k_policy<PAGED>()));
+                kr[u][c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, koff + 64 * c, 0, k_policy<PAGED, PREFILL>()));
         }
     };
 
@@ -549,7 +594,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
         static_for<VDMA>([&](auto I) {
             constexpr int i = decltype(I)::value;
             constexpr int imm = 1024 * (i % VPER);
-            buffer_to_lds16<kVPolicy, imm>(i < VPER ? r0 : r1,
+            buffer_to_lds16<v_policy<PREFILL>(), imm>(i < VPER ? r0 : r1,
                                            (lds_void *)((__attribute__((address_space(3))) char *)dst + 1024 * i - imm),
                                            vbase[CPR == 16 ? (i & 1) : 0]);
         });
@@ -844,7 +889,10 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
             const int4 gi = *reinterpret_cast<const int4 *>(&s_grp[g][0]);
             asm volatile("" ::"v"(gi.x), "v"(gi.y), "v"(gi.z), "v"(gi.w));  // one LDS read, not four
             const int lw = gi.x, ge = gi.y, it = gi.w;
-            if (vb + it >= a.n_slots || it < 0) continue;  // never store outside the workspace
+            // the group's slot: vb + it, or under the cyclic placement it B + (vb / n_items)
+            const int n_items_c = a.n_units * Hkv;
+            const int slot_c = PREFILL ? it * ((int)gridDim.x / n_items_c) + vb / n_items_c : vb + it;
+            if (slot_c >= a.n_slots || it < 0) continue;  // never store outside the workspace
             const int r0 = 16 * TPP * pass, r1 = min(gi.z, r0 + 16 * TPP);
             const bool whole = lw == 0 && ge == NW;  // the usual case: one group, all waves
             for (int u = tid_c; u < (r1 - r0) * CHU; u += NTH) {
@@ -892,7 +940,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
                 // L == 0 only when the group saw no keys: its accumulators are zero and so is
                 // o; a NaN input keeps propagating
                 const float inv = (L == 0.f) ? 0.f : __builtin_amdgcn_rcpf(L);
-                const size_t so = (size_t)(vb + it) * a.slot_rows + row;
+                const size_t so = (size_t)slot_c * a.slot_rows + row;
                 float *dst = a.part_o + so * HD + 4 * UQ * cu;
 #pragma unroll
                 for (int q = 0; q < UQ; ++q) *reinterpret_cast<f32x4 *>(dst + 4 * q) = o[q] * inv;
@@ -903,16 +951,16 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
     if (bad_page) atomicOr(a.err, kErrBadPage);
 }
 
-template <int HD, bool PAGED>
+template <int HD, bool PAGED, bool PREFILL>
 int blocks_per_cu_hd(int row_tiles)
 {
     const void *f = nullptr;
     int threads = 0;
     switch (row_tiles) {
-    case 1: f = reinterpret_cast<const void *>(&partials_kernel<HD, 1, PAGED>); threads = 256 * waves_per_simd<HD, 1, PAGED>(); break;
-    case 2: f = reinterpret_cast<const void *>(&partials_kernel<HD, 2, PAGED>); threads = 256 * waves_per_simd<HD, 2, PAGED>(); break;
-    case 3: f = reinterpret_cast<const void *>(&partials_kernel<HD, 3, PAGED>); threads = 256 * waves_per_simd<HD, 3, PAGED>(); break;
-    case 4: f = reinterpret_cast<const void *>(&partials_kernel<HD, 4, PAGED>); threads = 256 * waves_per_simd<HD, 4, PAGED>(); break;
+    case 1: f = reinterpret_cast<const void *>(&partials_kernel<HD, 1, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 1, PAGED>(); break;
+    case 2: f = reinterpret_cast<const void *>(&partials_kernel<HD, 2, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 2, PAGED>(); break;
+    case 3: f = reinterpret_cast<const void *>(&partials_kernel<HD, 3, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 3, PAGED>(); break;
+    case 4: f = reinterpret_cast<const void *>(&partials_kernel<HD, 4, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 4, PAGED>(); break;
     default: return 0;
     }
     int n = 0;
@@ -920,15 +968,15 @@ int blocks_per_cu_hd(int row_tiles)
     return n;
 }
 
-template <int HD, bool PAGED>
+template <int HD, bool PAGED, bool PREFILL>
 hipError_t launch_hd(const AttnArgs &a, int n_blocks, int row_tiles, hipStream_t s)
 {
     const dim3 grid(n_blocks);
     switch (row_tiles) {
-    case 1: partials_kernel<HD, 1, PAGED><<<grid, 256 * waves_per_simd<HD, 1, PAGED>(), 0, s>>>(a); break;
-    case 2: partials_kernel<HD, 2, PAGED><<<grid, 256 * waves_per_simd<HD, 2, PAGED>(), 0, s>>>(a); break;
-    case 3: partials_kernel<HD, 3, PAGED><<<grid, 256 * waves_per_simd<HD, 3, PAGED>(), 0, s>>>(a); break;
-    case 4: partials_kernel<HD, 4, PAGED><<<grid, 256 * waves_per_simd<HD, 4, PAGED>(), 0, s>>>(a); break;
+    case 1: partials_kernel<HD, 1, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 1, PAGED>(), 0, s>>>(a); break;
+    case 2: partials_kernel<HD, 2, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 2, PAGED>(), 0, s>>>(a); break;
+    case 3: partials_kernel<HD, 3, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 3, PAGED>(), 0, s>>>(a); break;
+    case 4: partials_kernel<HD, 4, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 4, PAGED>(), 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -938,8 +986,10 @@ hipError_t launch_hd(const AttnArgs &a, int n_blocks, int row_tiles, hipStream_t
 
 int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged)
 {
-    if (head_dim == 128) return paged ? blocks_per_cu_hd<128, true>(row_tiles) : blocks_per_cu_hd<128, false>(row_tiles);
-    if (head_dim == 64) return paged ? blocks_per_cu_hd<64, true>(row_tiles) : blocks_per_cu_hd<64, false>(row_tiles);
+    if (head_dim == 128)
+        return paged ? blocks_per_cu_hd<128, true, false>(row_tiles) : blocks_per_cu_hd<128, false, false>(row_tiles);
+    if (head_dim == 64)
+        return paged ? blocks_per_cu_hd<64, true, false>(row_tiles) : blocks_per_cu_hd<64, false, false>(row_tiles);
     return 0;
 }
 
@@ -964,10 +1014,25 @@ int partials_waves_per_block(int head_dim, int row_tiles, bool paged)
 hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s)
 {
     if (n_blocks <= 0) return hipSuccess;
-    if (head_dim == 128) return a.paged ? launch_hd<128, true>(a, n_blocks, row_tiles, s)
-                                        : launch_hd<128, false>(a, n_blocks, row_tiles, s);
-    if (head_dim == 64) return a.paged ? launch_hd<64, true>(a, n_blocks, row_tiles, s)
-                                       : launch_hd<64, false>(a, n_blocks, row_tiles, s);
+    if (head_dim == 128) return a.paged ? launch_hd<128, true, false>(a, n_blocks, row_tiles, s)
+                                        : launch_hd<128, false, false>(a, n_blocks, row_tiles, s);
+    if (head_dim == 64) return a.paged ? launch_hd<64, true, false>(a, n_blocks, row_tiles, s)
+                                       : launch_hd<64, false, false>(a, n_blocks, row_tiles, s);
+    return hipErrorInvalidValue;
+}
+
+int prefill_blocks_per_cu(int head_dim, int row_tiles)
+{
+    if (head_dim == 128) return blocks_per_cu_hd<128, false, true>(row_tiles);
+    if (head_dim == 64) return blocks_per_cu_hd<64, false, true>(row_tiles);
+    return 0;
+}
+
+hipError_t launch_prefill(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s)
+{
+    if (n_blocks <= 0) return hipSuccess;
+    if (head_dim == 128) return launch_hd<128, false, true>(a, n_blocks, row_tiles, s);
+    if (head_dim == 64) return launch_hd<64, false, true>(a, n_blocks, row_tiles, s);
     return hipErrorInvalidValue;
 }
 

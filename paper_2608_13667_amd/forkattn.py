@@ -42,6 +42,11 @@ class PagedDesc(C.Structure):
                 ("share_prefix", C.c_int32), ("rounds", C.c_int32), ("blocks", C.c_int32)]
 
 
+class PrefillDesc(C.Structure):
+    _fields_ = [("n_branches", C.c_int32), ("n_tokens", C.c_int32), ("prefix_len", C.c_int32),
+                ("suffix_cap", C.c_int32), ("max_suffix_len", C.c_int32), ("blocks", C.c_int32)]
+
+
 class PlanInfo(C.Structure):
     _fields_ = [("n_items", C.c_int32), ("n_units", C.c_int32), ("waves_per_block", C.c_int32),
                 ("n_blocks", C.c_int32), ("rounds", C.c_int32), ("n_slots", C.c_int32), ("slot_rows", C.c_int32),
@@ -69,6 +74,8 @@ _sig = {
     "fka_gather_paged": ([_vp, C.c_int32, _vp, _vp, _vp, C.c_int32, _vp, _vp, _vp], C.c_int),
     "fka_gather_paged_range": ([_vp, C.c_int32, C.c_int32, C.c_int32, _vp, _vp, _vp, _vp, _vp, _vp], C.c_int),
     "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
+    "fka_plan_create_prefill": ([C.POINTER(Heads), C.POINTER(PrefillDesc), C.POINTER(_vp)], C.c_int),
+    "fka_prefill": ([_vp] * 10, C.c_int),
     "fka_fork_decode_noalloc": ([C.POINTER(Heads), C.POINTER(ContigDesc)] + [_vp] * 10, C.c_int),
     "fka_plan_slots": ([_vp, _vp, _vp, C.c_int32, C.POINTER(C.c_int32)], C.c_int),
     "fka_partials": ([_vp] * 10, C.c_int),
@@ -178,6 +185,23 @@ class Plan:
         _check(_lib.fka_plan_create_paged(C.byref(h), C.byref(d), gs.ctypes.data_as(_vp), gl.ctypes.data_as(_vp),
                                           C.byref(out)))
         return cls(out.value, True, h, int(gs[-1]))
+
+    @classmethod
+    def prefill_plan(cls, n_q_heads, n_kv_heads, head_dim, n_branches, n_tokens, prefix_len, suffix_cap,
+                     max_suffix_len, softmax_scale=0.0, blocks=0) -> "Plan":
+        """An instruction-prefill plan (fka_plan_create_prefill): n_tokens per branch."""
+        h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
+        d = PrefillDesc(n_branches, n_tokens, prefix_len, suffix_cap, max_suffix_len, blocks)
+        out = _vp()
+        _check(_lib.fka_plan_create_prefill(C.byref(h), C.byref(d), C.byref(out)))
+        return cls(out.value, False, h, n_branches * n_tokens)
+
+    def prefill(self, q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, out, out_lse=None, stream=None):
+        """fka_prefill: q bf16 [N][n][Hq][d] -> out fp32 [N][n][Hq][d], out_lse fp32 [N][n][Hq]."""
+        d = self.device
+        _check(_lib.fka_prefill(self._h, _p(q, "bf16", d), _p(prefix_k, "bf16", d), _p(prefix_v, "bf16", d),
+                                _p(suffix_k, "bf16", d), _p(suffix_v, "bf16", d), _p(suffix_len, "i32", d),
+                                _p(out, "f32", d), _p(out_lse, "f32", d), _stream(stream)))
 
     def close(self):
         if self._h is not None and self._h.value:

@@ -1,0 +1,143 @@
+"""Instruction prefill (fka_prefill) against the oracle's causal definition.
+
+Branch b appends n instruction tokens over the shared prefix (paper Sec. 3.3): token t's queries
+attend to the whole prefix and to b's suffix positions [0, L_b + t].  The reference evaluates that
+definition directly: instruction token (b, t) is a sequence of its own over [prefix ; b's suffix up
+to L_b + t], computed by the fp64 oracle.  Bar: the gates of tests/gates.py on every row.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13667_amd import workloads as W
+from tests import gates
+from tests.gpu_util import dev_bf16, dev_i32
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fa():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_13667_amd import forkattn
+    return forkattn
+
+
+def _instruction(w, n):
+    """The workload's n per-step tokens as each branch's instruction: q [N][n][Hq][d], and the
+    suffix buffers with token t's key / value at position L_b + t."""
+    N = w.q.shape[0]
+    q = np.ascontiguousarray(w.step_q[:n].transpose(1, 0, 2, 3))
+    sk, sv = w.suffix_k.copy(), w.suffix_v.copy()
+    for b in range(N):
+        L = int(w.suffix_len[b])
+        sk[b, :, L:L + n] = w.step_k[:n, b].transpose(1, 0, 2)
+        sv[b, :, L:L + n] = w.step_v[:n, b].transpose(1, 0, 2)
+    return q, sk, sv
+
+
+def _reference(w, n, q, sk, sv):
+    """The causal definition, one oracle sequence per instruction token."""
+    N, _, Hq, d = q.shape
+    qv = q.reshape(N * n, Hq, d)
+    vlen = np.array([int(w.suffix_len[b]) + t + 1 for b in range(N) for t in range(n)], np.int32)
+    return oracle.decode_contig(qv, w.prefix_k, w.prefix_v, np.repeat(sk, n, axis=0), np.repeat(sv, n, axis=0),
+                                vlen, w.spec.softmax_scale)
+
+
+def _run(fa, w, n, q, sk, sv, blocks=0, suffix_len=None):
+    s = w.spec
+    N, _, Hq, d = q.shape
+    cap = w.suffix_cap
+    plan = fa.Plan.prefill_plan(s.n_q_heads, s.n_kv_heads, s.head_dim, N, n, w.prefix_len, cap, cap, blocks=blocks)
+    out = torch.full((N, n, Hq, d), float("nan"), device="cuda")
+    lse = torch.full((N, n, Hq), float("nan"), device="cuda")
+    ln = dev_i32(w.suffix_len if suffix_len is None else suffix_len)
+    plan.prefill(dev_bf16(q), dev_bf16(w.prefix_k), dev_bf16(w.prefix_v), dev_bf16(sk), dev_bf16(sv), ln, out, lse)
+    torch.cuda.synchronize()
+    return plan, out.cpu().numpy().reshape(N * n, Hq, d), lse.cpu().numpy().reshape(N * n, Hq)
+
+
+@pytest.mark.parametrize("n", [1, 16, 64])
+def test_prefill_long_shape(fa, n):
+    """The 32k-prefix agent context (40 query / 8 KV heads, d 128, 5 branches) with n-token
+    instructions over existing suffixes of 0..40 tokens; every row of every token checked."""
+    w = W.make("long", steps=n, suffix_range=(0, 40), seed=2600 + n)
+    q, sk, sv = _instruction(w, n)
+    print(f"[prefill] long n={n}: suffix_len {w.suffix_len.tolist()}", flush=True)
+    plan, out, lse = _run(fa, w, n, q, sk, sv)
+    info = plan.info()
+    print(f"[prefill] long n={n}: {info.n_units} units, {info.n_items} items, {info.n_blocks} blocks", flush=True)
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    m = gates.assert_gates(out, ref, what=f"prefill long n={n}")
+    gates.assert_lse(lse, ref_lse, what=f"prefill long n={n}")
+    assert plan.device_error() == 0
+    # the units of one KV head are a multiple of the 8 XCDs apart, so that they share prefix tiles
+    assert info.n_items % 8 == 0 and info.n_blocks % info.n_items == 0
+    print(f"[prefill] long n={n} {m}", flush=True)
+
+
+def _random_cases(k, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(k):
+        d = int(rng.choice([64, 128]))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.integers(1, 9))
+        nb = int(rng.integers(1, 7))
+        n = int(rng.integers(1, 40))
+        while nb * n > 512:
+            n //= 2
+        out.append(dict(head_dim=d, n_kv_heads=hkv, n_q_heads=hkv * g, n_branches=nb, n=n,
+                        prefix_len=int(rng.integers(0, 3000)), lo=int(rng.integers(0, 60)),
+                        blocks=int(rng.choice([0, 0, 7, 64])), seed=int(rng.integers(1, 1 << 30))))
+    return out
+
+
+@pytest.mark.parametrize("c", _random_cases(10, 2601),
+                         ids=lambda c: f"d{c['head_dim']}-kv{c['n_kv_heads']}-q{c['n_q_heads']}-b{c['n_branches']}"
+                                       f"-n{c['n']}-p{c['prefix_len']}-blk{c['blocks']}")
+def test_prefill_random_shapes(fa, c):
+    """Seeded shapes: d 64 / 128, 1..8 KV heads, G 1..8, 1..6 branches, 1..39 tokens, prefixes of
+    0..3000 (some not a multiple of the 32-key slice), existing suffixes, explicit grids."""
+    spec = W.CONFIGS["mid"].replace(head_dim=c["head_dim"], n_kv_heads=c["n_kv_heads"], n_q_heads=c["n_q_heads"],
+                                    n_branches=c["n_branches"], prefix_len=c["prefix_len"],
+                                    suffix_range=(c["lo"], c["lo"] + 30), steps=c["n"], seed=c["seed"])
+    w = W.make(spec)
+    n = c["n"]
+    q, sk, sv = _instruction(w, n)
+    plan, out, lse = _run(fa, w, n, q, sk, sv, blocks=c["blocks"])
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    gates.assert_gates(out, ref, what=str(c))
+    gates.assert_lse(lse, ref_lse, what=str(c))
+    assert plan.device_error() == 0
+
+
+def test_prefill_clamps_and_flags_a_suffix_past_the_bound(fa):
+    """A suffix length above max_suffix_len - n is clamped to it (and flagged), like a decode's."""
+    n = 5
+    w = W.make("tiny", steps=n, suffix_range=(10, 20), seed=2602)
+    q, sk, sv = _instruction(w, n)
+    cap = w.suffix_cap
+    bad = w.suffix_len.copy()
+    bad[1] = cap + 3
+    plan, out, lse = _run(fa, w, n, q, sk, sv, suffix_len=bad)
+    assert plan.device_error() == 1
+    # branch 1 now reads up to its clamped bound (the NaN past its data); the others are exact
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    N = q.shape[0]
+    rows = [s for s in range(N * n) if s // n != 1]
+    gates.assert_gates(out[rows], ref[rows], what="other branches unaffected")
+    gates.assert_lse(lse[rows], ref_lse[rows], what="other branches unaffected")
+
+
+def test_prefill_plan_rejects_other_calls(fa):
+    """A prefill plan serves fka_prefill only; decode entry points refuse it."""
+    plan = fa.Plan.prefill_plan(8, 2, 64, 3, 4, 100, 32, 32)
+    t = torch.zeros(1 << 16, dtype=torch.bfloat16, device="cuda")
+    ln = torch.zeros(3, dtype=torch.int32, device="cuda")
+    o = torch.zeros(1 << 14, dtype=torch.float32, device="cuda")
+    with pytest.raises(fa.FkaError, match="prefill"):
+        plan.decode(t, t, t, t, t, ln, o)
