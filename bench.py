@@ -89,6 +89,9 @@ def parse():
     ap.add_argument("--no-probe", action="store_true", help="skip the read-bandwidth probe")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-prefill", action="store_true", help="skip the instruction-prefill timing")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="time only the instruction prefill (for profiling its kernel alone)")
+    ap.add_argument("--prefill-tokens", default="1,16,64", help="instruction tokens per branch to time")
     ap.add_argument("--lifecycle", action="store_true",
                     help="also time the fork lifecycle on the page pool (contiguous workloads' shapes)")
     return ap.parse_args()
@@ -516,6 +519,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
 
+    ns = tuple(int(x) for x in args.prefill_tokens.split(",") if x)
+    if args.prefill_only:
+        print(json.dumps({"instruction_prefill": prefill_timing(torch, fa, W, ns, args.trials)}), flush=True)
+        return
+
     main_b = Bench(torch, fa, W, args.workload, args)
     K = args.steps if args.steps is not None else main_b.default_steps()
     if main_b.appends and math.ceil(K / main_b.R) > main_b.spec.steps:
@@ -542,7 +550,7 @@ def main():
 
     prefill = None
     if not args.no_prefill:
-        prefill = prefill_timing(torch, fa, W, (1, 16, 64), args.trials)
+        prefill = prefill_timing(torch, fa, W, ns, args.trials)
 
     probe = None
     if not args.no_probe:

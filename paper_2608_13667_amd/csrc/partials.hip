@@ -851,8 +851,10 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
         }
     }
     wait_vm<0>();  // this wave's ring is idle: it takes the wave's raw accumulators
-    // Staging: wave w writes [tile][row][d] of its own accumulator (the 16-float blocks of a
-    // row XOR-permuted by the row, for the banks): tiles 0 and 1 into its ring, further tiles
+    // Staging: wave w writes [tile][row][d] of its own accumulator (the 16-byte chunks of row r
+    // XOR-permuted by r mod 16, so that one chunk of 16 consecutive rows lies in 16 different
+    // bank groups: a staging store covers 16 rows at one chunk, and so does a combine load, whose
+    // consecutive lanes take consecutive rows): tiles 0 and 1 into its ring, further tiles
     // into stg_x when a pass holds them, else in later passes.  After one barrier, threads own
     // (row, unit) pieces of each group: they weigh the group's waves by exp(max_w - max), sum,
     // and normalise; the unit holding the row's first floats also stores its lse.  (A separate
@@ -867,7 +869,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
         return &stg_x[w][(tt - 2) * 16 * HD];
     };
     auto stg_off = [&](int r, int c4) {  // float offset of chunk c4 (4 floats) of row r in a tile
-        return r * HD + 16 * ((c4 >> 2) ^ (r & (NE - 1))) + 4 * (c4 & 3);
+        return r * HD + 4 * (c4 ^ (r & 15));
     };
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
@@ -896,7 +898,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
             const int r0 = 16 * TPP * pass, r1 = min(gi.z, r0 + 16 * TPP);
             const bool whole = lw == 0 && ge == NW;  // the usual case: one group, all waves
             for (int u = tid_c; u < (r1 - r0) * CHU; u += NTH) {
-                const int row = r0 + u / CHU, cu = u % CHU;
+                const int row = r0 + u % (r1 - r0), cu = u / (r1 - r0);
                 const int t = row >> 4, tt = t - TPP * pass, r = row & 15;
                 // a wave of the group that saw no keys has max -inf, weight 0 and a zero
                 // accumulator; waves outside the group are never read (their staging may

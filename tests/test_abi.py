@@ -187,7 +187,7 @@ def test_misaligned_pointers_are_rejected_by_plan_calls(fa):
     b16, b8 = vp(buf.data_ptr()), vp(buf.data_ptr() + 8)
     i4, i2 = vp(i32.data_ptr()), vp(i32.data_ptr() + 2)
     f16, f8, f2 = vp(f32.data_ptr()), vp(f32.data_ptr() + 8), vp(f32.data_ptr() + 2)
-    h = vp(plan._h)
+    h = plan._h
     good = [b16, b16, b16, b16, b16, i4, f16, f16]  # q, prefix k/v, suffix k/v, suffix_len, out, out_lse
     for i, name, bad in [(0, "q", b8), (2, "prefix_v", b8), (3, "suffix_k", b8), (5, "suffix_len", i2),
                          (6, "out", f8), (7, "out_lse", f2)]:
