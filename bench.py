@@ -32,7 +32,7 @@ HBM_PEAK_GBPS = 8000.0
 MALL_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_13667_amd", "csrc", "partials.hip")
-SUB_WORKLOADS = ("very-long", "paged", "mid")
+SUB_WORKLOADS = ("very-long", "paged", "mid", "onset", "tiny")
 
 
 def measured_traffic(workload: str):
@@ -89,6 +89,8 @@ def parse():
     ap.add_argument("--no-probe", action="store_true", help="skip the read-bandwidth probe")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-prefill", action="store_true", help="skip the instruction-prefill timing")
+    ap.add_argument("--yardstick-copy", action="store_true",
+                    help="first copy 256 MiB device to device (a kernel of known traffic, to scale HBM counters)")
     ap.add_argument("--prefill-only", action="store_true",
                     help="time only the instruction prefill (for profiling its kernel alone)")
     ap.add_argument("--prefill-tokens", default="1,16,64", help="instruction tokens per branch to time")
@@ -212,8 +214,10 @@ class Bench:
                 else:
                     plan.partials(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"],
                                   po, pl)
-        kp = max(20, min(200, 4 * self.R))
-        secs = self.timed(part, kp, warmup_body=lambda: part(5), trials=3)
+        # at least 60 launches per trial and the median of 5 trials: the device's clock settles over
+        # a few milliseconds of back-to-back launches, which 20 launches of the 128k workload do not span
+        kp = max(60, min(200, 4 * self.R))
+        secs = self.timed(part, kp, warmup_body=lambda: part(10), trials=5)
         return float(np.median(secs)) / kp
 
     def measure(self, n_steps, warmup, trials, naive=True, mall_warm=False):
@@ -519,6 +523,13 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
 
+    if args.yardstick_copy:
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     ns = tuple(int(x) for x in args.prefill_tokens.split(",") if x)
     if args.prefill_only:
         print(json.dumps({"instruction_prefill": prefill_timing(torch, fa, W, ns, args.trials)}), flush=True)
