@@ -22,6 +22,7 @@ struct fka_plan {
     int32_t share_prefix = 1;
     int32_t prefill_n = 0;     // instruction prefill plan: tokens per branch (sequences are b * n + t)
     int32_t n_branches = 0;    // instruction prefill plan: branches
+    int32_t prefill_groups = 1; // instruction prefill plan: units per block
     int32_t max_suffix_len = 0;
     // contiguous
     int32_t prefix_len = 0, suffix_cap = 0;
@@ -326,6 +327,7 @@ fka::AttnArgs attn_args(const fka_plan *p)
     a.max_pages = p->max_pages;
     a.n_pool_pages = p->n_pool_pages;
     a.paged = p->paged ? 1 : 0;
+    a.prefill_groups = p->prefill_groups;
     return a;
 }
 
@@ -478,20 +480,26 @@ fka_status fka_plan_create_prefill(const fka_heads *heads, const fka_prefill_des
     int cus = 0;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
         return bail(hip_fail(e, "hipDeviceGetAttribute"));
-    // Units of consecutive instruction tokens, at most kMaxRows query rows each, all over the one
-    // prefix: as few as that allows.  Each unit's waves load every prefix tile once more (from L2)
-    // and score it against the unit's 16-row tiles, so fewer, taller units keep the matrix cores
-    // busy per byte loaded (one tile per slice does not cover the loads; four do).  Each of the
-    // U x Hkv items then takes B = resident / items blocks (at least one); with U x Hkv a multiple
+    // Units of consecutive instruction tokens, at most prefill_max_rows query rows each (32 for
+    // d = 128: two waves per SIMD), all over the one prefix: as few as that allows.  Each unit's
+    // waves load every prefix tile once more (from L2) and score it against the unit's 16-row
+    // tiles, so taller units keep the matrix cores busy per byte loaded.  Each set of P units of
+    // one KV head then takes B = resident / sets blocks (at least one); with the sets a multiple
     // of the 8 XCDs the blocks of a KV head all run on one XCD and share its prefix tiles in L2.
-    const int32_t best_U = ceil_div(S, fka::kMaxRows / G);
+    const int32_t best_U = ceil_div(S, fka::prefill_max_rows(p->d, G) / G);
     const int32_t best_tiles = ceil_div(ceil_div(S, best_U) * G, 16);
     const int per_cu = fka::prefill_blocks_per_cu(p->d, best_tiles);
     if (per_cu <= 0) return bail(fail(FKA_ERR_HIP, "occupancy query of the prefill kernel failed"));
     const int64_t items = (int64_t)best_U * p->Hkv;
     const int64_t resident = (int64_t)cus * per_cu;
-    const int32_t best_B = (int32_t)(desc->blocks > 0 ? std::max<int64_t>(1, desc->blocks / items)
-                                                     : std::max<int64_t>(1, resident / items));
+    // Units per block: when the items alone would need more blocks than are resident at once (a
+    // second round would fetch the prefix from HBM again), an eight-wave block takes two units of
+    // one KV head, four waves each, over the same prefix range.
+    const int waves = fka::prefill_waves_per_block(p->d, best_tiles);
+    const int32_t P = (waves == 8 && p->d == 128 && items > resident && best_U > 1) ? 2 : 1;
+    const int64_t sets = (int64_t)ceil_div(best_U, P) * p->Hkv;
+    const int32_t best_B = (int32_t)(desc->blocks > 0 ? std::max<int64_t>(1, desc->blocks / sets)
+                                                     : std::max<int64_t>(1, resident / sets));
     const int32_t U = best_U;
     int32_t max_nseq = 0;
     for (int32_t u = 0; u < U; ++u) {
@@ -509,10 +517,11 @@ fka_status fka_plan_create_prefill(const fka_heads *heads, const fka_prefill_des
     p->n_items = U * p->Hkv;
     p->slot_rows = max_nseq * G;
     p->row_tiles = best_tiles;
-    p->waves = fka::partials_waves_per_block(p->d, p->row_tiles, false);
-    p->n_blocks = best_B * p->n_items;
+    p->waves = waves;
+    p->prefill_groups = P;
+    p->n_blocks = (int32_t)(best_B * sets);
     p->rounds = 1;
-    p->n_slots = p->n_blocks;
+    p->n_slots = best_B * p->n_items;
     if ((st = finish_plan(p)) != FKA_OK) return bail(st);
     *out = p;
     return ok();
@@ -594,6 +603,7 @@ fka_status fka_plan_get_info(const fka_plan *p, fka_plan_info *info)
     info->n_slots = p->n_slots;
     info->slot_rows = p->slot_rows;
     info->static_split = p->static_split ? 1 : 0;
+    info->units_per_block = p->prefill_groups;
     info->workspace_bytes = p->workspace_bytes;
     return ok();
 }

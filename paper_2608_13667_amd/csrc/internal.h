@@ -148,6 +148,7 @@ struct AttnArgs {
     // instruction prefill (the prefill kernel only): sequence s = b n + t is instruction token t of
     // branch b, reading b's suffix buffer up to position suffix_len[b] + t (n = prefill_n)
     int32_t prefill_n;
+    int32_t prefill_groups;  // instruction prefill: units per block, each taken by NW / groups waves
 };
 
 struct MergeArgs {
@@ -242,6 +243,10 @@ hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int ro
 int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged);
 // Waves per block of the partial kernel for this shape.
 int partials_waves_per_block(int head_dim, int row_tiles, bool paged);
+int prefill_waves_per_block(int head_dim, int row_tiles);
+// Query rows (tokens x G) per unit of the instruction prefill: 32 for d = 128 (two tiles, two
+// waves per SIMD) when a unit of 32 rows holds a token, else kMaxRows.
+int prefill_max_rows(int head_dim, int group);
 // Instruction prefill: the partial kernel over virtual sequences (AttnArgs::prefill_n) with the
 // cyclic placement (block vb holds item vb mod items), contiguous layout.
 hipError_t launch_prefill(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);

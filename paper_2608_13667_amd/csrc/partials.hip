@@ -219,11 +219,15 @@ __device__ inline bf16x8 join_tr16(vtr_t lo, vtr_t hi)
 // one wave per SIMD with the whole register file (three or four 16-row tiles need it; with one
 // or two, contiguous K/V measured 1% faster on the 32k-prefix workload and 5% on the 8k one
 // than two waves of <= 256 VGPRs, whose older wave finishes well before the younger), except
-// paged K/V with one or two tiles, where two waves per SIMD measured 11% faster.  d = 64: two.
-template <int HD, int NT, bool PAGED>
+// paged K/V with one or two tiles, where two waves per SIMD measured 11% faster, and the
+// instruction prefill with one or two tiles, which is bound by instruction issue rather than
+// bytes: there the second wave's matrix and vector work fills the first one's stalls (32-row
+// units at two waves per SIMD measured 4-11% faster at the 32k shape than 64-row units at one).
+// d = 64: two.
+template <int HD, int NT, bool PAGED, bool PREFILL>
 constexpr int waves_per_simd()
 {
-    return (HD <= 64 || (PAGED && NT <= 2)) ? 2 : 1;
+    return (HD <= 64 || ((PAGED || PREFILL) && NT <= 2)) ? 2 : 1;
 }
 
 // Where the keys of one slice come from (every field uniform over the wave).
@@ -238,10 +242,10 @@ struct SliceSrc {
 };
 
 template <int HD, int NT, bool PAGED, bool PREFILL>
-__global__ __launch_bounds__((256 * waves_per_simd<HD, NT, PAGED>()))
-__attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void partials_kernel(AttnArgs a)
+__global__ __launch_bounds__((256 * waves_per_simd<HD, NT, PAGED, PREFILL>()))
+__attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED, PREFILL>()))) void partials_kernel(AttnArgs a)
 {
-    constexpr int NW = 4 * waves_per_simd<HD, NT, PAGED>();  // waves per block
+    constexpr int NW = 4 * waves_per_simd<HD, NT, PAGED, PREFILL>();  // waves per block
     constexpr int NTH = 64 * NW;
     constexpr int CPR = HD / 8;                 // 16-byte chunks per K/V row
     constexpr int NC = HD / 32;                 // MFMA k-steps of q.k
@@ -276,7 +280,17 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
+    // Wave w runs on SIMD w mod 4, and of the two waves of a SIMD the older (w < 4) runs ahead.
+    // When an eight-wave prefill block takes two units (prefill_groups 2), the waves are numbered
+    // so that both units' groups hold two older waves at positions 0-1 and two younger ones at
+    // positions 2-3 (group 0: waves 0, 1, 6, 7; group 1: 2, 3, 4, 5): a prefix slice is then read
+    // by waves of the same age in both groups, so the units stay together on the prefix and share
+    // its tiles through L2 (with one group of older and one of younger waves, the younger group
+    // fell behind and a quarter of the prefix was fetched from HBM twice).
+    const int hw_wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(
+        (PREFILL && NW == 8 && a.prefill_groups == 2) ? (hw_wave < 2 ? hw_wave : hw_wave < 6 ? hw_wave + 2 : hw_wave - 4)
+                                                      : hw_wave);  // uniform per wave
     const int l16 = lane & 15, q4 = lane >> 4;
     const int G = a.group, Hkv = a.n_kv_heads, N = a.n_seqs;
     const int vb = (int)blockIdx.x;
@@ -350,29 +364,38 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
         if (vb == 0 && clamped) atomicOr(a.err, kErrSuffixClamped);
         if (tid < NW) s_wf[tid][0] = -1;  // waves the placement below does not reach have no item
         if constexpr (PREFILL) {
-            // Cyclic placement: block vb is block k = vb / n_items of item vb mod n_items (each
-            // item has B = blocks / n_items blocks, all its waves one group); with n_items a
-            // multiple of the 8 XCDs, every block of a KV head runs on one XCD, so the blocks of
-            // one prefix range, one per unit, share its tiles through that XCD's L2.
-            const int n_items = a.n_units * Hkv, B = (int)gridDim.x / n_items;
-            const int i = vb % n_items, k = vb / n_items;
+            // Cyclic placement over block sets: a set is P = prefill_groups units of one KV head
+            // (its blocks split into P groups of NW / P waves, group j taking the set's j-th unit
+            // over the same prefix range as the others, so they stream the same tiles side by
+            // side); block vb is block k = vb / n_sets of set vb mod n_sets, each set having
+            // B = blocks / n_sets blocks.  With n_sets a multiple of the 8 XCDs, every block of a
+            // KV head runs on one XCD, so the blocks of one prefix range, one per unit, share its
+            // tiles through that XCD's L2.
+            const int P = a.prefill_groups, GW = NW / P;
+            const int n_sets = (a.n_units + P - 1) / P * Hkv, B = (int)gridDim.x / n_sets;
+            const int set = vb % n_sets, k = vb / n_sets;
+            const int g = set % Hkv, us = set / Hkv;
             lds_barrier();  // the unit table
             if (tid < NW) {
+                const int grp = tid / GW, u = us * P + grp;
                 int32_t *d = s_wf[tid];
-                d[0] = i;
-                d[1] = i / Hkv;
-                d[2] = B * NW;
-                d[3] = k * NW;
-                d[4] = (k + 1) * NW;
-                d[5] = 0;
-                d[6] = NW;
+                d[0] = u < a.n_units ? u * Hkv + g : -1;
+                d[1] = u;
+                d[2] = B * GW;
+                d[3] = k * GW;
+                d[4] = (k + 1) * GW;
+                d[5] = grp * GW;
+                d[6] = grp * GW + GW;
             }
-            if (k == 0) {  // the item's rows read their B parts at slots i B .. i B + B - 1
-                const int u = i / Hkv, g = i - u * Hkv;
-                for (int r = tid; r < s_un[u] * G; r += NTH) {
-                    int32_t *rr = a.rowrec + ((size_t)(s_u0[u] + r / G) * a.n_q_heads + g * G + r % G) * kRowRec;
-                    rr[0] = i * B * a.slot_rows + r;
-                    rr[1] = B;
+            if (k == 0) {  // the rows of item i read their B parts at slots i B .. i B + B - 1
+                for (int grp = 0; grp < P; ++grp) {
+                    const int u = us * P + grp, i = u * Hkv + g;
+                    if (u >= a.n_units) break;
+                    for (int r = tid; r < s_un[u] * G; r += NTH) {
+                        int32_t *rr = a.rowrec + ((size_t)(s_u0[u] + r / G) * a.n_q_heads + g * G + r % G) * kRowRec;
+                        rr[0] = i * B * a.slot_rows + r;
+                        rr[1] = B;
+                    }
                 }
             }
         } else {
@@ -891,9 +914,9 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED>()))) void parti
             const int4 gi = *reinterpret_cast<const int4 *>(&s_grp[g][0]);
             asm volatile("" ::"v"(gi.x), "v"(gi.y), "v"(gi.z), "v"(gi.w));  // one LDS read, not four
             const int lw = gi.x, ge = gi.y, it = gi.w;
-            // the group's slot: vb + it, or under the cyclic placement it B + (vb / n_items)
-            const int n_items_c = a.n_units * Hkv;
-            const int slot_c = PREFILL ? it * ((int)gridDim.x / n_items_c) + vb / n_items_c : vb + it;
+            // the group's slot: vb + it, or under the cyclic placement it B + (vb / n_sets)
+            const int n_sets_c = (a.n_units + a.prefill_groups - 1) / a.prefill_groups * Hkv;
+            const int slot_c = PREFILL ? it * ((int)gridDim.x / n_sets_c) + vb / n_sets_c : vb + it;
             if (slot_c >= a.n_slots || it < 0) continue;  // never store outside the workspace
             const int r0 = 16 * TPP * pass, r1 = min(gi.z, r0 + 16 * TPP);
             const bool whole = lw == 0 && ge == NW;  // the usual case: one group, all waves
@@ -959,10 +982,10 @@ int blocks_per_cu_hd(int row_tiles)
     const void *f = nullptr;
     int threads = 0;
     switch (row_tiles) {
-    case 1: f = reinterpret_cast<const void *>(&partials_kernel<HD, 1, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 1, PAGED>(); break;
-    case 2: f = reinterpret_cast<const void *>(&partials_kernel<HD, 2, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 2, PAGED>(); break;
-    case 3: f = reinterpret_cast<const void *>(&partials_kernel<HD, 3, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 3, PAGED>(); break;
-    case 4: f = reinterpret_cast<const void *>(&partials_kernel<HD, 4, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 4, PAGED>(); break;
+    case 1: f = reinterpret_cast<const void *>(&partials_kernel<HD, 1, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 1, PAGED, PREFILL>(); break;
+    case 2: f = reinterpret_cast<const void *>(&partials_kernel<HD, 2, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 2, PAGED, PREFILL>(); break;
+    case 3: f = reinterpret_cast<const void *>(&partials_kernel<HD, 3, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 3, PAGED, PREFILL>(); break;
+    case 4: f = reinterpret_cast<const void *>(&partials_kernel<HD, 4, PAGED, PREFILL>); threads = 256 * waves_per_simd<HD, 4, PAGED, PREFILL>(); break;
     default: return 0;
     }
     int n = 0;
@@ -975,10 +998,10 @@ hipError_t launch_hd(const AttnArgs &a, int n_blocks, int row_tiles, hipStream_t
 {
     const dim3 grid(n_blocks);
     switch (row_tiles) {
-    case 1: partials_kernel<HD, 1, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 1, PAGED>(), 0, s>>>(a); break;
-    case 2: partials_kernel<HD, 2, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 2, PAGED>(), 0, s>>>(a); break;
-    case 3: partials_kernel<HD, 3, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 3, PAGED>(), 0, s>>>(a); break;
-    case 4: partials_kernel<HD, 4, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 4, PAGED>(), 0, s>>>(a); break;
+    case 1: partials_kernel<HD, 1, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 1, PAGED, PREFILL>(), 0, s>>>(a); break;
+    case 2: partials_kernel<HD, 2, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 2, PAGED, PREFILL>(), 0, s>>>(a); break;
+    case 3: partials_kernel<HD, 3, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 3, PAGED, PREFILL>(), 0, s>>>(a); break;
+    case 4: partials_kernel<HD, 4, PAGED, PREFILL><<<grid, 256 * waves_per_simd<HD, 4, PAGED, PREFILL>(), 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -995,22 +1018,34 @@ int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged)
     return 0;
 }
 
-template <bool PAGED>
+template <bool PAGED, bool PREFILL>
 int waves_per_block_hd128(int row_tiles)
 {
     switch (row_tiles) {
-    case 1: return 4 * waves_per_simd<128, 1, PAGED>();
-    case 2: return 4 * waves_per_simd<128, 2, PAGED>();
-    case 3: return 4 * waves_per_simd<128, 3, PAGED>();
-    case 4: return 4 * waves_per_simd<128, 4, PAGED>();
+    case 1: return 4 * waves_per_simd<128, 1, PAGED, PREFILL>();
+    case 2: return 4 * waves_per_simd<128, 2, PAGED, PREFILL>();
+    case 3: return 4 * waves_per_simd<128, 3, PAGED, PREFILL>();
+    case 4: return 4 * waves_per_simd<128, 4, PAGED, PREFILL>();
     default: return 0;
     }
 }
 
 int partials_waves_per_block(int head_dim, int row_tiles, bool paged)
 {
-    if (head_dim == 64) return 4 * waves_per_simd<64, 1, false>();
-    return paged ? waves_per_block_hd128<true>(row_tiles) : waves_per_block_hd128<false>(row_tiles);
+    if (head_dim == 64) return 4 * waves_per_simd<64, 1, false, false>();
+    return paged ? waves_per_block_hd128<true, false>(row_tiles) : waves_per_block_hd128<false, false>(row_tiles);
+}
+
+int prefill_max_rows(int head_dim, int group)
+{
+    // two 16-row tiles per wave where a unit of them holds at least one token (two waves per SIMD)
+    return (head_dim == 128 && group <= 32) ? 32 : kMaxRows;
+}
+
+int prefill_waves_per_block(int head_dim, int row_tiles)
+{
+    if (head_dim == 64) return 4 * waves_per_simd<64, 1, false, true>();
+    return waves_per_block_hd128<false, true>(row_tiles);
 }
 
 hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s)

@@ -50,7 +50,8 @@ class PrefillDesc(C.Structure):
 class PlanInfo(C.Structure):
     _fields_ = [("n_items", C.c_int32), ("n_units", C.c_int32), ("waves_per_block", C.c_int32),
                 ("n_blocks", C.c_int32), ("rounds", C.c_int32), ("n_slots", C.c_int32), ("slot_rows", C.c_int32),
-                ("static_split", C.c_int32), ("workspace_bytes", C.c_size_t)]
+                ("static_split", C.c_int32), ("units_per_block", C.c_int32),
+                ("workspace_bytes", C.c_size_t)]
 
 
 class Slot(C.Structure):

@@ -74,8 +74,11 @@ def test_prefill_long_shape(fa, n):
     m = gates.assert_gates(out, ref, what=f"prefill long n={n}")
     gates.assert_lse(lse, ref_lse, what=f"prefill long n={n}")
     assert plan.device_error() == 0
-    # the units of one KV head are a multiple of the 8 XCDs apart, so that they share prefix tiles
-    assert info.n_items % 8 == 0 and info.n_blocks % info.n_items == 0
+    # the block sets (units_per_block units of one KV head) are a multiple of the 8 XCDs apart, so
+    # that the units of a KV head share its prefix tiles; one round of resident blocks
+    P, cus = info.units_per_block, torch.cuda.get_device_properties(0).multi_processor_count
+    sets = -(-info.n_units // P) * 8
+    assert info.n_blocks % sets == 0 and info.n_blocks <= cus and (P == 1 or info.n_items > cus)
     print(f"[prefill] long n={n} {m}", flush=True)
 
 
@@ -102,6 +105,37 @@ def _random_cases(k, seed):
 def test_prefill_random_shapes(fa, c):
     """Seeded shapes: d 64 / 128, 1..8 KV heads, G 1..8, 1..6 branches, 1..39 tokens, prefixes of
     0..3000 (some not a multiple of the 32-key slice), existing suffixes, explicit grids."""
+    _check_case(fa, c)
+
+
+@pytest.mark.parametrize("g", [32, 40, 64])
+def test_prefill_wide_groups(fa, g):
+    """d 128 with G = 32 (units of one token, 32 rows, two waves per SIMD) and G = 40 and 64, where
+    a 32-row unit holds no token and the units take up to 64 rows (three or four tiles, one wave
+    per SIMD)."""
+    _check_case(fa, dict(head_dim=128, n_kv_heads=2, n_q_heads=2 * g, n_branches=3, n=3, prefix_len=1000, lo=7,
+                         blocks=0, seed=2603 + g))
+
+
+def test_prefill_paired_units(fa):
+    """More items than resident blocks (33 units of 6 tokens x 8 KV heads at the 32k shape's
+    heads): the plan pairs two units of a KV head per eight-wave block, the last block set holding
+    a single unit; every row of every token checked."""
+    n = 66
+    spec = W.CONFIGS["long"].replace(prefix_len=700, n_branches=3, suffix_range=(0, 9), steps=n, seed=2660)
+    w = W.make(spec)
+    q, sk, sv = _instruction(w, n)
+    plan, out, lse = _run(fa, w, n, q, sk, sv)
+    info = plan.info()
+    print(f"[prefill] paired: {info.n_units} units, {info.n_items} items, {info.n_blocks} blocks", flush=True)
+    assert info.n_units == 33 and info.units_per_block == 2 and info.n_blocks == 17 * 8
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    gates.assert_gates(out, ref, what="paired units")
+    gates.assert_lse(lse, ref_lse, what="paired units")
+    assert plan.device_error() == 0
+
+
+def _check_case(fa, c):
     spec = W.CONFIGS["mid"].replace(head_dim=c["head_dim"], n_kv_heads=c["n_kv_heads"], n_q_heads=c["n_q_heads"],
                                     n_branches=c["n_branches"], prefix_len=c["prefix_len"],
                                     suffix_range=(c["lo"], c["lo"] + 30), steps=c["n"], seed=c["seed"])
