@@ -170,7 +170,10 @@ fka_status fka_fork_step(const fka_plan *plan, const void *q, const void *k_new,
 
 /* Several independent forks ("groups", e.g. one per agent task) whose K/V live in
  * one pool of fixed-size pages.  Sequence i of group t shares the t-th prefix
- * pages with the other sequences of its group. */
+ * pages with the other sequences of its group: within a group this is the fork of
+ * Sec. 3.3 (every branch continues from the same snapshot, whose prefix K/V all of
+ * them reuse), and the groups are the agent tasks served side by side.  The page
+ * layout itself is a serving choice the paper leaves open. */
 typedef struct {
     int32_t n_seqs;            /* S sequences over all groups */
     int32_t n_groups;          /* T groups */
@@ -200,7 +203,9 @@ fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *d
                                  const int32_t *host_group_prefix_len, fka_plan **out);
 
 /*
- * One decode step over the paged pool.
+ * One decode step over the paged pool (Sec. 3.2 Overview: the branches of every fork
+ * decode concurrently; Sec. 3.3: the prefix pages of a group are read once for all its
+ * sequences).
  *   q          bf16 [S][Hq][d]
  *   k_pool     bf16 [n_pages][Hkv][page_size][d]   (v_pool likewise); a (page, head) block is contiguous
  *   page_table int32 [S][max_pages_per_seq] (device)
