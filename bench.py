@@ -339,9 +339,11 @@ def cpu_oracle(oracle, w, n_seq, hq, seconds):
 def lifecycle_timing(fa, torch, w):
     """One turn transition of the fork lifecycle at the workload's shape, with a page pool: fork
     the snapshot to all sequences, reserve their suffix pages, drop the branches, promote the main
-    sequence (host bookkeeping), and the promote's device work (a gather of the main context's tail,
-    from the first page the dense layout rewrites, and its scatter into the dense pages).  Host calls are timed with perf_counter over many cycles,
-    the device work with HIP events on the launch stream."""
+    sequence (host bookkeeping), the promote's device work (a gather of the main context's tail,
+    from the first page the dense layout rewrites, and its scatter into the dense pages), and the
+    branches' instruction prefill on the pool after a fork (fka_prefill_paged, 16 tokens per
+    branch).  Host calls are timed with perf_counter over many cycles, the device work with HIP
+    events on the launch stream."""
     spec = w.spec
     N, Hkv, d = w.n_branches, spec.n_kv_heads, spec.head_dim
     Lp, lens = w.prefix_len, [int(x) for x in w.suffix_len]
@@ -409,37 +411,38 @@ def lifecycle_timing(fa, torch, w):
     plan.close()
     pool.release(dense)
     pool.release(snap)
-    # branch-instruction prefill, one chunk: n tokens per branch as N * n virtual sequences in one
-    # group (token t of branch b reads b's pages with suffix length L_b + t + 1), as many as the
-    # 64 query rows per KV head allow; the prefix is read once per chunk
-    G = spec.n_q_heads // Hkv
-    n = max(1, 64 // (N * G))
+    # branch-instruction prefill on the pool (fka_prefill_paged): after a fresh fork (empty
+    # suffixes) every branch takes n instruction tokens into pages reserved for them (MALL-warm:
+    # one pool)
+    n = 16
+    Hq = spec.n_q_heads
     table = np.full((N, max_pages), -1, np.int32)
     snap2 = pool.alloc(a)
     pool.fork(snap2, table, 0, N)
     for b in range(N):
-        pool.reserve(table, b, Lp, min(lens[b] + n, max(lens)))
-    vt = torch.from_numpy(np.repeat(table, n, axis=0)).cuda()
-    vlen_np = np.array([min(lens[b] + t + 1, max(lens)) for b in range(N) for t in range(n)], np.int32)
-    vlen = torch.from_numpy(vlen_np).cuda()
-    pplan = fa.Plan.paged_plan(spec.n_q_heads, Hkv, d, [0, N * n], [Lp], max_pages, n_pages, max(lens))
-    q = torch.zeros((N * n, spec.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
-    o = torch.empty((N * n, spec.n_q_heads, d), device="cuda")
-    for _ in range(20):
-        pplan.decode_paged(q, pages, v_pages, vt, vlen, o, None, stream)
+        pool.reserve(table, b, Lp, n)
+    pplan = fa.Plan.prefill_paged_plan(Hq, Hkv, d, N, n, Lp, max_pages, n_pages, n)
+    vt = torch.from_numpy(table).cuda()
+    lens_dev = torch.zeros(N, dtype=torch.int32, device="cuda")
+    q = torch.zeros((N, n, Hq, d), dtype=torch.bfloat16, device="cuda")
+    o = torch.empty((N, n, Hq, d), device="cuda")
+    for _ in range(5):
+        pplan.prefill_paged(q, pages, v_pages, vt, lens_dev, o, None, stream)
     e0.record(stream)
-    for _ in range(reps * 5):
-        pplan.decode_paged(q, pages, v_pages, vt, vlen, o, None, stream)
+    for _ in range(reps):
+        pplan.prefill_paged(q, pages, v_pages, vt, lens_dev, o, None, stream)
     e1.record(stream)
     torch.cuda.synchronize()
-    pf_s = e0.elapsed_time(e1) / 1e3 / (reps * 5)
-    pf_bytes = per_tok * (Lp + sum(int(x) for x in vlen_np))  # the prefix once, each token's suffix
+    pf_s = e0.elapsed_time(e1) / 1e3 / reps
+    # the prefix once, each branch's instruction
+    pf_bytes = per_tok * (Lp + N * n)
     pplan.close()
     pool.close()
     ms = lambda v: float(np.median(v) * 1e6)
     return {"tokens_promoted": L0, "host_us": {k: ms(v) for k, v in host.items()},
             "promote_device_us": dev_s * 1e6, "promote_device_gbps": moved / dev_s / 1e9,
-            "prefill_chunk": {"tokens_per_branch": n, "us": pf_s * 1e6, "kv_gbps": pf_bytes / pf_s / 1e9}}
+            "prefill_paged": {"tokens_per_branch": n, "us": pf_s * 1e6, "us_per_token": pf_s * 1e6 / (N * n),
+                              "kv_gbps": pf_bytes / pf_s / 1e9, "cache": "MALL-warm (one pool)"}}
 
 
 def prefill_timing(torch, fa, W, ns, trials):
@@ -447,7 +450,8 @@ def prefill_timing(torch, fa, W, ns, trials):
     tokens at the fork (existing suffixes empty).  HBM-cold: the calls cycle over prefix replicas
     totalling 3x the 256 MiB MALL.  Per n: us per call and per token, effective K/V GB/s (the
     prefix once, each branch's instruction once) against 8 TB/s, and MFMA TFLOP/s (4 Lp d per
-    query row: q.k and p.v over the prefix) against the 2.5 PFLOP/s bf16 peak."""
+    query row: q.k and p.v over the prefix) against the 2.5 PFLOP/s bf16 peak; and the same calls
+    over a page pool with permuted page ids (fka_prefill_paged)."""
     n_max = max(ns)
     w = W.make("long", steps=n_max, suffix_range=(0, 0), seed=2700)
     s = w.spec
@@ -465,26 +469,41 @@ def prefill_timing(torch, fa, W, ns, trials):
     skd, svd = dev(sk), dev(sv)
     len0 = torch.zeros(N, dtype=torch.int32, device="cuda")
     cap = w.suffix_cap
+    # the same K/V in a page pool (fka_prefill_paged): 16-token pages whose ids are a seeded
+    # permutation, the prefix pages shared by every branch's row; R pool replicas, as above
+    npre, nsuf = -(-Lp // 16), -(-cap // 16)
+    perm = np.random.default_rng(2701).permutation(npre + N * nsuf)
+    table = np.empty((N, npre + nsuf), np.int32)
+    pools = []
+    for src_p, src_s in ((w.prefix_k, sk), (w.prefix_v, sv)):
+        pool = np.zeros((npre + N * nsuf, Hkv, 16, d), np.uint16)
+        pad = np.zeros((Hkv, npre * 16, d), np.uint16)
+        pad[:, :Lp] = src_p
+        pool[perm[:npre]] = pad.reshape(Hkv, npre, 16, d).transpose(1, 0, 2, 3)
+        for b in range(N):
+            spad = np.zeros((Hkv, nsuf * 16, d), np.uint16)
+            spad[:, :cap] = src_s[b]
+            ids = perm[npre + b * nsuf:npre + (b + 1) * nsuf]
+            pool[ids] = spad.reshape(Hkv, nsuf, 16, d).transpose(1, 0, 2, 3)
+            table[b] = np.concatenate([perm[:npre], ids])
+        pools.append(pool)
+    kp0, vp0 = dev(pools[0]), dev(pools[1])
+    del pools
+    preps = [(kp0, vp0)] + [(kp0.clone(), vp0.clone()) for _ in range(R - 1)]
+    tab = torch.from_numpy(table).cuda()
     res = {"workload": "long: 40 query / 8 KV heads, d 128, 32768-token prefix, 5 branches, empty suffixes",
-           "replicas": R, "cold": "calls cycle over prefix replicas of 3x the MALL"}
-    for n in ns:
-        plan = fa.Plan.prefill_plan(Hq, Hkv, d, N, n, Lp, cap, cap)
-        info = plan.info()
-        q = dev(np.ascontiguousarray(q_all[:, :n]))
-        out = torch.empty((N, n, Hq, d), device="cuda")
-        lse = torch.empty((N, n, Hq), device="cuda")
+           "replicas": R, "cold": "calls cycle over prefix replicas of 3x the MALL",
+           "paged": "the same calls over a page pool with permuted page ids (fka_prefill_paged)"}
 
-        def body(k):
-            for i in range(k):
-                pk, pv = reps[i % R]
-                plan.prefill(q, pk, pv, skd, svd, len0, out, lse)
-
+    def timed(call):
         K = 4 * R
-        body(2 * R)
+        for i in range(2 * R):
+            call(i)
         torch.cuda.synchronize()
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            body(K)
+            for i in range(K):
+                call(i)
         torch.cuda.synchronize()
         ts = []
         for _ in range(trials):
@@ -494,17 +513,32 @@ def prefill_timing(torch, fa, W, ns, trials):
             e1.record()
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1) * 1e-3 / K)
-        t = float(np.median(ts))
+        del graph
+        return float(np.median(ts)), ts
+
+    for n in ns:
+        plan = fa.Plan.prefill_plan(Hq, Hkv, d, N, n, Lp, cap, cap)
+        pplan = fa.Plan.prefill_paged_plan(Hq, Hkv, d, N, n, Lp, table.shape[1], kp0.shape[0], cap)
+        info = plan.info()
+        q = dev(np.ascontiguousarray(q_all[:, :n]))
+        out = torch.empty((N, n, Hq, d), device="cuda")
+        lse = torch.empty((N, n, Hq), device="cuda")
         kv = pref_bytes + N * n * 2 * Hkv * d * 2
         flop = 4.0 * Hq * N * n * Lp * d
+        t, ts = timed(lambda i: plan.prefill(q, reps[i % R][0], reps[i % R][1], skd, svd, len0, out, lse))
+        tp, tsp = timed(lambda i: pplan.prefill_paged(q, preps[i % R][0], preps[i % R][1], tab, len0, out, lse))
         res[f"n{n}"] = {"us_per_call": t * 1e6, "us_per_token": t * 1e6 / (N * n), "effective_kv_gbps": kv / t / 1e9,
                         "hbm_peak_frac": kv / t / 8e12, "tflops": flop / t / 1e12, "mfma_bf16_peak_frac": flop / t / 2.5e15,
-                        "units": info.n_units, "blocks": info.n_blocks, "trials_us": [x * 1e6 for x in ts]}
+                        "units": info.n_units, "blocks": info.n_blocks, "trials_us": [x * 1e6 for x in ts],
+                        "paged": {"us_per_call": tp * 1e6, "us_per_token": tp * 1e6 / (N * n),
+                                  "effective_kv_gbps": kv / tp / 1e9, "tflops": flop / tp / 1e12,
+                                  "trials_us": [x * 1e6 for x in tsp]}}
         log(f"[bench] prefill n={n}: {t * 1e6:.1f} us per call ({t * 1e6 / (N * n):.2f} us/token), "
             f"{kv / t / 1e9:.0f} GB/s ({kv / t / 8e12:.1%} of 8 TB/s), {flop / t / 1e12:.0f} TFLOP/s "
-            f"({flop / t / 2.5e15:.1%} of 2.5 PFLOP/s); {info.n_units} units, {info.n_blocks} blocks")
-        del plan, graph
-    del reps
+            f"({flop / t / 2.5e15:.1%} of 2.5 PFLOP/s); {info.n_units} units, {info.n_blocks} blocks; "
+            f"paged {tp * 1e6:.1f} us per call")
+        del plan, pplan
+    del reps, preps
     return res
 
 

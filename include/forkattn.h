@@ -363,6 +363,42 @@ fka_status fka_prefill(const fka_plan *plan, const void *q, const void *prefix_k
                        const void *suffix_k, const void *suffix_v, const int32_t *suffix_len, float *out,
                        float *out_lse, void *stream);
 
+/* The same prefill over the paged pool (the branches of one fork as in fka_fork_decode_paged):
+ * branch b's row of page_table holds the shared prefix pages at indices [0, ceil(Lp / 16)) (the
+ * same ids in every row) and its suffix position u at index ceil(Lp / 16) + u / 16, slot u % 16;
+ * its n instruction tokens' keys and values are already in its pages at positions
+ * [suffix_len[b], suffix_len[b] + n) (fka_pool_reserve, then fka_scatter_pages or appends). */
+typedef struct {
+    int32_t n_branches;         /* N, >= 1 */
+    int32_t n_tokens;           /* n instruction tokens per branch, >= 1; N x n <= 512 */
+    int32_t prefix_len;         /* Lp, >= 0 */
+    int32_t page_size;          /* tokens per page: 16 */
+    int32_t max_pages_per_seq;  /* columns of page_table; must hold ceil(Lp/16) + ceil(max_suffix_len/16) */
+    int32_t n_pool_pages;       /* pages in k_pool / v_pool; ids outside [0, n_pool_pages) are never read */
+    int32_t max_suffix_len;     /* bound on suffix_len[b] + n_tokens, >= n_tokens */
+    int32_t blocks;             /* 0 = automatic (fill the device); else about this many blocks */
+} fka_prefill_paged_desc;
+
+/* Build a paged instruction-prefill plan.  Only fka_prefill_paged, fka_plan_get_info,
+ * fka_plan_device_error and fka_plan_destroy take it.  Errors as fka_plan_create_prefill; also
+ * FKA_ERR_INVALID_ARG when page_size is not 16 or the pages do not fit max_pages_per_seq. */
+fka_status fka_plan_create_prefill_paged(const fka_heads *heads, const fka_prefill_paged_desc *desc,
+                                         fka_plan **out);
+
+/*
+ * Instruction prefill over the paged pool (two kernel launches, as fka_prefill).
+ *   q          bf16 [N][n][Hq][d]
+ *   k_pool     bf16 [n_pages][Hkv][16][d]   (v_pool likewise)
+ *   page_table int32 [N][max_pages_per_seq] (device), one row per branch
+ *   suffix_len int32 [N] (device): each branch's suffix before the instruction; not changed; a
+ *              value outside [0, max_suffix_len - n] is clamped into it and flagged (1)
+ *   out        fp32 [N][n][Hq][d];  out_lse fp32 [N][n][Hq] or NULL
+ * A page id outside [0, n_pool_pages) is not read (its rows count as zeros) and flag 4 is raised.
+ */
+fka_status fka_prefill_paged(const fka_plan *plan, const void *q, const void *k_pool, const void *v_pool,
+                             const int32_t *page_table, const int32_t *suffix_len, float *out, float *out_lse,
+                             void *stream);
+
 /* -------------------------------------------------------------- stage entry points */
 
 /* The first stage (Sec. 3.3: the prefix is read once for all branches) runs as one kernel

@@ -400,6 +400,102 @@ fka_status scratch_of(int device, char **out)
     return FKA_OK;
 }
 
+// The layout of a prefill plan's suffix keys: contiguous buffers of cap rows, or the page pool.
+struct PrefillLayout {
+    bool paged;
+    int32_t cap;        // contiguous: rows of each branch's suffix buffer
+    int32_t max_pages;  // paged: columns of the page table
+    int32_t n_pool_pages;
+};
+
+fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t Lp, int32_t max_suffix_len,
+                          int32_t blocks, const PrefillLayout &lay, fka_plan **out)
+{
+    const int64_t S = (int64_t)N * n;  // virtual sequences
+    if (S > fka::kMaxSeqs)
+        return fail(FKA_ERR_UNSUPPORTED, "%lld instruction tokens (n_branches x n_tokens) exceed the limit of %d",
+                    (long long)S, fka::kMaxSeqs);
+    const int G = heads->n_q_heads / heads->n_kv_heads;
+    if (G > fka::kMaxRows)
+        return fail(FKA_ERR_UNSUPPORTED, "%d query heads per KV head exceed the limit of %d", G, fka::kMaxRows);
+    if (Lp > kMaxTokens || max_suffix_len > kMaxTokens)
+        return fail(FKA_ERR_UNSUPPORTED, "prefix or suffix longer than %d tokens", kMaxTokens);
+
+    fka_plan *p = new (std::nothrow) fka_plan();
+    if (!p) return fail(FKA_ERR_NOMEM, "host allocation failed");
+    auto bail = [&](fka_status e) {
+        fka_plan_destroy(p);
+        return e;
+    };
+    init_heads(p, heads);
+    p->prefill_n = n;
+    p->n_branches = N;
+    p->n_seqs = (int32_t)S;
+    p->share_prefix = 1;
+    p->prefix_len = Lp;
+    p->max_suffix_len = max_suffix_len;
+    p->paged = lay.paged;
+    if (lay.paged) {
+        p->n_groups = 1;
+        p->page_size = fka::kPageSize;
+        p->max_pages = lay.max_pages;
+        p->n_pool_pages = lay.n_pool_pages;
+    } else {
+        p->suffix_cap = lay.cap;
+    }
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) return bail(hip_fail(e, "hipGetDevice"));
+    int cus = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
+        return bail(hip_fail(e, "hipDeviceGetAttribute"));
+    // Units of consecutive instruction tokens, at most prefill_max_rows query rows each (32 for
+    // d = 128: two waves per SIMD), all over the one prefix: as few as that allows.  Each unit's
+    // waves load every prefix tile once more (from L2) and score it against the unit's 16-row
+    // tiles, so taller units keep the matrix cores busy per byte loaded.  Each set of P units of
+    // one KV head then takes B = resident / sets blocks (at least one); with the sets a multiple
+    // of the 8 XCDs the blocks of a KV head all run on one XCD and share its prefix tiles in L2.
+    const int32_t best_U = ceil_div(S, fka::prefill_max_rows(p->d, G) / G);
+    const int32_t best_tiles = ceil_div(ceil_div(S, best_U) * G, 16);
+    const int per_cu = fka::prefill_blocks_per_cu(p->d, best_tiles, lay.paged);
+    if (per_cu <= 0) return bail(fail(FKA_ERR_HIP, "occupancy query of the prefill kernel failed"));
+    const int64_t items = (int64_t)best_U * p->Hkv;
+    const int64_t resident = (int64_t)cus * per_cu;
+    // Units per block: when the items alone would need more blocks than are resident at once (a
+    // second round would fetch the prefix from HBM again), an eight-wave block takes two units of
+    // one KV head, four waves each, over the same prefix range.
+    const int waves = fka::prefill_waves_per_block(p->d, best_tiles, lay.paged);
+    const int32_t P = (waves == 8 && p->d == 128 && items > resident && best_U > 1) ? 2 : 1;
+    const int64_t sets = (int64_t)ceil_div(best_U, P) * p->Hkv;
+    const int32_t best_B = (int32_t)(blocks > 0 ? std::max<int64_t>(1, blocks / sets)
+                                               : std::max<int64_t>(1, resident / sets));
+    const int32_t U = best_U;
+    int32_t max_nseq = 0;
+    for (int32_t u = 0; u < U; ++u) {
+        fka::UnitRec r{};
+        r.seq0 = (int32_t)(u * S / U);
+        r.nseq = (int32_t)((u + 1) * S / U) - r.seq0;
+        r.plen = Lp;
+        r.ps_before = u * fka::slices_of(Lp);
+        max_nseq = std::max(max_nseq, r.nseq);
+        p->units.push_back(r);
+    }
+    p->seq_prefix_len.assign(p->n_seqs, Lp);
+    p->ps_total = U * fka::slices_of(Lp);
+    p->static_split = false;
+    p->n_items = U * p->Hkv;
+    p->slot_rows = max_nseq * G;
+    p->row_tiles = best_tiles;
+    p->waves = waves;
+    p->prefill_groups = P;
+    p->n_blocks = (int32_t)(best_B * sets);
+    p->rounds = 1;
+    p->n_slots = best_B * p->n_items;
+    fka_status st = finish_plan(p);
+    if (st != FKA_OK) return bail(st);
+    *out = p;
+    return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -451,80 +547,30 @@ fka_status fka_plan_create_prefill(const fka_heads *heads, const fka_prefill_des
             "max_suffix_len (%d) must be in [n_tokens=%d, suffix_cap=%d]", desc->max_suffix_len, desc->n_tokens,
             desc->suffix_cap);
     REQUIRE(desc->blocks >= 0, "blocks (%d) must be >= 0", desc->blocks);
-    const int64_t S = (int64_t)desc->n_branches * desc->n_tokens;  // virtual sequences
-    if (S > fka::kMaxSeqs)
-        return fail(FKA_ERR_UNSUPPORTED, "%lld instruction tokens (n_branches x n_tokens) exceed the limit of %d",
-                    (long long)S, fka::kMaxSeqs);
-    const int G = heads->n_q_heads / heads->n_kv_heads;
-    if (G > fka::kMaxRows)
-        return fail(FKA_ERR_UNSUPPORTED, "%d query heads per KV head exceed the limit of %d", G, fka::kMaxRows);
-    if (desc->prefix_len > kMaxTokens || desc->max_suffix_len > kMaxTokens)
-        return fail(FKA_ERR_UNSUPPORTED, "prefix or suffix longer than %d tokens", kMaxTokens);
+    return create_prefill(heads, desc->n_branches, desc->n_tokens, desc->prefix_len, desc->max_suffix_len,
+                          desc->blocks, PrefillLayout{false, desc->suffix_cap, 0, 0}, out);
+}
 
-    fka_plan *p = new (std::nothrow) fka_plan();
-    if (!p) return fail(FKA_ERR_NOMEM, "host allocation failed");
-    auto bail = [&](fka_status e) {
-        fka_plan_destroy(p);
-        return e;
-    };
-    init_heads(p, heads);
-    p->prefill_n = desc->n_tokens;
-    p->n_branches = desc->n_branches;
-    p->n_seqs = (int32_t)S;
-    p->share_prefix = 1;
-    p->prefix_len = desc->prefix_len;
-    p->suffix_cap = desc->suffix_cap;
-    p->max_suffix_len = desc->max_suffix_len;
-    hipError_t e = hipGetDevice(&p->device);
-    if (e != hipSuccess) return bail(hip_fail(e, "hipGetDevice"));
-    int cus = 0;
-    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
-        return bail(hip_fail(e, "hipDeviceGetAttribute"));
-    // Units of consecutive instruction tokens, at most prefill_max_rows query rows each (32 for
-    // d = 128: two waves per SIMD), all over the one prefix: as few as that allows.  Each unit's
-    // waves load every prefix tile once more (from L2) and score it against the unit's 16-row
-    // tiles, so taller units keep the matrix cores busy per byte loaded.  Each set of P units of
-    // one KV head then takes B = resident / sets blocks (at least one); with the sets a multiple
-    // of the 8 XCDs the blocks of a KV head all run on one XCD and share its prefix tiles in L2.
-    const int32_t best_U = ceil_div(S, fka::prefill_max_rows(p->d, G) / G);
-    const int32_t best_tiles = ceil_div(ceil_div(S, best_U) * G, 16);
-    const int per_cu = fka::prefill_blocks_per_cu(p->d, best_tiles);
-    if (per_cu <= 0) return bail(fail(FKA_ERR_HIP, "occupancy query of the prefill kernel failed"));
-    const int64_t items = (int64_t)best_U * p->Hkv;
-    const int64_t resident = (int64_t)cus * per_cu;
-    // Units per block: when the items alone would need more blocks than are resident at once (a
-    // second round would fetch the prefix from HBM again), an eight-wave block takes two units of
-    // one KV head, four waves each, over the same prefix range.
-    const int waves = fka::prefill_waves_per_block(p->d, best_tiles);
-    const int32_t P = (waves == 8 && p->d == 128 && items > resident && best_U > 1) ? 2 : 1;
-    const int64_t sets = (int64_t)ceil_div(best_U, P) * p->Hkv;
-    const int32_t best_B = (int32_t)(desc->blocks > 0 ? std::max<int64_t>(1, desc->blocks / sets)
-                                                     : std::max<int64_t>(1, resident / sets));
-    const int32_t U = best_U;
-    int32_t max_nseq = 0;
-    for (int32_t u = 0; u < U; ++u) {
-        fka::UnitRec r{};
-        r.seq0 = (int32_t)(u * S / U);
-        r.nseq = (int32_t)((u + 1) * S / U) - r.seq0;
-        r.plen = desc->prefix_len;
-        r.ps_before = u * fka::slices_of(desc->prefix_len);
-        max_nseq = std::max(max_nseq, r.nseq);
-        p->units.push_back(r);
-    }
-    p->seq_prefix_len.assign(p->n_seqs, desc->prefix_len);
-    p->ps_total = U * fka::slices_of(desc->prefix_len);
-    p->static_split = false;
-    p->n_items = U * p->Hkv;
-    p->slot_rows = max_nseq * G;
-    p->row_tiles = best_tiles;
-    p->waves = waves;
-    p->prefill_groups = P;
-    p->n_blocks = (int32_t)(best_B * sets);
-    p->rounds = 1;
-    p->n_slots = best_B * p->n_items;
-    if ((st = finish_plan(p)) != FKA_OK) return bail(st);
-    *out = p;
-    return ok();
+fka_status fka_plan_create_prefill_paged(const fka_heads *heads, const fka_prefill_paged_desc *desc, fka_plan **out)
+{
+    REQUIRE(out != nullptr, "out is null");
+    *out = nullptr;
+    fka_status st = check_heads(heads);
+    if (st != FKA_OK) return st;
+    REQUIRE(desc != nullptr, "desc is null");
+    REQUIRE(desc->n_branches >= 1, "n_branches (%d) must be >= 1", desc->n_branches);
+    REQUIRE(desc->n_tokens >= 1, "n_tokens (%d) must be >= 1", desc->n_tokens);
+    REQUIRE(desc->prefix_len >= 0, "prefix_len (%d) must be >= 0", desc->prefix_len);
+    REQUIRE(desc->page_size == fka::kPageSize, "page_size (%d) must be %d", desc->page_size, fka::kPageSize);
+    REQUIRE(desc->n_pool_pages >= 1, "n_pool_pages must be >= 1");
+    REQUIRE(desc->max_suffix_len >= desc->n_tokens, "max_suffix_len (%d) must be >= n_tokens (%d)",
+            desc->max_suffix_len, desc->n_tokens);
+    REQUIRE(desc->blocks >= 0, "blocks (%d) must be >= 0", desc->blocks);
+    const int64_t pages = ceil_div(desc->prefix_len, fka::kPageSize) + ceil_div(desc->max_suffix_len, fka::kPageSize);
+    REQUIRE(pages <= desc->max_pages_per_seq, "the prefix and max_suffix_len need %lld pages, max_pages_per_seq is %d",
+            (long long)pages, desc->max_pages_per_seq);
+    return create_prefill(heads, desc->n_branches, desc->n_tokens, desc->prefix_len, desc->max_suffix_len,
+                          desc->blocks, PrefillLayout{true, 0, desc->max_pages_per_seq, desc->n_pool_pages}, out);
 }
 
 fka_status fka_plan_create_paged(const fka_heads *heads, const fka_paged_desc *desc, const int32_t *host_group_start,
@@ -764,6 +810,7 @@ fka_status fka_prefill(const fka_plan *p, const void *q, const void *prefix_k, c
 {
     REQUIRE(p != nullptr, "plan is null");
     REQUIRE(p->prefill_n > 0, "plan is not an instruction-prefill plan (fka_plan_create_prefill)");
+    REQUIRE(!p->paged, "plan is a paged prefill plan: use fka_prefill_paged");
     REQUIRE_PTR16(q);
     if (p->prefix_len > 0) {
         REQUIRE_PTR16(prefix_k);
@@ -780,6 +827,34 @@ fka_status fka_prefill(const fka_plan *p, const void *q, const void *prefix_k, c
     a.prefix_v = static_cast<const uint16_t *>(prefix_v);
     a.suffix_k = static_cast<const uint16_t *>(suffix_k);
     a.suffix_v = static_cast<const uint16_t *>(suffix_v);
+    a.suffix_len = suffix_len;
+    a.prefill_n = p->prefill_n;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = fka::launch_prefill(a, p->n_blocks, p->d, p->row_tiles, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill kernel launch");
+    e = fka::launch_merge(merge_args(p, suffix_len, out, out_lse), p->d, s);
+    if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+    return ok();
+}
+
+fka_status fka_prefill_paged(const fka_plan *p, const void *q, const void *k_pool, const void *v_pool,
+                             const int32_t *page_table, const int32_t *suffix_len, float *out, float *out_lse,
+                             void *stream)
+{
+    REQUIRE(p != nullptr, "plan is null");
+    REQUIRE(p->prefill_n > 0 && p->paged, "plan is not a paged instruction-prefill plan (fka_plan_create_prefill_paged)");
+    REQUIRE_PTR16(q);
+    REQUIRE_PTR16(k_pool);
+    REQUIRE_PTR16(v_pool);
+    REQUIRE_PTR4(page_table);
+    REQUIRE_PTR4(suffix_len);
+    REQUIRE_PTR16(out);
+    REQUIRE_OPT4(out_lse);
+    fka::AttnArgs a = attn_args(p);
+    a.q = static_cast<const uint16_t *>(q);
+    a.k_pool = static_cast<const uint16_t *>(k_pool);
+    a.v_pool = static_cast<const uint16_t *>(v_pool);
+    a.page_table = page_table;
     a.suffix_len = suffix_len;
     a.prefill_n = p->prefill_n;
     const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -827,6 +902,7 @@ fka_status fka_partials_paged(const fka_plan *p, const void *q, const void *k_po
 {
     REQUIRE(p != nullptr, "plan is null");
     REQUIRE(p->paged, "plan is contiguous: use fka_partials");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill_paged");
     REQUIRE_PTR16(q);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
@@ -917,6 +993,7 @@ fka_status fka_fork_step_paged(const fka_plan *p, const void *q, const void *k_n
 {
     REQUIRE(p != nullptr, "plan is null");
     REQUIRE(p->paged, "plan is contiguous: use fka_fork_step");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill_paged");
     REQUIRE_PTR16(q);
     REQUIRE_PTR16(k_new);
     REQUIRE_PTR16(v_new);
@@ -949,6 +1026,7 @@ fka_status fka_fork_decode_paged(const fka_plan *p, const void *q, const void *k
 {
     REQUIRE(p != nullptr, "plan is null");
     REQUIRE(p->paged, "plan is contiguous: use fka_fork_decode");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill_paged");
     REQUIRE_PTR16(q);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);
@@ -970,6 +1048,7 @@ fka_status fka_append_kv_paged(const fka_plan *p, const void *k_new, const void 
 {
     REQUIRE(p != nullptr, "plan is null");
     REQUIRE(p->paged, "plan is contiguous: use fka_append_kv");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill_paged");
     REQUIRE_PTR16(k_new);
     REQUIRE_PTR16(v_new);
     REQUIRE_PTR16(k_pool);
@@ -1008,6 +1087,7 @@ fka_status fka_gather_paged_range(const fka_plan *p, int32_t seq, int32_t begin,
 {
     REQUIRE(p != nullptr, "plan is null");
     REQUIRE(p->paged, "plan is contiguous");
+    REQUIRE(!p->prefill_n, "plan is an instruction-prefill plan: use fka_prefill_paged");
     REQUIRE(seq >= 0 && seq < p->n_seqs, "seq %d out of range [0, %d)", seq, p->n_seqs);
     REQUIRE_PTR16(k_pool);
     REQUIRE_PTR16(v_pool);

@@ -243,14 +243,15 @@ hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int ro
 int partials_blocks_per_cu(int head_dim, int row_tiles, bool paged);
 // Waves per block of the partial kernel for this shape.
 int partials_waves_per_block(int head_dim, int row_tiles, bool paged);
-int prefill_waves_per_block(int head_dim, int row_tiles);
+int prefill_waves_per_block(int head_dim, int row_tiles, bool paged);
 // Query rows (tokens x G) per unit of the instruction prefill: 32 for d = 128 (two tiles, two
 // waves per SIMD) when a unit of 32 rows holds a token, else kMaxRows.
 int prefill_max_rows(int head_dim, int group);
 // Instruction prefill: the partial kernel over virtual sequences (AttnArgs::prefill_n) with the
-// cyclic placement (block vb holds item vb mod items), contiguous layout.
+// cyclic placement over block sets, contiguous suffix buffers or (AttnArgs::paged) the page pool,
+// where a virtual sequence reads its branch's page-table row.
 hipError_t launch_prefill(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);
-int prefill_blocks_per_cu(int head_dim, int row_tiles);
+int prefill_blocks_per_cu(int head_dim, int row_tiles, bool paged);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);

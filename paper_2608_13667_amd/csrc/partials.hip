@@ -545,7 +545,9 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<HD, NT, PAGED, PREFILL>()))) v
         if (PAGED) {
             s.kb = arg_kp;
             s.vb = arg_vp;
-            s.ptab = uni_ptr(arg_pt + (size_t)(iss ? seq : seq0) * arg_maxp);
+            // the prefill's virtual sequence reads its branch's page-table row
+            const int prow = PREFILL ? (iss ? seq : seq0) / a.prefill_n : (iss ? seq : seq0);
+            s.ptab = uni_ptr(arg_pt + (size_t)prow * arg_maxp);
             s.page_off = iss ? (plen + kPageSize - 1) / kPageSize : 0;
         } else {
             const size_t pbase = (size_t)kvh * (size_t)arg_plen * ROWB;
@@ -1042,10 +1044,10 @@ int prefill_max_rows(int head_dim, int group)
     return (head_dim == 128 && group <= 32) ? 32 : kMaxRows;
 }
 
-int prefill_waves_per_block(int head_dim, int row_tiles)
+int prefill_waves_per_block(int head_dim, int row_tiles, bool paged)
 {
     if (head_dim == 64) return 4 * waves_per_simd<64, 1, false, true>();
-    return waves_per_block_hd128<false, true>(row_tiles);
+    return paged ? waves_per_block_hd128<true, true>(row_tiles) : waves_per_block_hd128<false, true>(row_tiles);
 }
 
 hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s)
@@ -1058,18 +1060,22 @@ hipError_t launch_partials(const AttnArgs &a, int n_blocks, int head_dim, int ro
     return hipErrorInvalidValue;
 }
 
-int prefill_blocks_per_cu(int head_dim, int row_tiles)
+int prefill_blocks_per_cu(int head_dim, int row_tiles, bool paged)
 {
-    if (head_dim == 128) return blocks_per_cu_hd<128, false, true>(row_tiles);
-    if (head_dim == 64) return blocks_per_cu_hd<64, false, true>(row_tiles);
+    if (head_dim == 128)
+        return paged ? blocks_per_cu_hd<128, true, true>(row_tiles) : blocks_per_cu_hd<128, false, true>(row_tiles);
+    if (head_dim == 64)
+        return paged ? blocks_per_cu_hd<64, true, true>(row_tiles) : blocks_per_cu_hd<64, false, true>(row_tiles);
     return 0;
 }
 
 hipError_t launch_prefill(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s)
 {
     if (n_blocks <= 0) return hipSuccess;
-    if (head_dim == 128) return launch_hd<128, false, true>(a, n_blocks, row_tiles, s);
-    if (head_dim == 64) return launch_hd<64, false, true>(a, n_blocks, row_tiles, s);
+    if (head_dim == 128) return a.paged ? launch_hd<128, true, true>(a, n_blocks, row_tiles, s)
+                                        : launch_hd<128, false, true>(a, n_blocks, row_tiles, s);
+    if (head_dim == 64) return a.paged ? launch_hd<64, true, true>(a, n_blocks, row_tiles, s)
+                                       : launch_hd<64, false, true>(a, n_blocks, row_tiles, s);
     return hipErrorInvalidValue;
 }
 

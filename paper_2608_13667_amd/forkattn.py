@@ -47,6 +47,12 @@ class PrefillDesc(C.Structure):
                 ("suffix_cap", C.c_int32), ("max_suffix_len", C.c_int32), ("blocks", C.c_int32)]
 
 
+class PrefillPagedDesc(C.Structure):
+    _fields_ = [("n_branches", C.c_int32), ("n_tokens", C.c_int32), ("prefix_len", C.c_int32),
+                ("page_size", C.c_int32), ("max_pages_per_seq", C.c_int32), ("n_pool_pages", C.c_int32),
+                ("max_suffix_len", C.c_int32), ("blocks", C.c_int32)]
+
+
 class PlanInfo(C.Structure):
     _fields_ = [("n_items", C.c_int32), ("n_units", C.c_int32), ("waves_per_block", C.c_int32),
                 ("n_blocks", C.c_int32), ("rounds", C.c_int32), ("n_slots", C.c_int32), ("slot_rows", C.c_int32),
@@ -77,6 +83,8 @@ _sig = {
     "fka_plan_get_info": ([_vp, C.POINTER(PlanInfo)], C.c_int),
     "fka_plan_create_prefill": ([C.POINTER(Heads), C.POINTER(PrefillDesc), C.POINTER(_vp)], C.c_int),
     "fka_prefill": ([_vp] * 10, C.c_int),
+    "fka_plan_create_prefill_paged": ([C.POINTER(Heads), C.POINTER(PrefillPagedDesc), C.POINTER(_vp)], C.c_int),
+    "fka_prefill_paged": ([_vp] * 9, C.c_int),
     "fka_fork_decode_noalloc": ([C.POINTER(Heads), C.POINTER(ContigDesc)] + [_vp] * 10, C.c_int),
     "fka_plan_slots": ([_vp, _vp, _vp, C.c_int32, C.POINTER(C.c_int32)], C.c_int),
     "fka_partials": ([_vp] * 10, C.c_int),
@@ -196,6 +204,24 @@ class Plan:
         out = _vp()
         _check(_lib.fka_plan_create_prefill(C.byref(h), C.byref(d), C.byref(out)))
         return cls(out.value, False, h, n_branches * n_tokens)
+
+    @classmethod
+    def prefill_paged_plan(cls, n_q_heads, n_kv_heads, head_dim, n_branches, n_tokens, prefix_len, max_pages_per_seq,
+                           n_pool_pages, max_suffix_len, softmax_scale=0.0, blocks=0, page_size=16) -> "Plan":
+        """A paged instruction-prefill plan (fka_plan_create_prefill_paged): n_tokens per branch."""
+        h = Heads(n_q_heads, n_kv_heads, head_dim, softmax_scale)
+        d = PrefillPagedDesc(n_branches, n_tokens, prefix_len, page_size, max_pages_per_seq, n_pool_pages,
+                             max_suffix_len, blocks)
+        out = _vp()
+        _check(_lib.fka_plan_create_prefill_paged(C.byref(h), C.byref(d), C.byref(out)))
+        return cls(out.value, True, h, n_branches * n_tokens)
+
+    def prefill_paged(self, q, k_pool, v_pool, page_table, suffix_len, out, out_lse=None, stream=None):
+        """fka_prefill_paged: q bf16 [N][n][Hq][d], page_table int32 [N][max_pages] -> out fp32 [N][n][Hq][d]."""
+        d = self.device
+        _check(_lib.fka_prefill_paged(self._h, _p(q, "bf16", d), _p(k_pool, "bf16", d), _p(v_pool, "bf16", d),
+                                      _p(page_table, "i32", d), _p(suffix_len, "i32", d), _p(out, "f32", d),
+                                      _p(out_lse, "f32", d), _stream(stream)))
 
     def prefill(self, q, prefix_k, prefix_v, suffix_k, suffix_v, suffix_len, out, out_lse=None, stream=None):
         """fka_prefill: q bf16 [N][n][Hq][d] -> out fp32 [N][n][Hq][d], out_lse fp32 [N][n][Hq]."""

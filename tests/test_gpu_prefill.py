@@ -149,6 +149,103 @@ def _check_case(fa, c):
     assert plan.device_error() == 0
 
 
+def _to_pool(w, sk, sv, seed, spare=5):
+    """The prefix and each branch's suffix buffer (instruction tokens included) in a page pool of
+    16-token pages whose ids are a seeded permutation: the prefix pages are shared by every
+    branch's row, branch b's suffix position u sits at index ceil(Lp / 16) + u // 16."""
+    N, Hkv, cap, d = sk.shape
+    Lp = w.prefix_len
+    npre, nsuf = -(-Lp // 16), -(-cap // 16)
+    n_pages = npre + N * nsuf + spare
+    perm = np.random.default_rng(seed).permutation(n_pages)
+    kp = np.zeros((n_pages, Hkv, 16, d), np.uint16)
+    vp = np.zeros_like(kp)
+    table = np.full((N, npre + nsuf), -1, np.int32)
+
+    def put(pid, k_src, v_src, lo, hi):
+        kp[pid, :, :hi - lo] = k_src[:, lo:hi]
+        vp[pid, :, :hi - lo] = v_src[:, lo:hi]
+
+    for i in range(npre):
+        put(perm[i], w.prefix_k, w.prefix_v, 16 * i, min(16 * i + 16, Lp))
+        table[:, i] = perm[i]
+    for b in range(N):
+        for j in range(nsuf):
+            pid = perm[npre + b * nsuf + j]
+            put(pid, sk[b], sv[b], 16 * j, min(16 * j + 16, cap))
+            table[b, npre + j] = pid
+    return kp, vp, table
+
+
+def _run_paged(fa, w, n, q, sk, sv, seed, blocks=0):
+    s = w.spec
+    N, _, Hq, d = q.shape
+    kp, vp, table = _to_pool(w, sk, sv, seed)
+    plan = fa.Plan.prefill_paged_plan(s.n_q_heads, s.n_kv_heads, s.head_dim, N, n, w.prefix_len, table.shape[1],
+                                      kp.shape[0], w.suffix_cap, blocks=blocks)
+    out = torch.full((N, n, Hq, d), float("nan"), device="cuda")
+    lse = torch.full((N, n, Hq), float("nan"), device="cuda")
+    plan.prefill_paged(dev_bf16(q), dev_bf16(kp), dev_bf16(vp), dev_i32(table), dev_i32(w.suffix_len), out, lse)
+    torch.cuda.synchronize()
+    return plan, out.cpu().numpy().reshape(N * n, Hq, d), lse.cpu().numpy().reshape(N * n, Hq)
+
+
+@pytest.mark.parametrize("n", [1, 16, 64])
+def test_prefill_paged_long_shape(fa, n):
+    """The paged prefill at the 32k-prefix shape (40 query / 8 KV heads, d 128, 5 branches): the
+    pool's pages in a seeded random order, the prefix pages shared; every row of every token
+    against the oracle's causal definition, as for the contiguous layout."""
+    w = W.make("long", steps=n, suffix_range=(0, 40), seed=2700 + n)
+    q, sk, sv = _instruction(w, n)
+    plan, out, lse = _run_paged(fa, w, n, q, sk, sv, seed=2710 + n)
+    info = plan.info()
+    print(f"[prefill paged] long n={n}: {info.n_units} units, {info.n_blocks} blocks", flush=True)
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    m = gates.assert_gates(out, ref, what=f"paged prefill long n={n}")
+    gates.assert_lse(lse, ref_lse, what=f"paged prefill long n={n}")
+    assert plan.device_error() == 0
+    print(f"[prefill paged] long n={n} {m}", flush=True)
+
+
+@pytest.mark.parametrize("c", _random_cases(6, 2720),
+                         ids=lambda c: f"d{c['head_dim']}-kv{c['n_kv_heads']}-q{c['n_q_heads']}-b{c['n_branches']}"
+                                       f"-n{c['n']}-p{c['prefix_len']}-blk{c['blocks']}")
+def test_prefill_paged_random_shapes(fa, c):
+    """Seeded shapes as for the contiguous prefill, over a permuted page pool."""
+    spec = W.CONFIGS["mid"].replace(head_dim=c["head_dim"], n_kv_heads=c["n_kv_heads"], n_q_heads=c["n_q_heads"],
+                                    n_branches=c["n_branches"], prefix_len=c["prefix_len"],
+                                    suffix_range=(c["lo"], c["lo"] + 30), steps=c["n"], seed=c["seed"])
+    w = W.make(spec)
+    n = c["n"]
+    q, sk, sv = _instruction(w, n)
+    plan, out, lse = _run_paged(fa, w, n, q, sk, sv, seed=c["seed"] + 1, blocks=c["blocks"])
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    gates.assert_gates(out, ref, what="paged " + str(c))
+    gates.assert_lse(lse, ref_lse, what="paged " + str(c))
+    assert plan.device_error() == 0
+
+
+def test_prefill_paged_flags_a_bad_page(fa):
+    """A page id outside the pool in one branch's suffix row is not read (flag 4); the other
+    branches are exact."""
+    n = 4
+    w = W.make("tiny", steps=n, suffix_range=(10, 20), seed=2730)
+    q, sk, sv = _instruction(w, n)
+    s = w.spec
+    N, _, Hq, d = q.shape
+    kp, vp, table = _to_pool(w, sk, sv, seed=2731)
+    table[2, -(-w.prefix_len // 16)] = kp.shape[0] + 100
+    plan = fa.Plan.prefill_paged_plan(s.n_q_heads, s.n_kv_heads, s.head_dim, N, n, w.prefix_len, table.shape[1],
+                                      kp.shape[0], w.suffix_cap)
+    out = torch.full((N, n, Hq, d), float("nan"), device="cuda")
+    plan.prefill_paged(dev_bf16(q), dev_bf16(kp), dev_bf16(vp), dev_i32(table), dev_i32(w.suffix_len), out)
+    torch.cuda.synchronize()
+    assert plan.device_error() & 4
+    ref, _ = _reference(w, n, q, sk, sv)
+    rows = [t for t in range(N * n) if t // n != 2]
+    gates.assert_gates(out.cpu().numpy().reshape(N * n, Hq, d)[rows], ref[rows], what="other branches exact")
+
+
 def test_prefill_clamps_and_flags_a_suffix_past_the_bound(fa):
     """A suffix length above max_suffix_len - n is clamped to it (and flagged), like a decode's."""
     n = 5
@@ -175,3 +272,11 @@ def test_prefill_plan_rejects_other_calls(fa):
     o = torch.zeros(1 << 14, dtype=torch.float32, device="cuda")
     with pytest.raises(fa.FkaError, match="prefill"):
         plan.decode(t, t, t, t, t, ln, o)
+    tab = torch.zeros((3, 16), dtype=torch.int32, device="cuda")
+    with pytest.raises(fa.FkaError, match="paged"):
+        plan.prefill_paged(t, t, t, tab, ln, o)
+    pp = fa.Plan.prefill_paged_plan(8, 2, 64, 3, 4, 100, 16, 64, 32)
+    with pytest.raises(fa.FkaError, match="paged"):
+        pp.prefill(t, t, t, t, t, ln, o)
+    with pytest.raises(fa.FkaError, match="prefill"):
+        pp.decode_paged(t, t, t, tab, ln, o)
