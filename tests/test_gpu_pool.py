@@ -113,11 +113,11 @@ def test_fork_lifecycle_on_device(fa):
 
 def test_branch_instruction_prefill(fa):
     """Each branch appends a short instruction (n tokens, causal among themselves) over the shared
-    prefix (Sec. 3.3: the snapshot followed by a branch-specific instruction).  It runs as one paged
-    decode over N*n virtual sequences in one group -- token t of branch b is a sequence whose page
-    row is b's and whose suffix length is L_b + t + 1 -- so the prefix is read once for all N*n*G
-    query rows.  Checked against the oracle's causal definition: query (b, t) attends to the
-    prefix and to b's suffix positions [0, L_b + t]."""
+    prefix (Sec. 3.3: the snapshot followed by a branch-specific instruction), on the page pool
+    after a fork: once as one paged decode over N*n virtual sequences in one group -- token t of
+    branch b is a sequence whose page row is b's and whose suffix length is L_b + t + 1 -- and once
+    through fka_prefill_paged on the same pages.  Both are checked against the oracle's causal
+    definition: query (b, t) attends to the prefix and to b's suffix positions [0, L_b + t]."""
     Hq, Hkv, d, N, n = 16, 4, 128, 5, 3  # 5 * 3 virtual sequences x 4 q heads = 60 rows per KV head
     Lp, n_pages, max_pages = 1000, 120, 70
     scale = 1.0 / math.sqrt(d)
@@ -160,6 +160,15 @@ def test_branch_instruction_prefill(fa):
     info = plan.info()
     # one item per KV head holding all N * n * G rows: the prefix is read once per chunk
     assert info.n_units == 1 and info.n_items == Hkv and info.slot_rows == N * n * (Hq // Hkv)
+    # the same instruction through the prefill kernel on the same pool and page rows
+    pplan = fa.Plan.prefill_paged_plan(Hq, Hkv, d, N, n, Lp, max_pages, n_pages, cap)
+    out2 = torch.empty((N, n, Hq, d), device="cuda")
+    lse2 = torch.empty((N, n, Hq), device="cuda")
+    pplan.prefill_paged(dev_bf16(q.reshape(N, n, Hq, d)), k_pool, v_pool, dev_i32(table), dev_i32(Lb), out2, lse2)
+    torch.cuda.synchronize()
+    gates.assert_gates(out2.cpu().numpy().reshape(N * n, Hq, d), ref, what="paged prefill kernel")
+    gates.assert_lse(lse2.cpu().numpy().reshape(N * n, Hq), ref_lse, what="paged prefill kernel")
+    assert pplan.device_error() == 0
 
 
 def test_ranged_gather_bit_exact(fa):
