@@ -342,7 +342,7 @@ def lifecycle_timing(fa, torch, w):
     sequence (host bookkeeping), the promote's device work (a gather of the main context's tail,
     from the first page the dense layout rewrites, and its scatter into the dense pages), and the
     branches' instruction prefill on the pool after a fork (fka_prefill_paged, 16 tokens per
-    branch).  Host calls are timed with perf_counter over many cycles, the device work with HIP
+    branch) and the harvest's prefill of 256 tokens into the promoted main context.  Host calls are timed with perf_counter over many cycles, the device work with HIP
     events on the launch stream."""
     spec = w.spec
     N, Hkv, d = w.n_branches, spec.n_kv_heads, spec.head_dim
@@ -436,13 +436,36 @@ def lifecycle_timing(fa, torch, w):
     pf_s = e0.elapsed_time(e1) / 1e3 / reps
     # the prefix once, each branch's instruction
     pf_bytes = per_tok * (Lp + N * n)
+    # thought harvesting: the promoted main context takes h harvested tokens (one sequence)
+    h = 256
+    mp2 = -(-L0 // 16) + -(-h // 16)
+    snap3 = pool.alloc(-(-L0 // 16))
+    t3 = np.full((1, mp2), -1, np.int32)
+    pool.fork(snap3, t3, 0, 1)
+    pool.reserve(t3, 0, L0, h)
+    hplan = fa.Plan.prefill_paged_plan(Hq, Hkv, d, 1, h, L0, mp2, n_pages, h)
+    t3d = torch.from_numpy(t3).cuda()
+    len1 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    qh = torch.zeros((1, h, Hq, d), dtype=torch.bfloat16, device="cuda")
+    oh = torch.empty((1, h, Hq, d), device="cuda")
+    for _ in range(5):
+        hplan.prefill_paged(qh, pages, v_pages, t3d, len1, oh, None, stream)
+    e0.record(stream)
+    for _ in range(reps):
+        hplan.prefill_paged(qh, pages, v_pages, t3d, len1, oh, None, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    hv_s = e0.elapsed_time(e1) / 1e3 / reps
+    hplan.close()
     pplan.close()
     pool.close()
     ms = lambda v: float(np.median(v) * 1e6)
     return {"tokens_promoted": L0, "host_us": {k: ms(v) for k, v in host.items()},
             "promote_device_us": dev_s * 1e6, "promote_device_gbps": moved / dev_s / 1e9,
             "prefill_paged": {"tokens_per_branch": n, "us": pf_s * 1e6, "us_per_token": pf_s * 1e6 / (N * n),
-                              "kv_gbps": pf_bytes / pf_s / 1e9, "cache": "MALL-warm (one pool)"}}
+                              "kv_gbps": pf_bytes / pf_s / 1e9, "cache": "MALL-warm (one pool)"},
+            "harvest_prefill_paged": {"tokens": h, "context": L0, "us": hv_s * 1e6, "us_per_token": hv_s * 1e6 / h,
+                                      "cache": "MALL-warm (one pool)"}}
 
 
 def prefill_timing(torch, fa, W, ns, trials):

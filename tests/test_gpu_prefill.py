@@ -108,6 +108,24 @@ def test_prefill_random_shapes(fa, c):
     _check_case(fa, c)
 
 
+def test_prefill_harvest_into_the_main_context(fa):
+    """Thought harvesting appends the harvested text to the main context (paper Sec. 3.5): one
+    sequence (n_branches 1) prefilling n tokens over its snapshot and its own suffix, contiguous
+    and paged; every row checked."""
+    n = 96
+    spec = W.CONFIGS["long"].replace(prefix_len=3000, n_branches=1, suffix_range=(300, 300), steps=n, seed=2740)
+    w = W.make(spec)
+    q, sk, sv = _instruction(w, n)
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    plan, out, lse = _run(fa, w, n, q, sk, sv)
+    gates.assert_gates(out, ref, what="harvest contiguous")
+    gates.assert_lse(lse, ref_lse, what="harvest contiguous")
+    pplan, pout, plse = _run_paged(fa, w, n, q, sk, sv, seed=2741)
+    gates.assert_gates(pout, ref, what="harvest paged")
+    gates.assert_lse(plse, ref_lse, what="harvest paged")
+    assert plan.device_error() == 0 and pplan.device_error() == 0
+
+
 @pytest.mark.parametrize("g", [32, 40, 64])
 def test_prefill_wide_groups(fa, g):
     """d 128 with G = 32 (units of one token, 32 rows, two waves per SIMD) and G = 40 and 64, where
