@@ -135,6 +135,62 @@ def test_prefill_wide_groups(fa, g):
                          blocks=0, seed=2603 + g))
 
 
+@pytest.mark.parametrize("case", [dict(hkv=8, g=5, nb=3, n=66, units=33, sets=17),
+                                  dict(hkv=4, g=5, nb=6, n=70, units=70, sets=35)],
+                         ids=["kv8-33units", "kv4-70units"])
+def test_prefill_paired_units(fa, case):
+    """More items than resident blocks (units of 6 tokens x the KV heads): the plan pairs two
+    units of a KV head per eight-wave block, with 8 KV heads (one per XCD) and 4; every row of every
+    token checked, contiguous and paged."""
+    n = case["n"]
+    spec = W.CONFIGS["long"].replace(prefix_len=700, n_branches=case["nb"], n_kv_heads=case["hkv"],
+                                     n_q_heads=case["hkv"] * case["g"], suffix_range=(0, 9), steps=n,
+                                     seed=2660 + case["hkv"])
+    w = W.make(spec)
+    q, sk, sv = _instruction(w, n)
+    plan, out, lse = _run(fa, w, n, q, sk, sv)
+    info = plan.info()
+    print(f"[prefill] paired: {info.n_units} units, {info.n_items} items, {info.n_blocks} blocks", flush=True)
+    assert info.n_units == case["units"] and info.units_per_block == 2
+    assert info.n_blocks == case["sets"] * case["hkv"]
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    gates.assert_gates(out, ref, what="paired units")
+    gates.assert_lse(lse, ref_lse, what="paired units")
+    assert plan.device_error() == 0
+    pplan, pout, plse = _run_paged(fa, w, n, q, sk, sv, seed=2670 + case["hkv"])
+    assert pplan.info().units_per_block == 2
+    gates.assert_gates(pout, ref, what="paired units, paged")
+    gates.assert_lse(plse, ref_lse, what="paired units, paged")
+    assert pplan.device_error() == 0
+
+
+def test_prefill_harvest_into_the_main_context(fa):
+    """Thought harvesting appends the harvested text to the main context (paper Sec. 3.5): one
+    sequence (n_branches 1) prefilling n tokens over its snapshot and its own suffix, contiguous
+    and paged; every row checked."""
+    n = 96
+    spec = W.CONFIGS["long"].replace(prefix_len=3000, n_branches=1, suffix_range=(300, 300), steps=n, seed=2740)
+    w = W.make(spec)
+    q, sk, sv = _instruction(w, n)
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    plan, out, lse = _run(fa, w, n, q, sk, sv)
+    gates.assert_gates(out, ref, what="harvest contiguous")
+    gates.assert_lse(lse, ref_lse, what="harvest contiguous")
+    pplan, pout, plse = _run_paged(fa, w, n, q, sk, sv, seed=2741)
+    gates.assert_gates(pout, ref, what="harvest paged")
+    gates.assert_lse(plse, ref_lse, what="harvest paged")
+    assert plan.device_error() == 0 and pplan.device_error() == 0
+
+
+@pytest.mark.parametrize("g", [32, 40, 64])
+def test_prefill_wide_groups(fa, g):
+    """d 128 with G = 32 (units of one token, 32 rows, two waves per SIMD) and G = 40 and 64, where
+    a 32-row unit holds no token and the units take up to 64 rows (three or four tiles, one wave
+    per SIMD)."""
+    _check_case(fa, dict(head_dim=128, n_kv_heads=2, n_q_heads=2 * g, n_branches=3, n=3, prefix_len=1000, lo=7,
+                         blocks=0, seed=2603 + g))
+
+
 def test_prefill_paired_units(fa):
     """More items than resident blocks (33 units of 6 tokens x 8 KV heads at the 32k shape's
     heads): the plan pairs two units of a KV head per eight-wave block, the last block set holding
