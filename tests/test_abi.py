@@ -104,6 +104,27 @@ def test_paged_plan_rejects(fa):
     assert "empty" in fa.last_error()
 
 
+def test_prefill_plans_reject(fa):
+    """Instruction-prefill plans, contiguous and paged: host validation before any HIP call."""
+    h = _heads(fa)
+    out = C.c_void_p()
+    create = lambda d: fa.raw_call("fka_plan_create_prefill", C.byref(h), C.byref(d), C.byref(out))
+    create_p = lambda d: fa.raw_call("fka_plan_create_prefill_paged", C.byref(h), C.byref(d), C.byref(out))
+    assert create(fa.PrefillDesc(5, 0, 100, 64, 64, 0)) == -1 and "n_tokens" in fa.last_error()
+    assert create(fa.PrefillDesc(5, 8, 100, 64, 4, 0)) == -1 and "max_suffix_len" in fa.last_error()
+    assert create(fa.PrefillDesc(5, 8, 100, 64, 64, -1)) == -1 and "blocks" in fa.last_error()
+    assert create(fa.PrefillDesc(64, 9, 100, 64, 64, 0)) == -2  # 576 tokens: more than 512
+    #                               N  n  Lp   page max_pages pool msl blocks
+    assert create_p(fa.PrefillPagedDesc(5, 8, 100, 8, 64, 100, 32, 0)) == -1 and "page_size" in fa.last_error()
+    assert create_p(fa.PrefillPagedDesc(5, 8, 100, 16, 8, 100, 32, 0)) == -1 and "pages" in fa.last_error()
+    assert create_p(fa.PrefillPagedDesc(5, 8, 100, 16, 64, 0, 32, 0)) == -1 and "n_pool_pages" in fa.last_error()
+    assert create_p(fa.PrefillPagedDesc(5, 8, 100, 16, 64, 100, 4, 0)) == -1 and "max_suffix_len" in fa.last_error()
+    assert not out.value
+    n = None
+    assert fa.raw_call("fka_prefill", n, n, n, n, n, n, n, n, n, n) == -1
+    assert fa.raw_call("fka_prefill_paged", n, n, n, n, n, n, n, n, n) == -1
+
+
 def test_calls_with_null_plan_are_rejected(fa):
     n = None
     assert fa.raw_call("fka_fork_decode", n, n, n, n, n, n, n, n, n, n) == -1
