@@ -164,51 +164,6 @@ def test_prefill_paired_units(fa, case):
     assert pplan.device_error() == 0
 
 
-def test_prefill_harvest_into_the_main_context(fa):
-    """Thought harvesting appends the harvested text to the main context (paper Sec. 3.5): one
-    sequence (n_branches 1) prefilling n tokens over its snapshot and its own suffix, contiguous
-    and paged; every row checked."""
-    n = 96
-    spec = W.CONFIGS["long"].replace(prefix_len=3000, n_branches=1, suffix_range=(300, 300), steps=n, seed=2740)
-    w = W.make(spec)
-    q, sk, sv = _instruction(w, n)
-    ref, ref_lse = _reference(w, n, q, sk, sv)
-    plan, out, lse = _run(fa, w, n, q, sk, sv)
-    gates.assert_gates(out, ref, what="harvest contiguous")
-    gates.assert_lse(lse, ref_lse, what="harvest contiguous")
-    pplan, pout, plse = _run_paged(fa, w, n, q, sk, sv, seed=2741)
-    gates.assert_gates(pout, ref, what="harvest paged")
-    gates.assert_lse(plse, ref_lse, what="harvest paged")
-    assert plan.device_error() == 0 and pplan.device_error() == 0
-
-
-@pytest.mark.parametrize("g", [32, 40, 64])
-def test_prefill_wide_groups(fa, g):
-    """d 128 with G = 32 (units of one token, 32 rows, two waves per SIMD) and G = 40 and 64, where
-    a 32-row unit holds no token and the units take up to 64 rows (three or four tiles, one wave
-    per SIMD)."""
-    _check_case(fa, dict(head_dim=128, n_kv_heads=2, n_q_heads=2 * g, n_branches=3, n=3, prefix_len=1000, lo=7,
-                         blocks=0, seed=2603 + g))
-
-
-def test_prefill_paired_units(fa):
-    """More items than resident blocks (33 units of 6 tokens x 8 KV heads at the 32k shape's
-    heads): the plan pairs two units of a KV head per eight-wave block, the last block set holding
-    a single unit; every row of every token checked."""
-    n = 66
-    spec = W.CONFIGS["long"].replace(prefix_len=700, n_branches=3, suffix_range=(0, 9), steps=n, seed=2660)
-    w = W.make(spec)
-    q, sk, sv = _instruction(w, n)
-    plan, out, lse = _run(fa, w, n, q, sk, sv)
-    info = plan.info()
-    print(f"[prefill] paired: {info.n_units} units, {info.n_items} items, {info.n_blocks} blocks", flush=True)
-    assert info.n_units == 33 and info.units_per_block == 2 and info.n_blocks == 17 * 8
-    ref, ref_lse = _reference(w, n, q, sk, sv)
-    gates.assert_gates(out, ref, what="paired units")
-    gates.assert_lse(lse, ref_lse, what="paired units")
-    assert plan.device_error() == 0
-
-
 def _check_case(fa, c):
     spec = W.CONFIGS["mid"].replace(head_dim=c["head_dim"], n_kv_heads=c["n_kv_heads"], n_q_heads=c["n_q_heads"],
                                     n_branches=c["n_branches"], prefix_len=c["prefix_len"],
