@@ -322,12 +322,16 @@ fka_status fka_scatter_pages(const void *k_src, const void *v_src, int32_t len, 
  * is dominated by prefill over the cached prefix).  Every branch b takes n_tokens instruction
  * tokens at once: token t's queries attend to the whole shared prefix and, causally, to b's
  * suffix up to and including its own position (suffix positions [0, suffix_len[b] + t]).
- * The plan splits the N x n_tokens tokens into units of consecutive tokens, at most 32 query
- * rows (tokens x G) per KV head each for head_dim 128 with G <= 32, else 64; all units stream
- * the same prefix, and the blocks that read one prefix range for different units run together
- * on one XCD (block vb holds work item vb mod n_items), so each prefix tile is fetched from HBM
- * once and served to the other units from that XCD's L2.  Then the merge stage combines each
- * row's partials. */
+ * With head_dim 128 and at least 256 query rows (N x n_tokens x G) per KV head, a tiled kernel
+ * runs: each KV head's rows are cut into units of 32 consecutive rows, a block of eight waves
+ * takes eight units (one each) over one range of 64-key prefix tiles, which it loads once into
+ * LDS for all eight, and the blocks of one KV head run on one XCD (the KV head varies fastest in
+ * the grid) so that its ranges come from HBM once; the block of the last range also reads the
+ * suffix keys.  Otherwise the plan splits the tokens into units of consecutive tokens (at most
+ * 32 query rows per KV head each for head_dim 128 with G <= 32, else 64), all streaming the same
+ * prefix on the partial kernel, the blocks that read one prefix range for different units
+ * together on one XCD (block vb holds work item vb mod n_items).  Then the merge stage combines
+ * each row's partials. */
 typedef struct {
     int32_t n_branches;      /* N, >= 1 */
     int32_t n_tokens;        /* n instruction tokens per branch, >= 1; N x n <= 512 */
@@ -421,7 +425,8 @@ typedef struct {
     int32_t n_slots;           /* partial-result slots in the workspace */
     int32_t slot_rows;         /* rows per slot: the largest item's query rows */
     int32_t static_split;      /* 1: one unit, items split statically */
-    int32_t units_per_block;   /* instruction prefill: units a block takes, 1 or 2 (decode plans: 1) */
+    int32_t units_per_block;   /* instruction prefill: units a block takes: 8 on the tiled kernel, else
+                                  1 or 2 (decode plans: 1) */
     size_t workspace_bytes;    /* device bytes held by the plan */
 } fka_plan_info;
 

@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libforkattn.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "kernels.hip", "partials.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("api.hip", "kernels.hip", "partials.hip", "prefill.hip")]
 ARCH = "gfx950"
 
 

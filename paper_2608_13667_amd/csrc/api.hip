@@ -23,6 +23,10 @@ struct fka_plan {
     int32_t prefill_n = 0;     // instruction prefill plan: tokens per branch (sequences are b * n + t)
     int32_t n_branches = 0;    // instruction prefill plan: branches
     int32_t prefill_groups = 1; // instruction prefill plan: units per block
+    // instruction prefill on the tiled kernel (head_dim 128): 32-row units per KV head, blocks of
+    // eight units, prefix ranges, prefix tiles of 64 keys, tiles of balance left to the suffix keys
+    bool prefill_tiles = false;
+    int32_t tile_units = 0, tile_unit_groups = 0, tile_ranges = 0, tile_prefix = 0, tile_reserve = 0;
     int32_t max_suffix_len = 0;
     // contiguous
     int32_t prefix_len = 0, suffix_cap = 0;
@@ -373,6 +377,66 @@ fka_status run_decode(const fka_plan *p, const fka::AttnArgs &a, const int32_t *
     return ok();
 }
 
+// The instruction prefill's two launches: the tiled kernel (head_dim 128) with the merge in its
+// explicit mode (every row merges its ranges' partials), or the partial kernel's prefill
+// instantiation with the plan-mode merge.
+fka_status run_prefill(const fka_plan *p, const fka::AttnArgs &a, float *out, float *out_lse, hipStream_t s)
+{
+    hipError_t e;
+    if (p->prefill_tiles) {
+        fka::PrefillArgs t{};
+        t.q = a.q;
+        t.prefix_k = a.prefix_k;
+        t.prefix_v = a.prefix_v;
+        t.suffix_k = a.suffix_k;
+        t.suffix_v = a.suffix_v;
+        t.k_pool = a.k_pool;
+        t.v_pool = a.v_pool;
+        t.page_table = a.page_table;
+        t.suffix_len = a.suffix_len;
+        t.part_o = p->part_o;
+        t.part_lse = p->part_lse;
+        t.err = p->err;
+        t.n_branches = p->n_branches;
+        t.n_tokens = p->prefill_n;
+        t.prefix_len = p->prefix_len;
+        t.suffix_cap = p->suffix_cap;
+        t.max_suffix_len = p->max_suffix_len;
+        t.max_pages = p->max_pages;
+        t.n_pool_pages = p->n_pool_pages;
+        t.paged = p->paged ? 1 : 0;
+        t.n_q_heads = p->Hq;
+        t.n_kv_heads = p->Hkv;
+        t.group = p->G;
+        t.n_units = p->tile_units;
+        t.unit_groups = p->tile_unit_groups;
+        t.ranges = p->tile_ranges;
+        t.prefix_tiles = p->tile_prefix;
+        t.tail_reserve = p->tile_reserve;
+        t.scale_log2 = p->scale * 1.4426950408889634f;
+        e = fka::launch_prefill_tiles(t, p->n_blocks, s);
+        if (e != hipSuccess) return hip_fail(e, "prefill kernel launch");
+        fka::MergeArgs m{};
+        m.part_o = p->part_o;
+        m.part_lse = p->part_lse;
+        m.out = out;
+        m.out_lse = out_lse;
+        m.rows = p->n_seqs * p->Hq;
+        m.n_q_heads = p->Hq;
+        m.n_parts = p->tile_ranges;
+        m.plan = 0;
+        m.err = p->err;
+        e = fka::launch_merge(m, p->d, s);
+        if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+        return ok();
+    }
+    e = fka::launch_prefill(a, p->n_blocks, p->d, p->row_tiles, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill kernel launch");
+    e = fka::launch_merge(merge_args(p, a.suffix_len, out, out_lse), p->d, s);
+    if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+    return ok();
+}
+
 // ---------------------------------------------------------------------------------------
 // Scratch of the no-allocation decode (fka_fork_decode_noalloc): the device memory one decode
 // needs beyond its inputs and outputs -- the partial results, the clamped lengths and an error
@@ -448,6 +512,56 @@ fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t 
     int cus = 0;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
         return bail(hip_fail(e, "hipDeviceGetAttribute"));
+    // The tiled kernel when each KV head has at least eight 32-row units (one block's worth);
+    // fewer rows than that leave most of a block's waves idle there, and the partial kernel's
+    // prefill instantiation, which spreads each unit's keys over four waves, is faster.
+    if (p->d == 128 && S * G >= 8 * 32) {
+        // The tiled kernel: units of 32 consecutive rows of a KV head, eight per block (one per
+        // wave) over one range of prefix tiles; R ranges fill the device, and the last range's
+        // share is shortened by the suffix keys it also reads, taken as the instruction itself
+        // (the branches' suffixes are empty at the fork): a 32-key suffix tile, read without
+        // prefetch, is counted as one 64-key prefix tile.
+        const int per_cu = fka::prefill_tiles_blocks_per_cu(lay.paged);
+        if (per_cu <= 0) return bail(fail(FKA_ERR_HIP, "occupancy query of the prefill kernel failed"));
+        const int64_t rows_head = S * G;
+        const int32_t U = (int32_t)ceil_div(rows_head, 32);
+        const int32_t UG = ceil_div(U, 8);
+        const int32_t PT = ceil_div(Lp, 64);
+        const int64_t base = (int64_t)p->Hkv * UG;
+        const int64_t want = blocks > 0 ? blocks : (int64_t)cus * per_cu;
+        int64_t R = std::max<int64_t>(1, want / base);
+        R = std::min<int64_t>(R, std::max(1, PT));
+        // the partials of one range: S Hq rows of d floats; the ranges together stay below 256 MiB
+        const int64_t range_bytes = S * p->Hq * (int64_t)p->d * 4;
+        R = std::max<int64_t>(1, std::min<int64_t>(R, ((int64_t)256 << 20) / range_bytes));
+        p->prefill_tiles = true;
+        p->tile_units = U;
+        p->tile_unit_groups = UG;
+        p->tile_ranges = (int32_t)R;
+        p->tile_prefix = PT;
+        p->tile_reserve = (int32_t)std::min<int64_t>(ceil_div(n, 32), PT / (2 * R));
+        for (int32_t u = 0; u < U; ++u) {
+            fka::UnitRec r{};
+            r.seq0 = (int32_t)(((int64_t)u * 32) / G);
+            r.nseq = (int32_t)((std::min<int64_t>(rows_head, (int64_t)u * 32 + 32) - 1) / G) - r.seq0 + 1;
+            r.plen = Lp;
+            p->units.push_back(r);
+        }
+        p->seq_prefix_len.assign(p->n_seqs, Lp);
+        p->static_split = false;
+        p->n_items = U * p->Hkv;
+        p->slot_rows = (int32_t)(S * p->Hq);
+        p->row_tiles = 2;
+        p->waves = 8;
+        p->prefill_groups = 8;
+        p->n_blocks = (int32_t)(base * R);
+        p->rounds = 1;
+        p->n_slots = (int32_t)R;
+        fka_status st = finish_plan(p);
+        if (st != FKA_OK) return bail(st);
+        *out = p;
+        return ok();
+    }
     // Units of consecutive instruction tokens, at most prefill_max_rows query rows each (32 for
     // d = 128: two waves per SIMD), all over the one prefix: as few as that allows.  Each unit's
     // waves load every prefix tile once more (from L2) and score it against the unit's 16-row
@@ -829,12 +943,7 @@ fka_status fka_prefill(const fka_plan *p, const void *q, const void *prefix_k, c
     a.suffix_v = static_cast<const uint16_t *>(suffix_v);
     a.suffix_len = suffix_len;
     a.prefill_n = p->prefill_n;
-    const hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = fka::launch_prefill(a, p->n_blocks, p->d, p->row_tiles, s);
-    if (e != hipSuccess) return hip_fail(e, "prefill kernel launch");
-    e = fka::launch_merge(merge_args(p, suffix_len, out, out_lse), p->d, s);
-    if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
-    return ok();
+    return run_prefill(p, a, out, out_lse, static_cast<hipStream_t>(stream));
 }
 
 fka_status fka_prefill_paged(const fka_plan *p, const void *q, const void *k_pool, const void *v_pool,
@@ -857,12 +966,7 @@ fka_status fka_prefill_paged(const fka_plan *p, const void *q, const void *k_poo
     a.page_table = page_table;
     a.suffix_len = suffix_len;
     a.prefill_n = p->prefill_n;
-    const hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = fka::launch_prefill(a, p->n_blocks, p->d, p->row_tiles, s);
-    if (e != hipSuccess) return hip_fail(e, "prefill kernel launch");
-    e = fka::launch_merge(merge_args(p, suffix_len, out, out_lse), p->d, s);
-    if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
-    return ok();
+    return run_prefill(p, a, out, out_lse, static_cast<hipStream_t>(stream));
 }
 
 fka_status fka_partials(const fka_plan *p, const void *q, const void *prefix_k, const void *prefix_v,

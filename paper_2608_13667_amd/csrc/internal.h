@@ -232,6 +232,37 @@ struct ScatterArgs {
     int32_t *err;                   // nullable
 };
 
+// Instruction prefill as a tiled multi-query kernel (prefill.hip, head_dim 128).  Rows of KV head g
+// are cut into units of 32 (row i: query head g G + i mod G of virtual sequence i / G, where
+// sequence s = b n + t is instruction token t of branch b); block vb takes KV head vb mod Hkv,
+// unit group (vb / Hkv) mod unit_groups (eight units, one per wave) and prefix range
+// vb / (Hkv unit_groups) of `ranges`, range r covering prefix tiles (64 keys) [floor(r T / R),
+// floor((r + 1) T / R)) of T = prefix_tiles + tail_reserve, clamped to the prefix; the last range
+// also reads the suffix keys.  Part r of output row (s, h) is written at
+// part_o[(r S Hq + s Hq + h) d] and part_lse[r S Hq + s Hq + h].
+struct PrefillArgs {
+    const uint16_t *q;                    // [S][Hq][d]
+    const uint16_t *prefix_k, *prefix_v;  // contiguous: [Hkv][Lp][d]
+    const uint16_t *suffix_k, *suffix_v;  // contiguous: [N][Hkv][cap][d]
+    const uint16_t *k_pool, *v_pool;      // paged: [pages][Hkv][16][d]
+    const int32_t *page_table;            // paged: [N][max_pages]
+    const int32_t *suffix_len;            // [N], each branch's suffix before the instruction
+    float *part_o;                        // [ranges][S Hq][d]
+    float *part_lse;                      // [ranges][S Hq]
+    int32_t *err;
+    int32_t n_branches, n_tokens;  // N, n
+    int32_t prefix_len, suffix_cap, max_suffix_len;
+    int32_t max_pages, n_pool_pages;
+    int32_t paged;
+    int32_t n_q_heads, n_kv_heads, group;
+    int32_t n_units;       // 32-row units per KV head
+    int32_t unit_groups;   // ceil(n_units / 8)
+    int32_t ranges;        // R
+    int32_t prefix_tiles;  // ceil(Lp / 64)
+    int32_t tail_reserve;  // tiles of the balance given to the last range's suffix keys
+    float scale_log2;      // softmax scale * log2(e)
+};
+
 // error-flag bits (device)
 constexpr int32_t kErrSuffixClamped = 1;
 constexpr int32_t kErrAppendNoRoom = 2;
@@ -253,6 +284,9 @@ int prefill_max_rows(int head_dim, int group);
 hipError_t launch_prefill(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);
 int prefill_blocks_per_cu(int head_dim, int row_tiles, bool paged);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
+// The tiled instruction prefill (head_dim 128): resident blocks per compute unit, and the launch.
+int prefill_tiles_blocks_per_cu(bool paged);
+hipError_t launch_prefill_tiles(const PrefillArgs &a, int n_blocks, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs &a, hipStream_t s);

@@ -29,7 +29,7 @@ FLAGS=(--offload-arch=gfx950 -O1 -g -std=c++17 -fPIC -ffp-contract=off -Xclang -
        -packed-fp32-ops -I "$T/include" -Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined
        -Xarch_host -fno-sanitize-recover=all -Xarch_host -fno-omit-frame-pointer)
 mkdir -p "$T/obj"
-for f in api kernels partials; do
+for f in api kernels partials prefill; do
     "$HIPCC" "${FLAGS[@]}" -c "$T/paper_2608_13667_amd/csrc/$f.hip" -o "$T/obj/$f.o" 2> "$T/obj/$f.log" &
 done
 wait

@@ -74,12 +74,30 @@ def test_prefill_long_shape(fa, n):
     m = gates.assert_gates(out, ref, what=f"prefill long n={n}")
     gates.assert_lse(lse, ref_lse, what=f"prefill long n={n}")
     assert plan.device_error() == 0
-    # the block sets (units_per_block units of one KV head) are a multiple of the 8 XCDs apart, so
-    # that the units of a KV head share its prefix tiles; one round of resident blocks
-    P, cus = info.units_per_block, torch.cuda.get_device_properties(0).multi_processor_count
-    sets = -(-info.n_units // P) * 8
-    assert info.n_blocks % sets == 0 and info.n_blocks <= cus and (P == 1 or info.n_items > cus)
+    rows_per_head = w.q.shape[0] * n * 5
+    if rows_per_head >= 8 * 32:
+        _check_tiled_plan(info, n_kv_heads=8, rows_per_head=rows_per_head)
+    else:
+        # the partial kernel's prefill instantiation: the block sets (units_per_block units of one
+        # KV head) are a multiple of the 8 XCDs apart, so that the units of a KV head share its
+        # prefix tiles; one round of resident blocks
+        P, cus = info.units_per_block, torch.cuda.get_device_properties(0).multi_processor_count
+        sets = -(-info.n_units // P) * 8
+        assert info.n_blocks % sets == 0 and info.n_blocks <= cus and (P == 1 or info.n_items > cus)
     print(f"[prefill] long n={n} {m}", flush=True)
+
+
+def _check_tiled_plan(info, n_kv_heads, rows_per_head):
+    """Head dim 128 with at least 256 rows per KV head runs the tiled kernel: 32-row units, eight
+    per block (one per wave), blocks =
+    KV heads x unit groups x prefix ranges in one round of resident blocks, one partial slot per
+    range (the KV head varies fastest in the grid, so with 8 KV heads a head's blocks share an XCD)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert info.units_per_block == 8 and info.waves_per_block == 8
+    assert info.n_units == -(-rows_per_head // 32) and info.n_items == info.n_units * n_kv_heads
+    groups = n_kv_heads * -(-info.n_units // 8)
+    assert info.n_blocks % groups == 0 and info.n_slots == info.n_blocks // groups
+    assert info.n_blocks <= max(cus, groups) and info.rounds == 1
 
 
 def _random_cases(k, seed):
@@ -128,20 +146,18 @@ def test_prefill_harvest_into_the_main_context(fa):
 
 @pytest.mark.parametrize("g", [32, 40, 64])
 def test_prefill_wide_groups(fa, g):
-    """d 128 with G = 32 (units of one token, 32 rows, two waves per SIMD) and G = 40 and 64, where
-    a 32-row unit holds no token and the units take up to 64 rows (three or four tiles, one wave
-    per SIMD)."""
+    """d 128 with G = 32 (a 32-row unit is one token) and G = 40 and 64, where a token's rows spread
+    over two units (the units do not follow token boundaries)."""
     _check_case(fa, dict(head_dim=128, n_kv_heads=2, n_q_heads=2 * g, n_branches=3, n=3, prefix_len=1000, lo=7,
                          blocks=0, seed=2603 + g))
 
 
-@pytest.mark.parametrize("case", [dict(hkv=8, g=5, nb=3, n=66, units=33, sets=17),
-                                  dict(hkv=4, g=5, nb=6, n=70, units=70, sets=35)],
-                         ids=["kv8-33units", "kv4-70units"])
-def test_prefill_paired_units(fa, case):
-    """More items than resident blocks (units of 6 tokens x the KV heads): the plan pairs two
-    units of a KV head per eight-wave block, with 8 KV heads (one per XCD) and 4; every row of every
-    token checked, contiguous and paged."""
+@pytest.mark.parametrize("case", [dict(hkv=8, g=5, nb=3, n=66), dict(hkv=4, g=5, nb=6, n=70)],
+                         ids=["kv8-31units", "kv4-66units"])
+def test_prefill_many_units(fa, case):
+    """Many 32-row units per KV head, with 8 KV heads (one per XCD) and 4, units straddling
+    branches, a last unit group of fewer than eight units and a prefix (700 keys) that is not a
+    multiple of the 64-key tile; every row of every token checked, contiguous and paged."""
     n = case["n"]
     spec = W.CONFIGS["long"].replace(prefix_len=700, n_branches=case["nb"], n_kv_heads=case["hkv"],
                                      n_q_heads=case["hkv"] * case["g"], suffix_range=(0, 9), steps=n,
@@ -150,17 +166,16 @@ def test_prefill_paired_units(fa, case):
     q, sk, sv = _instruction(w, n)
     plan, out, lse = _run(fa, w, n, q, sk, sv)
     info = plan.info()
-    print(f"[prefill] paired: {info.n_units} units, {info.n_items} items, {info.n_blocks} blocks", flush=True)
-    assert info.n_units == case["units"] and info.units_per_block == 2
-    assert info.n_blocks == case["sets"] * case["hkv"]
+    print(f"[prefill] many units: {info.n_units} units, {info.n_items} items, {info.n_blocks} blocks", flush=True)
+    _check_tiled_plan(info, n_kv_heads=case["hkv"], rows_per_head=case["nb"] * n * case["g"])
     ref, ref_lse = _reference(w, n, q, sk, sv)
-    gates.assert_gates(out, ref, what="paired units")
-    gates.assert_lse(lse, ref_lse, what="paired units")
+    gates.assert_gates(out, ref, what="many units")
+    gates.assert_lse(lse, ref_lse, what="many units")
     assert plan.device_error() == 0
     pplan, pout, plse = _run_paged(fa, w, n, q, sk, sv, seed=2670 + case["hkv"])
-    assert pplan.info().units_per_block == 2
-    gates.assert_gates(pout, ref, what="paired units, paged")
-    gates.assert_lse(plse, ref_lse, what="paired units, paged")
+    _check_tiled_plan(pplan.info(), n_kv_heads=case["hkv"], rows_per_head=case["nb"] * n * case["g"])
+    gates.assert_gates(pout, ref, what="many units, paged")
+    gates.assert_lse(plse, ref_lse, what="many units, paged")
     assert pplan.device_error() == 0
 
 

@@ -76,8 +76,8 @@ def scan(asm: str, kernel: str, horizon: int = 120):
     return pairs
 
 
-def kernels(asm: str):
-    return re.findall(r"^(_ZN3fka\w*partials_kernel\w+):", asm, re.M)
+def kernels(asm: str, name: str = "partials_kernel"):
+    return re.findall(r"^(_ZN3fka\w*" + name + r"\w+):", asm, re.M)
 
 
 def compile_asm(hipcc: str, src: str, include: str, out: str) -> str:
