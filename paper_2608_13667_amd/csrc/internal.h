@@ -235,7 +235,8 @@ struct ScatterArgs {
 // Instruction prefill as a tiled multi-query kernel (prefill.hip, head_dim 128).  Rows of KV head g
 // are cut into units of 32 (row i: query head g G + i mod G of virtual sequence i / G, where
 // sequence s = b n + t is instruction token t of branch b); block vb takes KV head vb mod Hkv,
-// unit group (vb / Hkv) mod unit_groups (eight units, one per wave) and prefix range
+// unit group k = (vb / Hkv) mod unit_groups (units [floor(k U / UG), floor((k + 1) U / UG)), at
+// most eight, one per wave) and prefix range
 // vb / (Hkv unit_groups) of `ranges`, range r covering prefix tiles (64 keys) [floor(r T / R),
 // floor((r + 1) T / R)) of T = prefix_tiles + tail_reserve, clamped to the prefix; the last range
 // also reads the suffix keys.  Part r of output row (s, h) is written at

@@ -11,15 +11,19 @@
 //
 // Work: the rows of KV head g are cut into units of 32 consecutive rows (row i of the head is
 // query head g G + i mod G of sequence i / G), one unit per wave.  A block of eight waves takes
-// eight units of one KV head over one range of prefix tiles (64 keys each); the prefix is split
+// up to eight units of one KV head (the units spread evenly over the blocks of a range) over one
+// range of prefix tiles (64 keys each); the prefix is split
 // into R ranges so that the blocks fill the device, and the block of the last range also takes
 // the suffix keys.  Each wave writes one normalised partial (o, lse) per row for its range, and
 // the merge kernel combines a row's R partials (its explicit mode).
 //   * K and V tiles go from HBM (or L2: the blocks of one KV head and range run on one XCD when
 //     the KV heads are a multiple of 8 apart in the grid order) into LDS by DMA
-//     (buffer_load_dwordx4 ... lds), three tiles in flight, each tile loaded once by the block
-//     (every wave moves 8 of its 64 rows) and read by all eight waves, with a block barrier per
-//     tile;
+//     (buffer_load_dwordx4 ... lds) into three tile buffers (two loading while one is read),
+//     each tile loaded once by the block (every wave moves 8 of its 64 rows) and read by all
+//     eight waves, with a block barrier per tile;
+//   * within a tile, row tile 0's scores come first and the V operands of both halves are
+//     requested before the softmax, so the exponentials of row tile 1 run while the matrix
+//     cores take row tile 0's p.v;
 //   * S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_16x16x32_bf16 with keys on M, so each
 //     lane owns two query rows of the online softmax (rows l16 and 16 + l16 of the unit) and
 //     16 keys of each per tile; P enters the second product as two bf16 terms (hi + lo);
@@ -213,8 +217,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
     const int vb = blockIdx.x;
     const int g = vb % Hkv, rest = vb / Hkv;
     const int ug = rest % a.unit_groups, r = rest / a.unit_groups;
-    const int u = ug * NW + wave;
-    const bool active = u < a.n_units;
+    // the units spread evenly over the groups (at most eight each): blocks of one range then
+    // stream its tiles at the same pace, so each tile is fetched once into the XCD's L2 for all
+    const int u = mul_div(ug, a.n_units, a.unit_groups) + wave;
+    const bool active = u < mul_div(ug + 1, a.n_units, a.unit_groups);
     const int R = a.ranges;
     const int PT = a.prefix_tiles;
     const int total = PT + a.tail_reserve;
@@ -305,40 +311,51 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 
     // Softmax of NM M tiles of scores (x[t][i][j]: row 16 t + l16, key 16 i + 4 q4 + j of the
     // tile, raw q.k or -inf) into the two bf16 terms of P per k-step of 32 keys.
-    auto softmax = [&](auto NMc, auto &x, auto &ph, auto &pl) {
+    // Row tile t's maximum over NM M tiles of scores (xt[i][j]: key 16 i + 4 q4 + j of the tile,
+    // raw q.k or -inf), moving the running maximum (and rescaling) when it grows by over 2^8.
+    auto row_max = [&](auto NMc, int t, const float (&xt)[decltype(NMc)::value][4]) {
         constexpr int NM = decltype(NMc)::value;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < NM; ++i) mx = fmaxf(mx, fmaxf(fmaxf(xt[i][0], xt[i][1]), fmaxf(xt[i][2], xt[i][3])));
+        mx = max_over_rows(mx) * a.scale_log2;  // the scale is positive: the order is kept
+        const bool move = mx > m_ref[t] + kRescaleGap;
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(move) != 0, 0)) {
+            const float m_new = move ? mx : m_ref[t];
+            // exactly 1 for a row that keeps its max; 0 when the row's max was -inf
+            const float alpha = move ? fast_exp2(m_ref[t] - m_new) : 1.f;
+            l_run[t] *= alpha;
+            xdl_result_wait();
+#pragma unroll
+            for (int e = 0; e < NE; ++e) acc[t][e] *= alpha;
+            m_ref[t] = m_new;
+        }
+    };
+    // Row tile t's p = 2^(scale q.k - max) into the two bf16 terms per k-step of 32 keys.
+    auto row_exp = [&](auto NMc, int t, const float (&xt)[decltype(NMc)::value][4],
+                       bf16x8 (&pht)[decltype(NMc)::value / 2], bf16x8 (&plt)[decltype(NMc)::value / 2]) {
+        constexpr int NM = decltype(NMc)::value;
+        const float nm = (m_ref[t] == -INFINITY) ? 0.f : -m_ref[t];
+        float ps = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < NM / 2; ++kk) {
+            float p[8];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                p[j] = fast_exp2(__builtin_fmaf(xt[2 * kk][j], a.scale_log2, nm));
+                p[4 + j] = fast_exp2(__builtin_fmaf(xt[2 * kk + 1][j], a.scale_log2, nm));
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) ps += p[j];
+            split_p(p, pht[kk], plt[kk]);
+        }
+        l_run[t] += ps;
+    };
+    auto softmax = [&](auto NMc, auto &x, auto &ph, auto &pl) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int i = 0; i < NM; ++i) mx = fmaxf(mx, fmaxf(fmaxf(x[t][i][0], x[t][i][1]), fmaxf(x[t][i][2], x[t][i][3])));
-            mx = max_over_rows(mx) * a.scale_log2;  // the scale is positive: the order is kept
-            const bool move = mx > m_ref[t] + kRescaleGap;
-            if (__builtin_expect(__builtin_amdgcn_ballot_w64(move) != 0, 0)) {
-                const float m_new = move ? mx : m_ref[t];
-                // exactly 1 for a row that keeps its max; 0 when the row's max was -inf
-                const float alpha = move ? fast_exp2(m_ref[t] - m_new) : 1.f;
-                l_run[t] *= alpha;
-                xdl_result_wait();
-#pragma unroll
-                for (int e = 0; e < NE; ++e) acc[t][e] *= alpha;
-                m_ref[t] = m_new;
-            }
-            const float nm = (m_ref[t] == -INFINITY) ? 0.f : -m_ref[t];
-            float ps = 0.f;
-#pragma unroll
-            for (int kk = 0; kk < NM / 2; ++kk) {
-                float p[8];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    p[j] = fast_exp2(__builtin_fmaf(x[t][2 * kk][j], a.scale_log2, nm));
-                    p[4 + j] = fast_exp2(__builtin_fmaf(x[t][2 * kk + 1][j], a.scale_log2, nm));
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) ps += p[j];
-                split_p(p, ph[t][kk], pl[t][kk]);
-            }
-            l_run[t] += ps;
+            row_max(NMc, t, x[t]);
+            row_exp(NMc, t, x[t], ph[t], pl[t]);
         }
     };
 
@@ -355,7 +372,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         }
     };
 
-    // ---- the prefix range: tiles [t0, t1), three in flight, one barrier per tile
+    // ---- the prefix range: tiles [t0, t1), two loading ahead, one barrier per tile
     if (ntile > 0) issue_prefix(t0, 0);
     if (ntile > 1) issue_prefix(t0 + 1, 1);
     for (int i = 0; i < ntile; ++i) {
@@ -382,16 +399,31 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
             for (int c = 0; c < NC; ++c) asm volatile("" : "+v"(ka[mi][c]));
+        // row tile 0's scores first, so its softmax can start while row tile 1's MFMAs run
         f32x4 sc[4][2];
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
+            for (int mi = 0; mi < 4; ++mi) {
                 f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int c = 0; c < NC; ++c) s = mfma16(ka[mi][c], qb[t][c], s);
                 sc[mi][t] = s;
             }
+        // V^T operands of both k-steps, requested now: they arrive during the softmax
+        vtr_t v0[NE][2], v1[NE][2];
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            const uint32_t ad = vaddr[e] + so;
+            v0[e][0] = ds_read_tr16<0 * 16 * ROWB>(ad);
+            v0[e][1] = ds_read_tr16<1 * 16 * ROWB>(ad);
+        }
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            const uint32_t ad = vaddr[e] + so;
+            v1[e][0] = ds_read_tr16<2 * 16 * ROWB>(ad);
+            v1[e][1] = ds_read_tr16<3 * 16 * ROWB>(ad);
+        }
         xdl_result_wait();
         float x[2][4][4];
 #pragma unroll
@@ -411,29 +443,36 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
                     for (int j = 0; j < 4; ++j) x[t][mi][j] = (16 * mi + j < v4) ? x[t][mi][j] : -INFINITY;
         }
         bf16x8 ph[2][2], pl[2][2];
-        softmax(std::integral_constant<int, 4>{}, x, ph, pl);
-        // p.v: V^T operands after the softmax, so they are not live with its temporaries
+        constexpr std::integral_constant<int, 4> nm4{};
+        row_max(nm4, 0, x[0]);
+        row_exp(nm4, 0, x[0], ph[0], pl[0]);
+        row_max(nm4, 1, x[1]);
+        // the first k-step's values: of the 32 reads, the 16 issued first (LDS reads return in
+        // order, so with at most 15 outstanding those have all returned)
+        asm volatile("s_waitcnt lgkmcnt(15)" ::: "memory");
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            vtr_t vr[NE][2];
+        for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v0[e][0]), "+v"(v0[e][1]));
+        // p.v of row tile 0 over the first 32 keys while row tile 1's exponentials run
 #pragma unroll
-            for (int e = 0; e < NE; ++e) {
-                const uint32_t ad = vaddr[e] + so;
-                if (kk == 0) {
-                    vr[e][0] = ds_read_tr16<0 * 16 * ROWB>(ad);
-                    vr[e][1] = ds_read_tr16<1 * 16 * ROWB>(ad);
-                } else {
-                    vr[e][0] = ds_read_tr16<2 * 16 * ROWB>(ad);
-                    vr[e][1] = ds_read_tr16<3 * 16 * ROWB>(ad);
-                }
-            }
-            lds_wait();
-#pragma unroll
-            for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(vr[e][0]), "+v"(vr[e][1]));
-            const bf16x8 h2[2] = {ph[0][kk], ph[1][kk]}, l2[2] = {pl[0][kk], pl[1][kk]};
-            pv_step(vr, h2, l2);
+        for (int e = 0; e < NE; ++e) {
+            const bf16x8 va = join_tr16(v0[e][0], v0[e][1]);
+            acc[0][e] = mfma16(va, ph[0][0], acc[0][e]);
+            acc[0][e] = mfma16(va, pl[0][0], acc[0][e]);
         }
+        row_exp(nm4, 1, x[1], ph[1], pl[1]);
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            const bf16x8 va = join_tr16(v0[e][0], v0[e][1]);
+            acc[1][e] = mfma16(va, ph[1][0], acc[1][e]);
+            acc[1][e] = mfma16(va, pl[1][0], acc[1][e]);
+        }
+        lds_wait();
+#pragma unroll
+        for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v1[e][0]), "+v"(v1[e][1]));
+        const bf16x8 h2[2] = {ph[0][1], ph[1][1]}, l2[2] = {pl[0][1], pl[1][1]};
+        pv_step(v1, h2, l2);
     }
+
 
     // ---- suffix keys (last range only): per wave, branch by branch of the unit's rows
     if (r == R - 1) {
