@@ -67,6 +67,8 @@ constexpr float kLn2 = 0.693147180559945309f;
 constexpr float kRescaleGap = 8.0f;  // log2 units
 
 static_assert(NW * SUF_LDS <= LDS_BYTES, "suffix areas fit the stage buffers");
+static_assert(STAGES == 3, "the tile loop is unrolled over three buffers");
+static_assert((STAGES - 1) * KBYTES + 3 * 16 * ROWB < 65536, "LDS offsets fit the immediate field");
 
 __device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c)
 {
@@ -116,13 +118,22 @@ __device__ inline void static_for(F &&f)
     static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// Reductions over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four lanes holding one query row).
+// max(a, b) in one instruction, for values that hold no signalling NaN (see max3 below).
+__device__ inline float max2(float a, float b)
+{
+    float r;
+    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+// Reductions over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four lanes holding one query row).  The
+// maximum's inputs are maxima of matrix-core results (no signalling NaN).
 __device__ inline float max_over_rows(float x)
 {
     const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    x = max2(__uint_as_float(a[0]), __uint_as_float(a[1]));
     const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+    return max2(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 __device__ inline float sum_over_rows(float x)
@@ -168,6 +179,38 @@ __device__ inline void xdl_result_wait()
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_nop 7\n\ts_nop 7" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
+}
+
+// max(a, b, c) in one instruction.  fmaxf on a matrix-core result makes the compiler quiet a
+// possible signalling NaN first (one more instruction per value); the matrix cores produce
+// only quiet NaNs, which v_max3_f32 ignores as fmaxf does.
+__device__ inline float max3(float a, float b, float c)
+{
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
+// Maximum of n values as a tree of v_max3_f32.
+template <int N>
+__device__ inline float max_of(const float (&v)[N])
+{
+    static_assert(N >= 3, "at least three values");
+    if constexpr (N == 3) {
+        return max3(v[0], v[1], v[2]);
+    } else {
+        constexpr int M = (N + 2) / 3;
+        float w[M];
+#pragma unroll
+        for (int i = 0; i < M; ++i) {
+            const int k = 3 * i;
+            w[i] = (k + 2 < N) ? max3(v[k], v[k + 1], v[k + 2]) : (k + 1 < N) ? max2(v[k], v[k + 1]) : v[k];
+        }
+        if constexpr (M < 3)
+            return max2(w[0], w[M - 1]);
+        else
+            return max_of(w);
+    }
 }
 
 __device__ inline int opaque_lane_id()
@@ -315,10 +358,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
     // raw q.k or -inf), moving the running maximum (and rescaling) when it grows by over 2^8.
     auto row_max = [&](auto NMc, int t, const float (&xt)[decltype(NMc)::value][4]) {
         constexpr int NM = decltype(NMc)::value;
-        float mx = -INFINITY;
+        float v[4 * NM];
 #pragma unroll
-        for (int i = 0; i < NM; ++i) mx = fmaxf(mx, fmaxf(fmaxf(xt[i][0], xt[i][1]), fmaxf(xt[i][2], xt[i][3])));
-        mx = max_over_rows(mx) * a.scale_log2;  // the scale is positive: the order is kept
+        for (int i = 0; i < NM; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[4 * i + j] = xt[i][j];
+        const float mx = max_over_rows(max_of(v)) * a.scale_log2;  // the scale is positive: the order is kept
         const bool move = mx > m_ref[t] + kRescaleGap;
         if (__builtin_expect(__builtin_amdgcn_ballot_w64(move) != 0, 0)) {
             const float m_new = move ? mx : m_ref[t];
@@ -375,24 +420,26 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
     // ---- the prefix range: tiles [t0, t1), two loading ahead, one barrier per tile
     if (ntile > 0) issue_prefix(t0, 0);
     if (ntile > 1) issue_prefix(t0 + 1, 1);
-    for (int i = 0; i < ntile; ++i) {
+    // tile i of the range, held in buffer ST = i mod 3 (a constant, so that every LDS address
+    // offset below is an instruction immediate)
+    auto tile_step = [&](int i, auto STc) {
+        constexpr int ST = decltype(STc)::value;
+        constexpr int SO = ST * KBYTES;
         if (i + 1 < ntile)
             wait_vm<4>();
         else
             wait_vm<0>();
         lds_barrier();  // tile i is in LDS, and every wave is done with tile i - 1
         if (i + 2 < ntile) issue_prefix(t0 + i + 2, (i + 2) % STAGES);
-        if (!active) continue;
-        const uint32_t so = (uint32_t)((i % STAGES) * KBYTES);
+        if (!active) return;
         // q.k: K A operands of all four M tiles, then 32 MFMAs
         bf16x8 ka[4][NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const uint32_t ad = kaddr[c] + so;
-            ka[0][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<0 * 16 * ROWB>(ad));
-            ka[1][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<1 * 16 * ROWB>(ad));
-            ka[2][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<2 * 16 * ROWB>(ad));
-            ka[3][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<3 * 16 * ROWB>(ad));
+            ka[0][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 0 * 16 * ROWB>(kaddr[c]));
+            ka[1][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 1 * 16 * ROWB>(kaddr[c]));
+            ka[2][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 2 * 16 * ROWB>(kaddr[c]));
+            ka[3][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 3 * 16 * ROWB>(kaddr[c]));
         }
         lds_wait();
 #pragma unroll
@@ -414,15 +461,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         vtr_t v0[NE][2], v1[NE][2];
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
-            const uint32_t ad = vaddr[e] + so;
-            v0[e][0] = ds_read_tr16<0 * 16 * ROWB>(ad);
-            v0[e][1] = ds_read_tr16<1 * 16 * ROWB>(ad);
+            v0[e][0] = ds_read_tr16<SO + 0 * 16 * ROWB>(vaddr[e]);
+            v0[e][1] = ds_read_tr16<SO + 1 * 16 * ROWB>(vaddr[e]);
         }
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
-            const uint32_t ad = vaddr[e] + so;
-            v1[e][0] = ds_read_tr16<2 * 16 * ROWB>(ad);
-            v1[e][1] = ds_read_tr16<3 * 16 * ROWB>(ad);
+            v1[e][0] = ds_read_tr16<SO + 2 * 16 * ROWB>(vaddr[e]);
+            v1[e][1] = ds_read_tr16<SO + 3 * 16 * ROWB>(vaddr[e]);
         }
         xdl_result_wait();
         float x[2][4][4];
@@ -471,6 +516,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v1[e][0]), "+v"(v1[e][1]));
         const bf16x8 h2[2] = {ph[0][1], ph[1][1]}, l2[2] = {pl[0][1], pl[1][1]};
         pv_step(v1, h2, l2);
+    };
+    for (int i = 0; i < ntile; i += STAGES) {
+        tile_step(i, std::integral_constant<int, 0>{});
+        if (i + 1 < ntile) tile_step(i + 1, std::integral_constant<int, 1>{});
+        if (i + 2 < ntile) tile_step(i + 2, std::integral_constant<int, 2>{});
     }
 
 
