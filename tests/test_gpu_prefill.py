@@ -193,6 +193,46 @@ def _check_case(fa, c):
     assert plan.device_error() == 0
 
 
+@pytest.mark.parametrize("c", [dict(head_dim=128, n_kv_heads=2, n_q_heads=8, n_branches=4, n=20, prefix_len=0, lo=5,
+                                      blocks=0, seed=2750),
+                                 dict(head_dim=128, n_kv_heads=2, n_q_heads=8, n_branches=4, n=20, prefix_len=1500,
+                                      lo=5, blocks=3, seed=2751),
+                                 dict(head_dim=128, n_kv_heads=1, n_q_heads=1, n_branches=256, n=2, prefix_len=700,
+                                      lo=0, blocks=0, seed=2752)],
+                         ids=["empty-prefix", "one-range", "16-branches-per-unit"])
+def test_prefill_tiled_edges(fa, c):
+    """The tiled kernel (at least 256 rows per KV head) with no prefix at all (the suffix keys
+    only), with an explicit grid of one prefix range, and with G = 1 and 2-token instructions of
+    256 branches, where a 32-row unit holds 16 branches (each masked to its own suffix)."""
+    _check_case(fa, c)
+
+
+def test_prefill_tiled_nonfinite_instruction_value(fa):
+    """A NaN in the value of instruction token 17 of branch 1 (KV head 1) reaches exactly the rows
+    that attend to it: branch 1's tokens 17.. on that KV head's query heads.  Its earlier tokens and
+    every other branch and KV head stay exact (a row that does not read the key multiplies it by
+    p = 0, which must not turn into NaN), contiguous and paged."""
+    n, G, hkv = 40, 5, 2
+    spec = W.CONFIGS["mid"].replace(n_kv_heads=hkv, n_q_heads=hkv * G, n_branches=3, prefix_len=900,
+                                    suffix_range=(3, 30), steps=n, seed=2760)
+    w = W.make(spec)
+    q, sk, sv = _instruction(w, n)
+    ref, _ = _reference(w, n, q, sk, sv)
+    bad_b, bad_t, bad_g = 1, 17, 1
+    sv[bad_b, bad_g, int(w.suffix_len[bad_b]) + bad_t, 5] = W.BF16_NAN
+    N, _, Hq, d = q.shape
+    hit = np.zeros((N * n, Hq), bool)
+    for t in range(bad_t, n):
+        hit[bad_b * n + t, bad_g * G:(bad_g + 1) * G] = True
+    plan, out, _ = _run(fa, w, n, q, sk, sv)
+    assert plan.info().units_per_block == 8
+    pplan, pout, _ = _run_paged(fa, w, n, q, sk, sv, seed=2761)
+    for what, o in (("contiguous", out), ("paged", pout)):
+        assert np.all(np.isnan(o[hit])), what
+        gates.assert_gates(o[~hit], ref[~hit], what=f"rows that do not read the NaN, {what}")
+    assert plan.device_error() == 0 and pplan.device_error() == 0
+
+
 def _to_pool(w, sk, sv, seed, spare=5):
     """The prefix and each branch's suffix buffer (instruction tokens included) in a page pool of
     16-token pages whose ids are a seeded permutation: the prefix pages are shared by every
