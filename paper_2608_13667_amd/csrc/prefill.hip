@@ -18,12 +18,12 @@
 // the merge kernel combines a row's R partials (its explicit mode).
 //   * K and V tiles go from HBM (or L2: the blocks of one KV head and range run on one XCD when
 //     the KV heads are a multiple of 8 apart in the grid order) into LDS by DMA
-//     (buffer_load_dwordx4 ... lds) into three tile buffers (two loading while one is read),
-//     each tile loaded once by the block (every wave moves 8 of its 64 rows) and read by all
-//     eight waves, with a block barrier per tile;
-//   * within a tile, row tile 0's scores come first and the V operands of both halves are
-//     requested before the softmax, so the exponentials of row tile 1 run while the matrix
-//     cores take row tile 0's p.v;
+//     (buffer_load_dwordx4 ... lds) into four tile buffers (two read while two load), each
+//     tile loaded once by the block (every wave moves 8 of its 64 rows) and read by all eight
+//     waves;
+//   * the two waves of a SIMD alternate between matrix and vector work, in two phases per tile
+//     with a block barrier between them: while one takes p.v of the previous tile and q.k of
+//     this one (at raised priority), the other takes a softmax, and then the roles swap;
 //   * S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_16x16x32_bf16 with keys on M, so each
 //     lane owns two query rows of the online softmax (rows l16 and 16 + l16 of the unit) and
 //     16 keys of each per tile; P enters the second product as two bf16 terms (hi + lo);
@@ -56,10 +56,10 @@ constexpr int NC = HD / 32;        // k-steps of the q.k product
 constexpr int NE = HD / 16;        // 16-wide d tiles of the output
 constexpr int KT = 64;             // keys per prefix tile
 constexpr int NW = 8;              // waves per block (two per SIMD)
-constexpr int STAGES = 3;          // prefix tiles in flight
+constexpr int STAGES = 4;          // prefix tile buffers: two read, two loading
 constexpr int KBYTES = KT * ROWB;  // 16 KiB of K (or V) per tile
-constexpr int K_LDS = 0;           // K stages at [0, 48 KiB)
-constexpr int V_LDS = STAGES * KBYTES;  // V stages at [48, 96 KiB)
+constexpr int K_LDS = 0;           // K buffers at [0, 64 KiB)
+constexpr int V_LDS = STAGES * KBYTES;  // V buffers at [64, 128 KiB)
 constexpr int LDS_BYTES = 2 * STAGES * KBYTES;
 constexpr int ST = 32;             // keys per suffix tile
 constexpr int SUF_LDS = ST * ROWB; // per-wave V area for a suffix tile (8 KiB), reusing the stages
@@ -67,7 +67,7 @@ constexpr float kLn2 = 0.693147180559945309f;
 constexpr float kRescaleGap = 8.0f;  // log2 units
 
 static_assert(NW * SUF_LDS <= LDS_BYTES, "suffix areas fit the stage buffers");
-static_assert(STAGES == 3, "the tile loop is unrolled over three buffers");
+static_assert(STAGES == 4, "the tile loop is unrolled over its four buffers");
 static_assert((STAGES - 1) * KBYTES + 3 * 16 * ROWB < 65536, "LDS offsets fit the immediate field");
 
 __device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c)
@@ -417,58 +417,48 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         }
     };
 
-    // ---- the prefix range: tiles [t0, t1), two loading ahead, one barrier per tile
-    if (ntile > 0) issue_prefix(t0, 0);
-    if (ntile > 1) issue_prefix(t0 + 1, 1);
-    // tile i of the range, held in buffer ST = i mod 3 (a constant, so that every LDS address
-    // offset below is an instruction immediate)
-    auto tile_step = [&](int i, auto STc) {
-        constexpr int ST = decltype(STc)::value;
-        constexpr int SO = ST * KBYTES;
-        if (i + 1 < ntile)
-            wait_vm<4>();
-        else
-            wait_vm<0>();
-        lds_barrier();  // tile i is in LDS, and every wave is done with tile i - 1
-        if (i + 2 < ntile) issue_prefix(t0 + i + 2, (i + 2) % STAGES);
-        if (!active) return;
-        // q.k: K A operands of all four M tiles, then 32 MFMAs
-        bf16x8 ka[4][NC];
+    // ---- the prefix range: tiles [t0, t1), two loading ahead, in two phases per tile.  The two
+    // waves of a SIMD alternate between matrix and vector work: in phase 1 of step i the first
+    // wave (waves 0..3) takes q.k of tile i and p.v of tile i - 1 while the second (waves 4..7)
+    // takes the softmax of tile i - 1; in phase 2 the first takes the softmax of tile i while the
+    // second takes p.v of tile i - 1 and q.k of tile i (both waves take p.v before q.k, so that p
+    // and the new scores are not live together).  A block barrier separates the phases; the
+    // wave in its matrix phase runs at raised priority.  Four tile buffers: tiles i - 1 and i are
+    // read during step i while i + 1 and i + 2 load.
+    using nm4_t = std::integral_constant<int, 4>;
+    // q.k of the tile at buffer offset SO: each M tile's K operands are read one M tile ahead of
+    // its MFMAs (LDS reads return in order, so "at most 4 outstanding" means the earlier M tile's
+    // four reads are in)
+    auto qk = [&](auto SOc, f32x4 (&sc)[4][2]) {
+        constexpr int SO = decltype(SOc)::value;
+        bf16x8 ka[2][NC];
+        auto rd = [&](auto MIc) {
+            constexpr int mi = decltype(MIc)::value;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            ka[0][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 0 * 16 * ROWB>(kaddr[c]));
-            ka[1][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 1 * 16 * ROWB>(kaddr[c]));
-            ka[2][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 2 * 16 * ROWB>(kaddr[c]));
-            ka[3][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + 3 * 16 * ROWB>(kaddr[c]));
-        }
-        lds_wait();
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-            for (int c = 0; c < NC; ++c) asm volatile("" : "+v"(ka[mi][c]));
-        // row tile 0's scores first, so its softmax can start while row tile 1's MFMAs run
-        f32x4 sc[4][2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi) {
-                f32x4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int c = 0; c < NC; ++c) s = mfma16(ka[mi][c], qb[t][c], s);
-                sc[mi][t] = s;
+            for (int c = 0; c < NC; ++c)
+                ka[mi & 1][c] = __builtin_bit_cast(bf16x8, ds_read_b128_at<SO + mi * 16 * ROWB>(kaddr[c]));
+        };
+        rd(std::integral_constant<int, 0>{});
+        static_for<4>([&](auto MIc) {
+            constexpr int mi = decltype(MIc)::value;
+            if constexpr (mi + 1 < 4) {
+                rd(std::integral_constant<int, mi + 1>{});
+                asm volatile("s_waitcnt lgkmcnt(4)" ::: "memory");
+            } else {
+                lds_wait();
             }
-        // V^T operands of both k-steps, requested now: they arrive during the softmax
-        vtr_t v0[NE][2], v1[NE][2];
 #pragma unroll
-        for (int e = 0; e < NE; ++e) {
-            v0[e][0] = ds_read_tr16<SO + 0 * 16 * ROWB>(vaddr[e]);
-            v0[e][1] = ds_read_tr16<SO + 1 * 16 * ROWB>(vaddr[e]);
-        }
+            for (int c = 0; c < NC; ++c) asm volatile("" : "+v"(ka[mi & 1][c]));
 #pragma unroll
-        for (int e = 0; e < NE; ++e) {
-            v1[e][0] = ds_read_tr16<SO + 2 * 16 * ROWB>(vaddr[e]);
-            v1[e][1] = ds_read_tr16<SO + 3 * 16 * ROWB>(vaddr[e]);
-        }
+            for (int t = 0; t < 2; ++t) {
+                f32x4 v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int c = 0; c < NC; ++c) v = mfma16(ka[mi & 1][c], qb[t][c], v);
+                sc[mi][t] = v;
+            }
+        });
+    };
+    auto sm = [&](const f32x4 (&sc)[4][2], int tile, bf16x8 (&ph)[2][2], bf16x8 (&pl)[2][2]) {
         xdl_result_wait();
         float x[2][4][4];
 #pragma unroll
@@ -477,7 +467,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
             for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) x[t][mi][j] = sc[mi][t][j];
-        const int valid = Lp - (t0 + i) * KT;  // keys of this tile that exist (may exceed 64)
+        const int valid = Lp - tile * KT;  // keys of this tile that exist (may exceed 64)
         if (__builtin_expect(valid < KT, 0)) {
             const int v4 = valid - 4 * (opaque_lane_id() >> 4);
 #pragma unroll
@@ -487,40 +477,85 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
                     for (int j = 0; j < 4; ++j) x[t][mi][j] = (16 * mi + j < v4) ? x[t][mi][j] : -INFINITY;
         }
-        bf16x8 ph[2][2], pl[2][2];
-        constexpr std::integral_constant<int, 4> nm4{};
-        row_max(nm4, 0, x[0]);
-        row_exp(nm4, 0, x[0], ph[0], pl[0]);
-        row_max(nm4, 1, x[1]);
-        // the first k-step's values: of the 32 reads, the 16 issued first (LDS reads return in
-        // order, so with at most 15 outstanding those have all returned)
-        asm volatile("s_waitcnt lgkmcnt(15)" ::: "memory");
 #pragma unroll
-        for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v0[e][0]), "+v"(v0[e][1]));
-        // p.v of row tile 0 over the first 32 keys while row tile 1's exponentials run
-#pragma unroll
-        for (int e = 0; e < NE; ++e) {
-            const bf16x8 va = join_tr16(v0[e][0], v0[e][1]);
-            acc[0][e] = mfma16(va, ph[0][0], acc[0][e]);
-            acc[0][e] = mfma16(va, pl[0][0], acc[0][e]);
+        for (int t = 0; t < 2; ++t) {
+            row_max(nm4_t{}, t, x[t]);
+            row_exp(nm4_t{}, t, x[t], ph[t], pl[t]);
         }
-        row_exp(nm4, 1, x[1], ph[1], pl[1]);
-#pragma unroll
-        for (int e = 0; e < NE; ++e) {
-            const bf16x8 va = join_tr16(v0[e][0], v0[e][1]);
-            acc[1][e] = mfma16(va, ph[1][0], acc[1][e]);
-            acc[1][e] = mfma16(va, pl[1][0], acc[1][e]);
-        }
-        lds_wait();
-#pragma unroll
-        for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v1[e][0]), "+v"(v1[e][1]));
-        const bf16x8 h2[2] = {ph[0][1], ph[1][1]}, l2[2] = {pl[0][1], pl[1][1]};
-        pv_step(v1, h2, l2);
     };
-    for (int i = 0; i < ntile; i += STAGES) {
-        tile_step(i, std::integral_constant<int, 0>{});
-        if (i + 1 < ntile) tile_step(i + 1, std::integral_constant<int, 1>{});
-        if (i + 2 < ntile) tile_step(i + 2, std::integral_constant<int, 2>{});
+    auto pv_tile = [&](auto SOc, const bf16x8 (&ph)[2][2], const bf16x8 (&pl)[2][2]) {
+        constexpr int SO = decltype(SOc)::value;
+        static_for<2>([&](auto KKc) {
+            constexpr int kk = decltype(KKc)::value;
+            vtr_t vr[NE][2];
+#pragma unroll
+            for (int e = 0; e < NE; ++e) {
+                vr[e][0] = ds_read_tr16<SO + (2 * kk) * 16 * ROWB>(vaddr[e]);
+                vr[e][1] = ds_read_tr16<SO + (2 * kk + 1) * 16 * ROWB>(vaddr[e]);
+            }
+            lds_wait();
+#pragma unroll
+            for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(vr[e][0]), "+v"(vr[e][1]));
+            const bf16x8 h2[2] = {ph[0][kk], ph[1][kk]}, l2[2] = {pl[0][kk], pl[1][kk]};
+            pv_step(vr, h2, l2);
+        });
+    };
+    f32x4 sc[4][2];
+    bf16x8 ph[2][2], pl[2][2];
+    // step i (0 <= i <= ntile; the last one only finishes tile ntile - 1), tile i in buffer B.  The
+    // two roles run in loops of their own (a role test in each phase would keep both roles'
+    // values live at once); both pass the same barriers.
+    auto step = [&](int i, auto Bc, auto LEADc) {
+        constexpr int B = decltype(Bc)::value;
+        constexpr bool LEAD = decltype(LEADc)::value;
+        constexpr int SO = B * KBYTES, SOP = ((B + STAGES - 1) % STAGES) * KBYTES;
+        using so_t = std::integral_constant<int, SO>;
+        using sop_t = std::integral_constant<int, SOP>;
+        if (i < ntile) {
+            if (i + 1 < ntile)
+                wait_vm<4>();
+            else
+                wait_vm<0>();
+        }
+        lds_barrier();  // tile i is in LDS; every wave is done with tile i - 2
+        if (i + 2 < ntile) issue_prefix(t0 + i + 2, (i + 2) % STAGES);
+        if (active) {
+            if constexpr (LEAD) {
+                __builtin_amdgcn_s_setprio(1);
+                if (i > 0) pv_tile(sop_t{}, ph, pl);
+                if (i < ntile) qk(so_t{}, sc);
+                __builtin_amdgcn_s_setprio(0);
+            } else {
+                if (i > 0) sm(sc, t0 + i - 1, ph, pl);
+            }
+        }
+        lds_barrier();
+        if (active) {
+            if constexpr (LEAD) {
+                if (i < ntile) sm(sc, t0 + i, ph, pl);
+            } else {
+                __builtin_amdgcn_s_setprio(1);
+                if (i > 0) pv_tile(sop_t{}, ph, pl);
+                if (i < ntile) qk(so_t{}, sc);
+                __builtin_amdgcn_s_setprio(0);
+            }
+        }
+    };
+    auto run = [&](auto LEADc) {
+        for (int i = 0; i <= ntile; i += STAGES) {
+            step(i, std::integral_constant<int, 0>{}, LEADc);
+            if (i + 1 <= ntile) step(i + 1, std::integral_constant<int, 1>{}, LEADc);
+            if (i + 2 <= ntile) step(i + 2, std::integral_constant<int, 2>{}, LEADc);
+            if (i + 3 <= ntile) step(i + 3, std::integral_constant<int, 3>{}, LEADc);
+        }
+    };
+    if (ntile > 0) issue_prefix(t0, 0);
+    if (ntile > 1) issue_prefix(t0 + 1, 1);
+    if (ntile > 0) {
+        if (wave < 4)
+            run(std::true_type{});
+        else
+            run(std::false_type{});
     }
 
 
