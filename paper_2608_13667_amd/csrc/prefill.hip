@@ -12,9 +12,8 @@
 // Work: the rows of KV head g are cut into units of 32 consecutive rows (row i of the head is
 // query head g G + i mod G of sequence i / G), one unit per wave.  A block of eight waves takes
 // up to eight units of one KV head (the units spread evenly over the blocks of a range) over one
-// range of prefix tiles (64 keys each); the prefix is split
-// into R ranges so that the blocks fill the device, and the block of the last range also takes
-// the suffix keys.  Each wave writes one normalised partial (o, lse) per row for its range, and
+// range of prefix tiles (64 keys each); the prefix is split into R ranges so that the blocks fill
+// the device, and the block of the last range also takes the suffix keys.  Each wave writes one normalised partial (o, lse) per row for its range, and
 // the merge kernel combines a row's R partials (its explicit mode).
 //   * K and V tiles go from HBM (or L2: the blocks of one KV head and range run on one XCD when
 //     the KV heads are a multiple of 8 apart in the grid order) into LDS by DMA
@@ -419,10 +418,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 
     // ---- the prefix range: tiles [t0, t1), two loading ahead, in two phases per tile.  The two
     // waves of a SIMD alternate between matrix and vector work: in phase 1 of step i the first
-    // wave (waves 0..3) takes q.k of tile i and p.v of tile i - 1 while the second (waves 4..7)
+    // wave (waves 0..3) takes p.v of tile i - 1 and q.k of tile i while the second (waves 4..7)
     // takes the softmax of tile i - 1; in phase 2 the first takes the softmax of tile i while the
-    // second takes p.v of tile i - 1 and q.k of tile i (both waves take p.v before q.k, so that p
-    // and the new scores are not live together).  A block barrier separates the phases; the
+    // second takes p.v of tile i - 1 and q.k of tile i (p.v first, so that p and the new scores
+    // are not live together).  A block barrier separates the phases; the
     // wave in its matrix phase runs at raised priority.  Four tile buffers: tiles i - 1 and i are
     // read during step i while i + 1 and i + 2 load.
     using nm4_t = std::integral_constant<int, 4>;
@@ -557,7 +556,6 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
         else
             run(std::false_type{});
     }
-
 
     // ---- suffix keys (last range only): per wave, branch by branch of the unit's rows
     if (r == R - 1) {
