@@ -233,6 +233,30 @@ def test_prefill_tiled_nonfinite_instruction_value(fa):
     assert plan.device_error() == 0 and pplan.device_error() == 0
 
 
+def test_prefill_paired_units_on_the_streaming_path(fa):
+    """Fewer than 256 rows per KV head keeps the partial kernel's prefill instantiation; with 64 KV
+    heads its items (5 units of 32 rows x 64) outnumber the resident blocks, so an eight-wave block
+    takes two units of one KV head, four waves each.  Every row checked, contiguous and paged."""
+    n = 30
+    spec = W.CONFIGS["long"].replace(prefix_len=700, n_branches=5, n_kv_heads=64, n_q_heads=64,
+                                     suffix_range=(0, 9), steps=n, seed=2780)
+    w = W.make(spec)
+    q, sk, sv = _instruction(w, n)
+    plan, out, lse = _run(fa, w, n, q, sk, sv)
+    info = plan.info()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    print(f"[prefill] streaming, paired: {info.n_units} units, {info.n_items} items, {info.n_blocks} blocks",
+          flush=True)
+    assert info.units_per_block == 2 and info.n_units == 5 and info.n_items > cus
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    gates.assert_gates(out, ref, what="paired units, streaming")
+    gates.assert_lse(lse, ref_lse, what="paired units, streaming")
+    pplan, pout, _ = _run_paged(fa, w, n, q, sk, sv, seed=2781)
+    assert pplan.info().units_per_block == 2
+    gates.assert_gates(pout, ref, what="paired units, streaming, paged")
+    assert plan.device_error() == 0 and pplan.device_error() == 0
+
+
 def _to_pool(w, sk, sv, seed, spare=5):
     """The prefix and each branch's suffix buffer (instruction tokens included) in a page pool of
     16-token pages whose ids are a seeded permutation: the prefix pages are shared by every
