@@ -422,8 +422,9 @@ typedef struct {
     int32_t waves_per_block;   /* waves of one block of the partial kernel */
     int32_t n_blocks;          /* blocks of the partial kernel per round */
     int32_t rounds;            /* the kernel runs n_blocks * rounds blocks */
-    int32_t n_slots;           /* partial-result slots in the workspace */
-    int32_t slot_rows;         /* rows per slot: the largest item's query rows */
+    int32_t n_slots;           /* partial-result slots in the workspace (tiled prefill: one per prefix range) */
+    int32_t slot_rows;         /* rows per slot: the largest item's query rows (tiled prefill: all
+                                  N x n_tokens x Hq output rows) */
     int32_t static_split;      /* 1: one unit, items split statically */
     int32_t units_per_block;   /* instruction prefill: units a block takes: 8 on the tiled kernel, else
                                   1 or 2 (decode plans: 1) */
