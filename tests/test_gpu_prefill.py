@@ -257,6 +257,60 @@ def test_prefill_paired_units_on_the_streaming_path(fa):
     assert plan.device_error() == 0 and pplan.device_error() == 0
 
 
+def _tiled_case(seed, n=20):
+    """A small shape on the tiled kernel: d 128, 2 KV heads x G 4, 4 branches of n tokens
+    (320 rows per KV head), a 500-key prefix, suffixes of 10-20 keys."""
+    spec = W.CONFIGS["mid"].replace(n_kv_heads=2, n_q_heads=8, n_branches=4, prefix_len=500,
+                                    suffix_range=(10, 20), steps=n, seed=seed)
+    return W.make(spec), n
+
+
+def test_prefill_tiled_clamps_and_flags_a_suffix_past_the_bound(fa):
+    """The tiled kernel clamps a suffix length above max_suffix_len - n (flag 1); the other
+    branches stay exact."""
+    w, n = _tiled_case(2790)
+    q, sk, sv = _instruction(w, n)
+    bad = w.suffix_len.copy()
+    bad[1] = w.suffix_cap + 3
+    plan, out, lse = _run(fa, w, n, q, sk, sv, suffix_len=bad)
+    assert plan.info().units_per_block == 8
+    assert plan.device_error() == 1
+    ref, ref_lse = _reference(w, n, q, sk, sv)
+    rows = [t for t in range(q.shape[0] * n) if t // n != 1]
+    gates.assert_gates(out[rows], ref[rows], what="tiled, other branches unaffected")
+    gates.assert_lse(lse[rows], ref_lse[rows], what="tiled, other branches unaffected")
+
+
+@pytest.mark.parametrize("where", ["suffix", "prefix"])
+def test_prefill_tiled_paged_flags_a_bad_page(fa, where):
+    """The tiled kernel over the pool skips a page id outside the pool (its rows read as zeros) and
+    raises flag 4: in one branch's suffix row the other branches stay exact; in the shared prefix
+    the flag is raised."""
+    w, n = _tiled_case(2791)
+    q, sk, sv = _instruction(w, n)
+    s = w.spec
+    N, _, Hq, d = q.shape
+    kp, vp, table = _to_pool(w, sk, sv, seed=2792)
+    npre = -(-w.prefix_len // 16)
+    if where == "suffix":
+        table[2, npre] = kp.shape[0] + 100
+    else:
+        table[:, 3] = kp.shape[0] + 7
+    plan = fa.Plan.prefill_paged_plan(s.n_q_heads, s.n_kv_heads, s.head_dim, N, n, w.prefix_len, table.shape[1],
+                                      kp.shape[0], w.suffix_cap)
+    assert plan.info().units_per_block == 8
+    out = torch.full((N, n, Hq, d), float("nan"), device="cuda")
+    plan.prefill_paged(dev_bf16(q), dev_bf16(kp), dev_bf16(vp), dev_i32(table), dev_i32(w.suffix_len), out)
+    torch.cuda.synchronize()
+    assert plan.device_error() & 4
+    o = out.cpu().numpy().reshape(N * n, Hq, d)
+    assert np.all(np.isfinite(o))
+    if where == "suffix":
+        ref, _ = _reference(w, n, q, sk, sv)
+        rows = [t for t in range(N * n) if t // n != 2]
+        gates.assert_gates(o[rows], ref[rows], what="tiled paged, other branches exact")
+
+
 def _to_pool(w, sk, sv, seed, spare=5):
     """The prefix and each branch's suffix buffer (instruction tokens included) in a page pool of
     16-token pages whose ids are a seeded permutation: the prefix pages are shared by every
