@@ -512,10 +512,11 @@ fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t 
     int cus = 0;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device)) != hipSuccess)
         return bail(hip_fail(e, "hipDeviceGetAttribute"));
-    // The tiled kernel when each KV head has at least eight 32-row units (one block's worth);
-    // fewer rows than that leave most of a block's waves idle there, and the partial kernel's
+    // The tiled kernel when each KV head has at least one block's worth of units (eight of 32
+    // rows); fewer rows than that leave most of a block's waves idle there, and the partial kernel's
     // prefill instantiation, which spreads each unit's keys over four waves, is faster.
-    if (p->d == 128 && S * G >= 8 * 32) {
+    const int tile_rows = fka::prefill_tiles_unit_rows(), tile_waves = fka::prefill_tiles_waves();
+    if (p->d == 128 && S * G >= (int64_t)tile_waves * tile_rows) {
         // The tiled kernel: units of 32 consecutive rows of a KV head, eight per block (one per
         // wave) over one range of prefix tiles; R ranges fill the device, and the last range's
         // share is shortened by the suffix keys it also reads, taken as the instruction itself
@@ -524,8 +525,8 @@ fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t 
         const int per_cu = fka::prefill_tiles_blocks_per_cu(lay.paged);
         if (per_cu <= 0) return bail(fail(FKA_ERR_HIP, "occupancy query of the prefill kernel failed"));
         const int64_t rows_head = S * G;
-        const int32_t U = (int32_t)ceil_div(rows_head, 32);
-        const int32_t UG = ceil_div(U, 8);
+        const int32_t U = (int32_t)ceil_div(rows_head, tile_rows);
+        const int32_t UG = ceil_div(U, tile_waves);
         const int32_t PT = ceil_div(Lp, 64);
         const int64_t base = (int64_t)p->Hkv * UG;
         const int64_t want = blocks > 0 ? blocks : (int64_t)cus * per_cu;
@@ -542,8 +543,8 @@ fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t 
         p->tile_reserve = (int32_t)std::min<int64_t>(ceil_div(n, 32), PT / (2 * R));
         for (int32_t u = 0; u < U; ++u) {
             fka::UnitRec r{};
-            r.seq0 = (int32_t)(((int64_t)u * 32) / G);
-            r.nseq = (int32_t)((std::min<int64_t>(rows_head, (int64_t)u * 32 + 32) - 1) / G) - r.seq0 + 1;
+            r.seq0 = (int32_t)(((int64_t)u * tile_rows) / G);
+            r.nseq = (int32_t)((std::min<int64_t>(rows_head, (int64_t)u * tile_rows + tile_rows) - 1) / G) - r.seq0 + 1;
             r.plen = Lp;
             p->units.push_back(r);
         }
@@ -551,9 +552,9 @@ fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t 
         p->static_split = false;
         p->n_items = U * p->Hkv;
         p->slot_rows = (int32_t)(S * p->Hq);
-        p->row_tiles = 2;
-        p->waves = 8;
-        p->prefill_groups = 8;
+        p->row_tiles = tile_rows / 16;
+        p->waves = tile_waves;
+        p->prefill_groups = tile_waves;
         p->n_blocks = (int32_t)(base * R);
         p->rounds = 1;
         p->n_slots = (int32_t)R;

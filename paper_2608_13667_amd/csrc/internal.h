@@ -285,7 +285,10 @@ int prefill_max_rows(int head_dim, int group);
 hipError_t launch_prefill(const AttnArgs &a, int n_blocks, int head_dim, int row_tiles, hipStream_t s);
 int prefill_blocks_per_cu(int head_dim, int row_tiles, bool paged);
 hipError_t launch_merge(const MergeArgs &a, int head_dim, hipStream_t s);
-// The tiled instruction prefill (head_dim 128): resident blocks per compute unit, and the launch.
+// The tiled instruction prefill (head_dim 128): query rows per unit (one wave each), waves (and
+// so units) per block, resident blocks per compute unit, and the launch.
+int prefill_tiles_unit_rows();
+int prefill_tiles_waves();
 int prefill_tiles_blocks_per_cu(bool paged);
 hipError_t launch_prefill_tiles(const PrefillArgs &a, int n_blocks, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_seqs, hipStream_t s);

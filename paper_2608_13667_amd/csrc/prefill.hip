@@ -739,6 +739,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
 
 }  // namespace
 
+int prefill_tiles_unit_rows() { return 32; }
+int prefill_tiles_waves() { return NW; }
+
 int prefill_tiles_blocks_per_cu(bool paged)
 {
     int n = 0;
