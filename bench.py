@@ -197,9 +197,10 @@ class Bench:
             total += self.kvb["prefix"] + (sl0 + extra) * self.per_tok
         return total
 
-    def partial_kernel(self, plan):
+    def partial_kernel(self, plan, step_s):
         """Average duration of the partial-attention kernel alone (its launches replayed as one graph on
-        the stream they run on), as the suffix lengths of the first step leave it."""
+        the stream they run on), as the suffix lengths of the first step leave it.  step_s: the
+        measured step time, which sizes the trials."""
         torch = self.torch
         info = plan.info()
         d = self.spec.head_dim
@@ -214,9 +215,10 @@ class Bench:
                 else:
                     plan.partials(r["q"], r["prefix_k"], r["prefix_v"], r["suffix_k"], r["suffix_v"], r["suffix_len"],
                                   po, pl)
-        # at least 60 launches per trial and the median of 5 trials: the device's clock settles over
-        # a few milliseconds of back-to-back launches, which 20 launches of the 128k workload do not span
-        kp = max(60, min(200, 4 * self.R))
+        # at least 60 launches and about 20 ms of them per trial, and the median of 5 trials: the
+        # device's clock settles over a few milliseconds of back-to-back launches (20 launches of the
+        # 128k workload, or 200 of the tiny one, do not span that)
+        kp = max(60, min(4000, int(0.02 / max(step_s, 1e-6))))
         secs = self.timed(part, kp, warmup_body=lambda: part(10), trials=5)
         return float(np.median(secs)) / kp
 
@@ -230,7 +232,7 @@ class Bench:
         med = float(np.median(secs))
         alg = self.step_bytes(n_steps)
         gbps = alg / med / 1e9
-        k_secs = self.partial_kernel(plan)
+        k_secs = self.partial_kernel(plan, med / n_steps)
         k_gbps = self.kvb["total"] / k_secs / 1e9
         rec = {"steps_per_s": n_steps / med, "us_per_step": med / n_steps * 1e6,
                "trials_us_per_step": [s / n_steps * 1e6 for s in secs], "steps": n_steps, "warmup": warmup,
