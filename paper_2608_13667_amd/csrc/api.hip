@@ -518,16 +518,17 @@ fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t 
     const int tile_rows = fka::prefill_tiles_unit_rows(), tile_waves = fka::prefill_tiles_waves();
     if (p->d == 128 && S * G >= (int64_t)tile_waves * tile_rows) {
         // The tiled kernel: units of 32 consecutive rows of a KV head, eight per block (one per
-        // wave) over one range of prefix tiles; R ranges fill the device, and the last range's
-        // share is shortened by the suffix keys it also reads, taken as the instruction itself
-        // (the branches' suffixes are empty at the fork): a 32-key suffix tile, read without
-        // prefetch, is counted as one 64-key prefix tile.
+        // wave) over one range of whole 64-key prefix tiles; R ranges fill the device, and the
+        // last range's share is shortened by the keys it also reads per wave: the prefix's last
+        // Lp mod 64 and the suffix keys, taken as the instruction itself (the branches' suffixes
+        // are empty at the fork); a 32-key tile, read without prefetch, is counted as one 64-key
+        // prefix tile.
         const int per_cu = fka::prefill_tiles_blocks_per_cu(lay.paged);
         if (per_cu <= 0) return bail(fail(FKA_ERR_HIP, "occupancy query of the prefill kernel failed"));
         const int64_t rows_head = S * G;
         const int32_t U = (int32_t)ceil_div(rows_head, tile_rows);
         const int32_t UG = ceil_div(U, tile_waves);
-        const int32_t PT = ceil_div(Lp, 64);
+        const int32_t PT = Lp / 64;  // whole tiles; the last range reads the rest per wave
         const int64_t base = (int64_t)p->Hkv * UG;
         const int64_t want = blocks > 0 ? blocks : (int64_t)cus * per_cu;
         int64_t R = std::max<int64_t>(1, want / base);
@@ -540,7 +541,7 @@ fka_status create_prefill(const fka_heads *heads, int32_t N, int32_t n, int32_t 
         p->tile_unit_groups = UG;
         p->tile_ranges = (int32_t)R;
         p->tile_prefix = PT;
-        p->tile_reserve = (int32_t)std::min<int64_t>(ceil_div(n, 32), PT / (2 * R));
+        p->tile_reserve = (int32_t)std::min<int64_t>(ceil_div(n, 32) + (Lp % 64 != 0), PT / (2 * R));
         for (int32_t u = 0; u < U; ++u) {
             fka::UnitRec r{};
             r.seq0 = (int32_t)(((int64_t)u * tile_rows) / G);

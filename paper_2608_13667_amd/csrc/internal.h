@@ -238,8 +238,8 @@ struct ScatterArgs {
 // unit group k = (vb / Hkv) mod unit_groups (units [floor(k U / UG), floor((k + 1) U / UG)), at
 // most eight, one per wave) and prefix range
 // vb / (Hkv unit_groups) of `ranges`, range r covering prefix tiles (64 keys) [floor(r T / R),
-// floor((r + 1) T / R)) of T = prefix_tiles + tail_reserve, clamped to the prefix; the last range
-// also reads the suffix keys.  Part r of output row (s, h) is written at
+// floor((r + 1) T / R)) of T = prefix_tiles + tail_reserve, clamped to the whole tiles; the last
+// range also reads the prefix keys past them (Lp mod 64) and the suffix keys.  Part r of output row (s, h) is written at
 // part_o[(r S Hq + s Hq + h) d] and part_lse[r S Hq + s Hq + h].
 struct PrefillArgs {
     const uint16_t *q;                    // [S][Hq][d]
@@ -259,8 +259,8 @@ struct PrefillArgs {
     int32_t n_units;       // 32-row units per KV head
     int32_t unit_groups;   // ceil(n_units / 8)
     int32_t ranges;        // R
-    int32_t prefix_tiles;  // ceil(Lp / 64)
-    int32_t tail_reserve;  // tiles of the balance given to the last range's suffix keys
+    int32_t prefix_tiles;  // floor(Lp / 64): whole 64-key tiles
+    int32_t tail_reserve;  // tiles of the balance given to the last range's per-wave keys
     float scale_log2;      // softmax scale * log2(e)
 };
 

@@ -457,7 +457,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
             }
         });
     };
-    auto sm = [&](const f32x4 (&sc)[4][2], int tile, bf16x8 (&ph)[2][2], bf16x8 (&pl)[2][2]) {
+    // (every tile here is whole: no key mask, which would make the compiler copy the scores
+    // into the masked path's registers, 32 moves per tile)
+    auto sm = [&](const f32x4 (&sc)[4][2], bf16x8 (&ph)[2][2], bf16x8 (&pl)[2][2]) {
         xdl_result_wait();
         float x[2][4][4];
 #pragma unroll
@@ -466,16 +468,6 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
             for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) x[t][mi][j] = sc[mi][t][j];
-        const int valid = Lp - tile * KT;  // keys of this tile that exist (may exceed 64)
-        if (__builtin_expect(valid < KT, 0)) {
-            const int v4 = valid - 4 * (opaque_lane_id() >> 4);
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) x[t][mi][j] = (16 * mi + j < v4) ? x[t][mi][j] : -INFINITY;
-        }
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             row_max(nm4_t{}, t, x[t]);
@@ -525,13 +517,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
                 if (i < ntile) qk(so_t{}, sc);
                 __builtin_amdgcn_s_setprio(0);
             } else {
-                if (i > 0) sm(sc, t0 + i - 1, ph, pl);
+                if (i > 0) sm(sc, ph, pl);
             }
         }
         lds_barrier();
         if (active) {
             if constexpr (LEAD) {
-                if (i < ntile) sm(sc, t0 + i, ph, pl);
+                if (i < ntile) sm(sc, ph, pl);
             } else {
                 __builtin_amdgcn_s_setprio(1);
                 if (i > 0) pv_tile(sop_t{}, ph, pl);
@@ -557,7 +549,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
             run(std::false_type{});
     }
 
-    // ---- suffix keys (last range only): per wave, branch by branch of the unit's rows
+    // ---- keys outside the whole prefix tiles (last range only), per wave: the prefix's last
+    // Lp mod 64 keys (every row reads them), then the suffix keys branch by branch of the unit's
+    // rows (the waves of a block hold different branches)
     if (r == R - 1) {
         lds_barrier();  // every wave is done with the stage buffers (no DMA in flight: all waited)
         if (active) {
@@ -585,90 +579,70 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
             const char *const sk = reinterpret_cast<const char *>(PAGED ? a.k_pool : a.suffix_k);
             const char *const sv = reinterpret_cast<const char *>(PAGED ? a.v_pool : a.suffix_v);
             const int pre_pages = (Lp + kPageSize - 1) / kPageSize;
-            for (int b = b_lo; b <= b_hi; ++b) {
-                const int lraw = scalar_load(a.suffix_len + b);
-                const int L = min(max(lraw, 0), max_L);
-                if (L != lraw && lane == 0) atomicOr(a.err, kErrSuffixClamped);
-                const int tmax = min(n - 1, s_hi - b * n);
-                const int klim = L + tmax + 1;  // keys of b's suffix this unit reads
-                // the last key each of this lane's rows reads, or -1 for a row of another branch
-                int lim[2];
+            // One 32-key tile [p0, p0 + 32) of a key run whose 16-row groups `grp` addresses (K from
+            // srck, V from srcv), row t of this lane masked to the run's keys <= lim[t] (-1: none).
+            // CHECK: a non-finite value is zeroed for the product and the first key holding one
+            // is kept in kbad.
+            auto key_tile = [&](auto CHECKc, auto &grp, const char *srck, const char *srcv, int p0, const int (&lim)[2],
+                                int &kbad) {
+                constexpr bool CHECK = decltype(CHECKc)::value;
+                // K rows straight into registers (A operand): M tile mi = rows 16 mi + l16
+                bf16x8 ka[2][NC];
 #pragma unroll
-                for (int t = 0; t < 2; ++t) lim[t] = (srow[t] >= 0 && srow[t] / n == b) ? L + srow[t] % n : -1;
-                int kbad = 0x7fffffff;  // first key of b holding a non-finite value
-                // 16-row group resource of b's suffix positions [p, p + 16)
-                auto grp = [&](const char *src, int p) -> __amdgpu_buffer_rsrc_t {
-                    int rows_ok = max(0, min(kPageSize, klim - p));
-                    size_t off;
-                    if constexpr (PAGED) {
-                        const int32_t page = scalar_load(
-                            a.page_table + (size_t)b * a.max_pages + uni(min(pre_pages + p / kPageSize, a.max_pages - 1)));
-                        const bool bad = rows_ok > 0 && (page < 0 || page >= a.n_pool_pages);
-                        bad_page |= bad;
-                        rows_ok = bad ? 0 : rows_ok;
-                        off = rows_ok > 0 ? ((size_t)page * Hkv + g) * kPageSize * ROWB : 0;
-                    } else {
-                        off = rows_ok > 0 ? (((size_t)b * Hkv + g) * a.suffix_cap + p) * ROWB : 0;
+                for (int mi = 0; mi < 2; ++mi) {
+                    const __amdgpu_buffer_rsrc_t rk = grp(srck, p0 + 16 * mi);
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        ka[mi][c] = __builtin_bit_cast(
+                            bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, l16 * ROWB + 16 * (4 * c + q4), 0, 0));
+                }
+                // V rows into this wave's LDS area
+                {
+                    const __amdgpu_buffer_rsrc_t r0 = grp(srcv, p0), r1 = grp(srcv, p0 + 16);
+                    static_for<8>([&](auto I) {
+                        constexpr int ii = decltype(I)::value;
+                        constexpr int imm = 1024 * (ii % 4);
+                        dma16<imm>(ii < 4 ? r0 : r1,
+                                   (lds_void *)((__attribute__((address_space(3))) char *)vwp + 1024 * ii - imm),
+                                   svoff[ii & 1]);
+                    });
+                }
+                wait_vm<0>();
+                f32x4 sc[2][2];
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+                        f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) s = mfma16(ka[mi][c], qb[t][c], s);
+                        sc[mi][t] = s;
                     }
-                    return make_rsrc(src + off, rows_ok * ROWB);
-                };
-                for (int p0 = 0; p0 < klim; p0 += ST) {
-                    // K rows straight into registers (A operand): M tile mi = rows 16 mi + l16
-                    bf16x8 ka[2][NC];
+                xdl_result_wait();
+                float x[2][2][4];
+                {
+                    const int kq = p0 + 4 * (opaque_lane_id() >> 4);  // key of j = 0 in M tile 0
 #pragma unroll
-                    for (int mi = 0; mi < 2; ++mi) {
-                        const __amdgpu_buffer_rsrc_t rk = grp(sk, p0 + 16 * mi);
+                    for (int t = 0; t < 2; ++t)
 #pragma unroll
-                        for (int c = 0; c < NC; ++c)
-                            ka[mi][c] = __builtin_bit_cast(
-                                bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, l16 * ROWB + 16 * (4 * c + q4), 0, 0));
-                    }
-                    // V rows into this wave's LDS area
-                    {
-                        const __amdgpu_buffer_rsrc_t r0 = grp(sv, p0), r1 = grp(sv, p0 + 16);
-                        static_for<8>([&](auto I) {
-                            constexpr int ii = decltype(I)::value;
-                            constexpr int imm = 1024 * (ii % 4);
-                            dma16<imm>(ii < 4 ? r0 : r1,
-                                       (lds_void *)((__attribute__((address_space(3))) char *)vwp + 1024 * ii - imm),
-                                       svoff[ii & 1]);
-                        });
-                    }
-                    wait_vm<0>();
-                    f32x4 sc[2][2];
+                        for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-                    for (int mi = 0; mi < 2; ++mi)
+                            for (int j = 0; j < 4; ++j)
+                                x[t][mi][j] = (kq + 16 * mi + j <= lim[t]) ? sc[mi][t][j] : -INFINITY;
+                }
+                bf16x8 ph[2][1], pl[2][1];
+                softmax(std::integral_constant<int, 2>{}, x, ph, pl);
+                vtr_t vr[NE][2];
 #pragma unroll
-                        for (int t = 0; t < 2; ++t) {
-                            f32x4 s = {0.f, 0.f, 0.f, 0.f};
+                for (int e = 0; e < NE; ++e) {
+                    const uint32_t ad = vaddr[e] - (lds0 + V_LDS) + vw;
+                    vr[e][0] = ds_read_tr16<0>(ad);
+                    vr[e][1] = ds_read_tr16<16 * ROWB>(ad);
+                }
+                lds_wait();
 #pragma unroll
-                            for (int c = 0; c < NC; ++c) s = mfma16(ka[mi][c], qb[t][c], s);
-                            sc[mi][t] = s;
-                        }
-                    xdl_result_wait();
-                    float x[2][2][4];
-                    {
-                        const int kq = p0 + 4 * (opaque_lane_id() >> 4);  // key of j = 0 in M tile 0
-#pragma unroll
-                        for (int t = 0; t < 2; ++t)
-#pragma unroll
-                            for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-                                for (int j = 0; j < 4; ++j)
-                                    x[t][mi][j] = (kq + 16 * mi + j <= lim[t]) ? sc[mi][t][j] : -INFINITY;
-                    }
-                    bf16x8 ph[2][1], pl[2][1];
-                    softmax(std::integral_constant<int, 2>{}, x, ph, pl);
-                    vtr_t vr[NE][2];
-#pragma unroll
-                    for (int e = 0; e < NE; ++e) {
-                        const uint32_t ad = vaddr[e] - (lds0 + V_LDS) + vw;
-                        vr[e][0] = ds_read_tr16<0>(ad);
-                        vr[e][1] = ds_read_tr16<16 * ROWB>(ad);
-                    }
-                    lds_wait();
-#pragma unroll
-                    for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(vr[e][0]), "+v"(vr[e][1]));
+                for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(vr[e][0]), "+v"(vr[e][1]));
+                if constexpr (CHECK) {
                     // non-finite values: zero for the product, remember the first such key
                     uint32_t bits = 0;
 #pragma unroll
@@ -702,11 +676,64 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2))) vo
                         for (int off = 1; off < 64; off <<= 1) first = min(first, __shfl_xor(first, off));
                         kbad = min(kbad, first);
                     }
-                    const bf16x8 h2[2] = {ph[0][0], ph[1][0]}, l2[2] = {pl[0][0], pl[1][0]};
-                    pv_step(vr, h2, l2);
-                    // the next tile's V overwrites this area: the transposed reads are done
-                    // (waited above) before its DMA is issued
                 }
+                const bf16x8 h2[2] = {ph[0][0], ph[1][0]}, l2[2] = {pl[0][0], pl[1][0]};
+                pv_step(vr, h2, l2);
+                // the next tile's V overwrites this area: the transposed reads are done
+                // (waited above) before its DMA is issued
+            };
+            // the prefix keys past its whole tiles: rows of KV head g, or the prefix pages (the
+            // same ids in every branch's row: branch 0's row is read)
+            const int tail0 = PT * KT, tl = Lp - tail0;
+            if (tl > 0) {
+                auto grp_pre = [&](const char *src, int p) -> __amdgpu_buffer_rsrc_t {
+                    int rows_ok = max(0, min(kPageSize, tl - p));
+                    size_t off;
+                    if constexpr (PAGED) {
+                        const int32_t page = scalar_load(a.page_table + uni(min((tail0 + p) / kPageSize, a.max_pages - 1)));
+                        const bool bad = rows_ok > 0 && (page < 0 || page >= a.n_pool_pages);
+                        bad_page |= bad;
+                        rows_ok = bad ? 0 : rows_ok;
+                        off = rows_ok > 0 ? ((size_t)page * Hkv + g) * kPageSize * ROWB : 0;
+                    } else {
+                        off = rows_ok > 0 ? ((size_t)g * Lp + tail0 + p) * ROWB : 0;
+                    }
+                    return make_rsrc(src + off, rows_ok * ROWB);
+                };
+                int lim[2];
+#pragma unroll
+                for (int t = 0; t < 2; ++t) lim[t] = srow[t] >= 0 ? tl - 1 : -1;
+                int unused = 0x7fffffff;
+                for (int p0 = 0; p0 < tl; p0 += ST) key_tile(std::false_type{}, grp_pre, pk, pv, p0, lim, unused);
+            }
+            for (int b = b_lo; b <= b_hi; ++b) {
+                const int lraw = scalar_load(a.suffix_len + b);
+                const int L = min(max(lraw, 0), max_L);
+                if (L != lraw && lane == 0) atomicOr(a.err, kErrSuffixClamped);
+                const int tmax = min(n - 1, s_hi - b * n);
+                const int klim = L + tmax + 1;  // keys of b's suffix this unit reads
+                // the last key each of this lane's rows reads, or -1 for a row of another branch
+                int lim[2];
+#pragma unroll
+                for (int t = 0; t < 2; ++t) lim[t] = (srow[t] >= 0 && srow[t] / n == b) ? L + srow[t] % n : -1;
+                int kbad = 0x7fffffff;  // first key of b holding a non-finite value
+                // 16-row group resource of b's suffix positions [p, p + 16)
+                auto grp = [&](const char *src, int p) -> __amdgpu_buffer_rsrc_t {
+                    int rows_ok = max(0, min(kPageSize, klim - p));
+                    size_t off;
+                    if constexpr (PAGED) {
+                        const int32_t page = scalar_load(
+                            a.page_table + (size_t)b * a.max_pages + uni(min(pre_pages + p / kPageSize, a.max_pages - 1)));
+                        const bool bad = rows_ok > 0 && (page < 0 || page >= a.n_pool_pages);
+                        bad_page |= bad;
+                        rows_ok = bad ? 0 : rows_ok;
+                        off = rows_ok > 0 ? ((size_t)page * Hkv + g) * kPageSize * ROWB : 0;
+                    } else {
+                        off = rows_ok > 0 ? (((size_t)b * Hkv + g) * a.suffix_cap + p) * ROWB : 0;
+                    }
+                    return make_rsrc(src + off, rows_ok * ROWB);
+                };
+                for (int p0 = 0; p0 < klim; p0 += ST) key_tile(std::true_type{}, grp, sk, sv, p0, lim, kbad);
 #pragma unroll
                 for (int t = 0; t < 2; ++t) l_run[t] = (lim[t] >= kbad) ? __builtin_nanf("") : l_run[t];
             }

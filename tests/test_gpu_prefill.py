@@ -198,12 +198,15 @@ def _check_case(fa, c):
                                  dict(head_dim=128, n_kv_heads=2, n_q_heads=8, n_branches=4, n=20, prefix_len=1500,
                                       lo=5, blocks=3, seed=2751),
                                  dict(head_dim=128, n_kv_heads=1, n_q_heads=1, n_branches=256, n=2, prefix_len=700,
-                                      lo=0, blocks=0, seed=2752)],
-                         ids=["empty-prefix", "one-range", "16-branches-per-unit"])
+                                      lo=0, blocks=0, seed=2752),
+                                 dict(head_dim=128, n_kv_heads=2, n_q_heads=8, n_branches=4, n=20, prefix_len=40, lo=5,
+                                      blocks=0, seed=2753)],
+                         ids=["empty-prefix", "one-range", "16-branches-per-unit", "prefix-under-one-tile"])
 def test_prefill_tiled_edges(fa, c):
     """The tiled kernel (at least 256 rows per KV head) with no prefix at all (the suffix keys
-    only), with an explicit grid of one prefix range, and with G = 1 and 2-token instructions of
-    256 branches, where a 32-row unit holds 16 branches (each masked to its own suffix)."""
+    only), with an explicit grid of one prefix range, with G = 1 and 2-token instructions of
+    256 branches, where a 32-row unit holds 16 branches (each masked to its own suffix), and with a
+    prefix shorter than one 64-key tile (no whole tile: every prefix key on the per-wave path)."""
     _check_case(fa, c)
 
 
@@ -281,11 +284,11 @@ def test_prefill_tiled_clamps_and_flags_a_suffix_past_the_bound(fa):
     gates.assert_lse(lse[rows], ref_lse[rows], what="tiled, other branches unaffected")
 
 
-@pytest.mark.parametrize("where", ["suffix", "prefix"])
+@pytest.mark.parametrize("where", ["suffix", "prefix", "prefix-tail"])
 def test_prefill_tiled_paged_flags_a_bad_page(fa, where):
     """The tiled kernel over the pool skips a page id outside the pool (its rows read as zeros) and
     raises flag 4: in one branch's suffix row the other branches stay exact; in the shared prefix
-    the flag is raised."""
+    (a page of a whole 64-key tile, or of the last 52 keys past them) the flag is raised."""
     w, n = _tiled_case(2791)
     q, sk, sv = _instruction(w, n)
     s = w.spec
@@ -294,8 +297,11 @@ def test_prefill_tiled_paged_flags_a_bad_page(fa, where):
     npre = -(-w.prefix_len // 16)
     if where == "suffix":
         table[2, npre] = kp.shape[0] + 100
-    else:
+    elif where == "prefix":
         table[:, 3] = kp.shape[0] + 7
+    else:
+        assert w.prefix_len % 64 == 52
+        table[:, npre - 1] = kp.shape[0] + 7
     plan = fa.Plan.prefill_paged_plan(s.n_q_heads, s.n_kv_heads, s.head_dim, N, n, w.prefix_len, table.shape[1],
                                       kp.shape[0], w.suffix_cap)
     assert plan.info().units_per_block == 8
