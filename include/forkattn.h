@@ -324,10 +324,10 @@ fka_status fka_scatter_pages(const void *k_src, const void *v_src, int32_t len, 
  * suffix up to and including its own position (suffix positions [0, suffix_len[b] + t]).
  * With head_dim 128 and at least 256 query rows (N x n_tokens x G) per KV head, a tiled kernel
  * runs: each KV head's rows are cut into units of 32 consecutive rows, a block of eight waves
- * takes eight units (one each) over one range of 64-key prefix tiles, which it loads once into
- * LDS for all eight, and the blocks of one KV head run on one XCD (the KV head varies fastest in
- * the grid) so that its ranges come from HBM once; the block of the last range also reads the
- * suffix keys.  Otherwise the plan splits the tokens into units of consecutive tokens (at most
+ * takes eight units (one each) over one range of whole 64-key prefix tiles, which it loads once
+ * into LDS for all eight, and the blocks of one KV head run on one XCD (the KV head varies
+ * fastest in the grid) so that its ranges come from HBM once; the block of the last range also
+ * reads the prefix's last prefix_len mod 64 keys and the suffix keys.  Otherwise the plan splits the tokens into units of consecutive tokens (at most
  * 32 query rows per KV head each for head_dim 128 with G <= 32, else 64), all streaming the same
  * prefix on the partial kernel, the blocks that read one prefix range for different units
  * together on one XCD (block vb holds work item vb mod n_items).  Then the merge stage combines
